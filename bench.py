@@ -1,0 +1,304 @@
+"""Benchmark of the UltraMem memory-layer forward on one MI355X.
+
+A step is one whole forward of the layer (axis scoring, per-axis top-k, grid top-m, gather-sum)
+over one batch of the 20.07M-slot decode workload: 32 tokens, 2 heads, dk 128, 4480 x 4480
+keys, a 20,070,400 x 512 bf16 value table (20.55 GB), k = m = 32.  Inputs are resident in HBM
+before timing starts.  Successive steps take distinct query batches from a rotating set large
+enough (over 1 GiB of distinct value rows) that the gathered rows are not cache-resident.
+
+Prints one JSON line.  Besides the headline it carries the roofline of the dominant kernel
+(per-launch durations from HIP events recorded on the launch stream), the value-gather
+bandwidth, a decode batch sweep, and the CPU oracle's throughput on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+FP32_PEAK_TFLOPS = 157.3       # MI355X dense fp32 matrix
+METRIC = "memory-layer tokens/sec + value-gather HBM GB/s (% of peak), 20M-slot decode"
+KERNEL_SOURCES = {
+    "axis_scores_kernel": "score.hip",
+    "select_kernel": "select.hip",
+    "gather_kernel": "gather.hip",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--batches", type=int, default=512, help="distinct query batches rotated")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--graph", action="store_true", help="replay the steps from a HIP graph")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------- byte and flop accounting
+
+def kernel_work(cfg, T):
+    """Algorithmic bytes (and flops) per launch of each kernel at T tokens."""
+    H, n, dk, k, m = cfg.heads, cfg.n_keys, cfg.dk, cfg.topk, cfg.topm
+    keys = 2 * H * n * dk * 4
+    q = 2 * T * H * dk * 4
+    sel = 2 * T * H * n * 4
+    sel_out = T * H * m * 8
+    rows = T * cfg.bag * cfg.dv * cfg.vbytes
+    return {
+        "axis_scores_kernel": dict(bytes=keys + q + sel, flops=2 * 2 * T * H * n * dk),
+        "select_kernel": dict(bytes=sel + sel_out, flops=0),
+        "gather_kernel": dict(bytes=rows + T * cfg.bag * 8 + T * cfg.expand * cfg.dv * 4,
+                              flops=2 * T * cfg.bag * cfg.dv, row_bytes=rows),
+    }
+
+
+def source_digest(name):
+    path = os.path.join(ROOT, "paper_2411_12364_amd", "csrc", KERNEL_SOURCES[name])
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(name, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken on the
+    kernel source as it is now; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get(workload, {}).get(name)
+    if not rec or rec.get("source_sha256_16") != source_digest(name):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+# ---------------------------------------------------------------- GPU measurement
+
+class Runner:
+    def __init__(self, cfg, batches, values=None):
+        import torch
+
+        import paper_2411_12364_amd as U
+        from synth import device as SD
+        self.U, self.torch, self.cfg = U, torch, cfg
+        t0 = time.time()
+        self.dl = SD.make_layer(cfg, batches=batches, values=values)
+        torch.cuda.synchronize()
+        log(f"inputs for {cfg.name} T={cfg.T} ({batches} query batches) ready in {time.time() - t0:.1f}s")
+        self.desc = self._desc()
+        T = cfg.T
+        st, nbytes = U.umem_workspace_size(self.desc, T)
+        U.check(st)
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+        self.out = torch.empty((T, cfg.dv), dtype=torch.float32, device="cuda")
+        self.idx = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda")
+        self.w = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.float32, device="cuda")
+        self.sel = torch.empty((2, T, cfg.heads, cfg.n_keys), dtype=torch.float32, device="cuda")
+        self.R = batches
+
+    def _desc(self):
+        c, d = self.cfg, self.U.umem_desc()
+        d.heads, d.dk, d.n_keys, d.rank = c.heads, c.dk, c.n_keys, c.rank
+        d.topk, d.topm, d.grid, d.weight = c.topk, c.topm, c.grid, c.weight
+        d.n_values, d.dv, d.vdtype, d.expand = c.n_values, c.dv, c.vdtype, c.expand
+        d.dv_virt, d.d_out, d.reserved = c.dv_virt, c.d_out, 0
+        return d
+
+    def forward(self, b):
+        U, dl, c = self.U, self.dl, self.cfg
+        st = U.umem_forward(self.desc, c.T, dl.q_row[b], dl.q_col[b], dl.k_row, dl.k_col, dl.core,
+                            dl.values, dl.perm, dl.w_proj, dl.w_out, self.out, self.idx, self.w,
+                            self.ws, self.ws.numel())
+        if st:
+            U.check(st, "umem_forward")
+
+    def stages(self, b, ev):
+        """The same kernels through the per-stage entry points, with an event after each."""
+        U, dl, c = self.U, self.dl, self.cfg
+        ev[0].record()
+        U.check(U.umem_axis_scores(self.desc, c.T, dl.q_row[b], dl.q_col[b], dl.k_row, dl.k_col,
+                                   dl.core, self.sel))
+        ev[1].record()
+        U.check(U.umem_select(self.desc, c.T, self.sel, dl.q_row[b], dl.q_col[b], dl.k_row,
+                              dl.k_col, dl.core, self.idx, self.w, None))
+        ev[2].record()
+        U.check(U.umem_gather_sum(c.n_values, c.dv, c.vdtype, dl.values, c.T, c.bag, self.idx,
+                                  self.w, dl.perm, c.expand, self.out))
+        ev[3].record()
+
+    def time_forward(self, steps, warmup, graph=False):
+        torch = self.torch
+        for s in range(warmup):
+            self.forward(s % self.R)
+        torch.cuda.synchronize()
+        if graph:
+            g = torch.cuda.CUDAGraph()
+            n_cap = min(self.R, steps)
+            with torch.cuda.graph(g):
+                for s in range(n_cap):
+                    self.forward(s % self.R)
+            g.replay()
+            torch.cuda.synchronize()
+            reps = max(1, steps // n_cap)
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                g.replay()
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0), reps * n_cap
+        t0 = time.perf_counter()
+        for s in range(steps):
+            self.forward(s % self.R)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0, steps
+
+    def time_stages(self, steps, warmup):
+        torch = self.torch
+        for s in range(warmup):
+            self.stages(s % self.R, [torch.cuda.Event(enable_timing=True) for _ in range(4)])
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        for s in range(steps):
+            self.stages(s % self.R, evs[s])
+        torch.cuda.synchronize()
+        names = ["axis_scores_kernel", "select_kernel", "gather_kernel"]
+        avg = {}
+        for i, nm in enumerate(names):
+            avg[nm] = sum(e[i].elapsed_time(e[i + 1]) for e in evs) / steps * 1e3   # us
+        return avg
+
+
+def roofline_for(cfg, T, name, avg_us, workload):
+    work = kernel_work(cfg, T)[name]
+    if name == "axis_scores_kernel" and work["flops"] / work["bytes"] > FP32_PEAK_TFLOPS * 1e3 / HBM_PEAK_GBS:
+        achieved = work["flops"] / (avg_us * 1e-6) / 1e12
+        return dict(kernel=name, bound="mfma", achieved=round(achieved, 3), peak=FP32_PEAK_TFLOPS,
+                    unit="TFLOP/s", frac=round(achieved / FP32_PEAK_TFLOPS, 4),
+                    traffic=measured_traffic(name, workload), avg_us=round(avg_us, 3))
+    achieved = work["bytes"] / (avg_us * 1e-6) / 1e9
+    return dict(kernel=name, bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS,
+                unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4),
+                traffic=measured_traffic(name, workload), avg_us=round(avg_us, 3),
+                algorithmic_bytes=work["bytes"])
+
+
+def distinct_batches(T, row_bytes_per_token):
+    """Enough query batches that one rotation touches over 1 GiB of value rows (capped)."""
+    return int(min(4096, max(1, math.ceil((1 << 30) / (T * row_bytes_per_token)))))
+
+
+def sweep(base_cfg, values, steps=300, warmup=30):
+    res = []
+    for T in (1, 4, 16, 64, 256, 1024):
+        cfg = base_cfg.with_tokens(T)
+        R = distinct_batches(T, cfg.bag * cfg.dv * cfg.vbytes)
+        r = Runner(cfg, R, values)
+        secs, n = r.time_forward(steps, warmup)
+        st = r.time_stages(steps, warmup)
+        g = kernel_work(cfg, T)["gather_kernel"]
+        res.append(dict(tokens=T, query_batches=R, ms_per_step=round(secs / n * 1e3, 4),
+                        tokens_per_s=round(T * n / secs, 1),
+                        kernel_us={k: round(v, 3) for k, v in st.items()},
+                        gather_GBps=round(g["row_bytes"] / (st["gather_kernel"] * 1e-6) / 1e9, 1),
+                        gather_frac=round(g["row_bytes"] / (st["gather_kernel"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)))
+        log(f"sweep T={T}: {res[-1]}")
+        del r
+        import torch
+        torch.cuda.empty_cache()
+    return res
+
+
+# ---------------------------------------------------------------- CPU oracle baseline
+
+def cpu_baseline(cfg, seconds):
+    """The oracle (unchanged) on the host, single-threaded, on successive 32-token batches of the
+    same workload until ``seconds`` of CPU time have elapsed.  Value rows are drawn before the
+    timed call (a first untimed call learns which rows are gathered), so input generation is
+    excluded."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle.umem_oracle as O
+    from synth import configs as CF
+
+    kr, kc = CF.keys(cfg)
+    tokens, spent, b = 0, 0.0, 0
+    with threadpool_limits(limits=1):
+        while spent < seconds and b < 400:
+            qr, qc = CF.queries(cfg, batch=1000 + b)
+            sel = O.score_topk(qr, qc, kr, kc, cfg.topk, cfg.topm, cfg.grid, cfg.weight)
+            rows = np.unique(sel["idx"].reshape(-1))
+            table = dict(zip(rows.tolist(), CF.value_rows_f32(cfg, rows)))
+            fetch = lambda r: np.stack([table[int(x)] for x in r])
+            t0 = time.perf_counter()
+            O.forward(qr, qc, kr, kc, fetch, cfg.topk, cfg.topm, cfg.grid, cfg.weight)
+            spent += time.perf_counter() - t0
+            tokens += cfg.T
+            b += 1
+    return dict(value=round(tokens / spent, 2), unit="tokens/s", cores=1, kind="oracle",
+                sample=f"{b} batches x {cfg.T} tokens of {cfg.name} (fp64 numpy oracle, 1 thread, "
+                       f"{spent:.1f} s)")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the memory layer's "
+              "multi-GPU sharding is not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from synth import configs as CF
+    cfg = CF.C3
+    torch.cuda.set_device(0)
+    r = Runner(cfg, args.batches)
+    secs, n = r.time_forward(args.steps, args.warmup, graph=args.graph)
+    ms = secs / n * 1e3
+    log(f"forward: {n} steps in {secs:.3f}s = {ms * 1e3:.2f} us/step")
+    stage_us = r.time_stages(min(args.steps, 1000), args.warmup)
+    log(f"per-kernel (events): {stage_us}")
+    dominant = max(stage_us, key=stage_us.get)
+    work = kernel_work(cfg, cfg.T)
+    g_us = stage_us["gather_kernel"]
+    gather = dict(row_bytes_per_launch=work["gather_kernel"]["row_bytes"], avg_us=round(g_us, 3),
+                  GBps=round(work["gather_kernel"]["row_bytes"] / (g_us * 1e-6) / 1e9, 1))
+    gather["frac_of_peak"] = round(gather["GBps"] / HBM_PEAK_GBS, 4)
+    values = r.dl.values
+    del r
+    sw = None if args.no_sweep else sweep(cfg, values)
+    del values
+    torch.cuda.empty_cache()
+    cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, args.cpu_seconds)
+    line = {
+        "metric": METRIC, "value": round(cfg.T * n / secs, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": n, "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "tokens": cfg.T, "heads": cfg.heads, "dk": cfg.dk,
+                   "n_keys": cfg.n_keys, "slots": cfg.n_slots, "dv": cfg.dv, "values": "bf16",
+                   "topk": cfg.topk, "topm": cfg.topm, "query_batches": args.batches,
+                   "graph": bool(args.graph)},
+        "roofline": roofline_for(cfg, cfg.T, dominant, stage_us[dominant], cfg.name),
+        "kernel_us": {k: round(v, 3) for k, v in stage_us.items()},
+        "gather": gather,
+        "batch_sweep": sw,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

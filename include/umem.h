@@ -1,0 +1,162 @@
+/*
+ * umem.h -- C ABI of the UltraMem memory-layer forward on AMD Instinct MI355X (gfx950).
+ *
+ * The layer is the ultra-sparse memory layer of "Ultra-Sparse Memory Network" (Huang et al.):
+ *   a1  axis scores        Sec. 3.1 eq. (2); Sec. 3.2 TDQKR eq. (4)
+ *   a2  rank-1 reduction   Sec. 3.2 TDQKR eqs. (6)-(9), (11)  (Tucker grid only)
+ *   a3  per-axis top-k     eq. (2) sigma_TopM; eqs. (8), (9) I_TopM
+ *   a4  grid scores        eq. (3) (additive); eq. (10) (Tucker core, exact on the candidates)
+ *   a5  global top-m       eq. (3) / eq. (10); weights raw (Sec. 3.2 Trick 1) or SoftMax (eq. (3))
+ *   a6  IVE address map    Sec. 3.2 IVE eqs. (13), (14)
+ *   a7  gather-sum         eq. (1) o = V^T s; eq. (15) per virtual block; heads add (Sec. 3.1)
+ *   a8  projection         eq. (15) sum_p W_p^T (.); Sec. 3.2 Trick 6 output linear
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller, dense and row-major, unless
+ *     stated otherwise.  The library never allocates, frees or synchronises; it only enqueues
+ *     kernels on `stream` (NULL = the default stream).  Scratch memory comes from the caller
+ *     (`ws`, sized by umem_workspace_size).
+ *   - Calls are asynchronous.  The returned status covers argument validation and launch
+ *     errors only.  On any error nothing is enqueued and no output is written.  Device-side
+ *     faults (e.g. an index out of range in a caller-supplied bag) are not detected.
+ *   - Ties: every selection orders by (score desc, index asc) -- the per-axis key index, or the
+ *     logical flat index i*n + j on the grid; -0.0 equals +0.0; NaN ranks below -inf.
+ *     Selections are returned sorted in that order.
+ *   - Indices are int32 (n*n < 2^31); byte offsets into the value table are 64-bit.
+ *   - Alignment: q/k/core 16 bytes, values and fp32 outputs 16 bytes, other arrays 4 bytes.
+ *   - T == 0 is a no-op once the descriptor is valid.
+ *   - Functions are reentrant; calls on one stream run in order.
+ */
+#ifndef UMEM_H
+#define UMEM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define UMEM_API __attribute__((visibility("default")))
+
+typedef enum umem_status {
+  UMEM_OK = 0,
+  UMEM_ERR_INVALID_ARG = -1, /* a null pointer, a bad size or a misaligned buffer */
+  UMEM_ERR_UNSUPPORTED = -2, /* valid for the paper, beyond this library's limits (below) */
+  UMEM_ERR_WORKSPACE = -3,   /* ws too small or misaligned */
+  UMEM_ERR_HIP = -4          /* a HIP launch failed */
+} umem_status;
+
+enum { UMEM_F32 = 0, UMEM_BF16 = 1 };             /* value-table element type */
+enum { UMEM_GRID_ADD = 0, UMEM_GRID_TUCKER = 1 }; /* eq. (3) / eq. (10) */
+enum { UMEM_W_RAW = 0, UMEM_W_SOFTMAX = 1 };      /* Trick 1 (raw scores) / eq. (3) SoftMax */
+
+/* Shape of one memory layer.
+ * Requirements (UMEM_ERR_INVALID_ARG otherwise): every count >= 1; dk % rank == 0;
+ *   rank == 1 for UMEM_GRID_ADD; topk <= n_keys; topm <= topk^2; expand a perfect square with
+ *   n_values * expand == n_keys^2; dv_virt > 0 when expand > 1; reserved == 0.
+ * Limits of this library (UMEM_ERR_UNSUPPORTED beyond them): max(n_keys, topk^2) <= 12288;
+ *   topk <= 110; topm <= 256; rank <= 4; (dk / rank) % 4 == 0; dk <= 1024; heads <= 64;
+ *   heads * topm <= 2048; expand <= 64; a value row (dv * element size) of 16 * 2^j <= 1024
+ *   bytes or a multiple of 1024 up to 8192 bytes; T <= 2^20. */
+typedef struct umem_desc {
+  int32_t heads;    /* H: key sets (each with its own keys and core) sharing one value table */
+  int32_t dk;       /* query/key dimension per axis per head */
+  int32_t n_keys;   /* n keys per axis; the logical grid has N = n*n slots */
+  int32_t rank;     /* Tucker rank r: dk is read as r contiguous slices of dk/r (eq. (4)) */
+  int32_t topk;     /* k: per-axis top-k */
+  int32_t topm;     /* m: global top-m per head; each token's bag holds heads*topm slots */
+  int32_t grid;     /* UMEM_GRID_ADD or UMEM_GRID_TUCKER */
+  int32_t weight;   /* UMEM_W_RAW or UMEM_W_SOFTMAX */
+  int64_t n_values; /* N_p physical value rows (= N / expand) */
+  int32_t dv;       /* physical value dimension */
+  int32_t vdtype;   /* UMEM_F32 or UMEM_BF16 */
+  int32_t expand;   /* E: implicit value expansion (1 = none) */
+  int32_t dv_virt;  /* D'v: IVE projector width (0 = no projection; required when expand > 1) */
+  int32_t d_out;    /* output linear width (0 = none) */
+  int32_t reserved; /* must be 0 */
+} umem_desc;
+
+/* Bytes of scratch `ws` that umem_score_topk / umem_forward need for T tokens (a multiple of
+ * 256; pass ws aligned to 256 bytes).  Writes 0 to *bytes and returns an error for an invalid
+ * descriptor. */
+UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_t* bytes);
+
+/* a1 + a2: per-axis selection scores -- eq. (2) for the additive grid; u^T S_row and
+ * t^T S_col of eqs. (6), (8), (9) for the Tucker grid, with (u, t) the leading singular pair of
+ * each head's core (eq. (11)), the sign fixed so that u's largest-magnitude component is
+ * positive and t = C^T u / sigma_1.
+ *   q_row, q_col  fp32 [T, H, dk]  the two queries; may be the same pointer (Trick 5)
+ *   k_row, k_col  fp32 [H, n, dk]  keys; with rank r each dk row holds r contiguous slices
+ *   core          fp32 [H, r, r]   Tucker cores (NULL for UMEM_GRID_ADD)
+ *   sel           fp32 [2, T, H, n] out: [0] row scores, [1] column scores */
+UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const float* q_row,
+                             const float* q_col, const float* k_row, const float* k_col,
+                             const float* core, float* sel, hipStream_t stream);
+
+/* a3 + a4 + a5 from selection scores: per-axis top-k, grid scores of the k*k candidates
+ * (additive eq. (3); Tucker eq. (10) with the per-slice scores recomputed exactly for the
+ * candidates, non-candidates excluded), global top-m and weights.
+ *   sel       fp32 [2, T, H, n] as written by umem_axis_scores
+ *   q_*, k_*, core  as above; read only for UMEM_GRID_TUCKER (may be NULL for ADD)
+ *   idx       int32 [T, H, m] out: logical slot i*n + j, sorted by (score desc, index asc)
+ *   w         fp32 [T, H, m] out: the weight of each slot (raw grid score, or SoftMax)
+ *   axis_idx  int32 [2, T, H, k] out, optional (NULL): per-axis top-k, sorted */
+UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* sel, const float* q_row,
+                        const float* q_col, const float* k_row, const float* k_col,
+                        const float* core, int32_t* idx, float* w, int32_t* axis_idx,
+                        hipStream_t stream);
+
+/* a1 .. a5: umem_axis_scores followed by umem_select, the scores kept in `ws`
+ * (ws_bytes >= umem_workspace_size(desc, T)). */
+UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const float* q_row,
+                            const float* q_col, const float* k_row, const float* k_col,
+                            const float* core, int32_t* idx, float* w, int32_t* axis_idx,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* a6 + a7: score-weighted gather-sum (embedding bag) of value rows -- eq. (1), eq. (15).
+ *   values  [n_values, dv] of vdtype, 16-byte aligned
+ *   idx     int32 [T, bag]: logical slots; without perm and with expand == 1 they are physical
+ *           rows (Sec. 3.1: slot (i, j) lives at row n*i + j)
+ *   w       fp32 [T, bag]
+ *   perm    int32 [expand * n_values] or NULL: the IVE shuffle (eq. (14)); slot x goes to virtual
+ *           slot v = perm[x], block p = v / n_values, physical row v % n_values
+ *   out     fp32 [T, expand, dv], 16-byte aligned: out[t, p, :] = sum over the bag entries of
+ *           block p of w * values[row, :] (fp32 accumulation; repeated rows add)
+ * Every index must be in range ([0, n_values) without perm, [0, expand*n_values) with it). */
+UMEM_API umem_status umem_gather_sum(int64_t n_values, int32_t dv, int32_t vdtype, const void* values,
+                            int32_t T, int32_t bag, const int32_t* idx, const float* w,
+                            const int32_t* perm, int32_t expand, float* out,
+                            hipStream_t stream);
+
+/* a8: y = sum_p pooled[:, p, :] W_p (eq. (15)), then y W_out (Trick 6).  bf16 operands (the
+ * fp32 pooled sums and the intermediate are rounded to bf16, nearest even), fp32 accumulation.
+ *   pooled  fp32 [T, E, dv]; w_proj bf16 bits [E, dv, dv_virt]; w_out bf16 bits [dv_virt, d_out]
+ *           or NULL; out fp32 [T, d_out] (or [T, dv_virt] without w_out)
+ *   ws      scratch for the intermediate: T * dv_virt * 4 bytes (may be NULL without w_out) */
+UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
+                         const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
+                         float* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* a1 .. a8: the whole forward of the layer for T tokens.
+ *   values, perm     as for umem_gather_sum (perm required iff expand > 1)
+ *   w_proj, w_out    as for umem_project (w_proj required iff dv_virt > 0; w_out iff d_out > 0)
+ *   out              fp32: [T, dv] without projection, else [T, d_out] (or [T, dv_virt])
+ *   idx_out, w_out_scores  optional (NULL) copies of the selection, [T, H, m] each
+ * ws_bytes >= umem_workspace_size(desc, T). */
+UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float* q_row, const float* q_col,
+                         const float* k_row, const float* k_col, const float* core,
+                         const void* values, const int32_t* perm, const uint16_t* w_proj,
+                         const uint16_t* w_out, float* out, int32_t* idx_out,
+                         float* w_out_scores, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* A static, human-readable name of a status code. */
+UMEM_API const char* umem_status_string(umem_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UMEM_H */

@@ -1,0 +1,285 @@
+// The C ABI of libumem: argument validation, workspace layout and kernel sequencing.
+// Every entry point validates everything before it enqueues anything.
+#include <stdint.h>
+
+#include "umem_internal.h"
+
+using namespace umem;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int64_t isqrt64(int64_t x) {
+  int64_t r = 0;
+  while ((r + 1) * (r + 1) <= x) ++r;
+  return r;
+}
+
+umem_status check_desc(const umem_desc* d) {
+  if (d == nullptr) return UMEM_ERR_INVALID_ARG;
+  if (d->heads < 1 || d->dk < 1 || d->n_keys < 1 || d->rank < 1 || d->topk < 1 || d->topm < 1 ||
+      d->dv < 1 || d->expand < 1 || d->n_values < 1 || d->dv_virt < 0 || d->d_out < 0)
+    return UMEM_ERR_INVALID_ARG;
+  if (d->grid != UMEM_GRID_ADD && d->grid != UMEM_GRID_TUCKER) return UMEM_ERR_INVALID_ARG;
+  if (d->weight != UMEM_W_RAW && d->weight != UMEM_W_SOFTMAX) return UMEM_ERR_INVALID_ARG;
+  if (d->vdtype != UMEM_F32 && d->vdtype != UMEM_BF16) return UMEM_ERR_INVALID_ARG;
+  if (d->reserved != 0) return UMEM_ERR_INVALID_ARG;
+  if (d->dk % d->rank != 0) return UMEM_ERR_INVALID_ARG;
+  if (d->grid == UMEM_GRID_ADD && d->rank != 1) return UMEM_ERR_INVALID_ARG;
+  if (d->topk > d->n_keys) return UMEM_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(d->topm) > static_cast<int64_t>(d->topk) * d->topk)
+    return UMEM_ERR_INVALID_ARG;
+  const int64_t e = isqrt64(d->expand);
+  if (e * e != d->expand) return UMEM_ERR_INVALID_ARG;
+  if (d->expand > 1 && d->dv_virt == 0) return UMEM_ERR_INVALID_ARG;
+  if (d->n_keys > kMaxSelect) return UMEM_ERR_UNSUPPORTED;   // also keeps n*n < 2^31
+  if (static_cast<int64_t>(d->n_keys) * d->n_keys != d->n_values * d->expand)
+    return UMEM_ERR_INVALID_ARG;
+  if (d->topk > kMaxTopK || d->topk * d->topk > kMaxSelect || d->topm > kMaxTopM)
+    return UMEM_ERR_UNSUPPORTED;
+  if (d->rank > kMaxRank || (d->dk / d->rank) % 4 != 0 || d->dk > kMaxDk) return UMEM_ERR_UNSUPPORTED;
+  if (d->heads > kMaxHeads || d->heads * d->topm > kMaxBag) return UMEM_ERR_UNSUPPORTED;
+  if (d->expand > kMaxExpand) return UMEM_ERR_UNSUPPORTED;
+  if (!gather_row_supported(d->dv, d->vdtype)) return UMEM_ERR_UNSUPPORTED;
+  return UMEM_OK;
+}
+
+umem_status check_tokens(int32_t T) {
+  if (T < 0) return UMEM_ERR_INVALID_ARG;
+  if (T > kMaxTokens) return UMEM_ERR_UNSUPPORTED;
+  return UMEM_OK;
+}
+
+umem_status check_scoring_ptrs(const umem_desc* d, const float* q_row, const float* q_col,
+                               const float* k_row, const float* k_col, const float* core) {
+  if (!q_row || !q_col || !k_row || !k_col) return UMEM_ERR_INVALID_ARG;
+  if (!aligned(q_row, 16) || !aligned(q_col, 16) || !aligned(k_row, 16) || !aligned(k_col, 16))
+    return UMEM_ERR_INVALID_ARG;
+  if (d->grid == UMEM_GRID_TUCKER && (core == nullptr || !aligned(core, 4))) return UMEM_ERR_INVALID_ARG;
+  return UMEM_OK;
+}
+
+struct Layout {
+  size_t sel, idx, w, pooled, tmp, total;
+};
+
+Layout layout(const umem_desc* d, int32_t T) {
+  Layout L{};
+  const size_t th = static_cast<size_t>(T) * d->heads;
+  size_t off = 0;
+  L.sel = off;
+  off += round_up(2 * th * d->n_keys * sizeof(float));
+  L.idx = off;
+  off += round_up(th * d->topm * sizeof(int32_t));
+  L.w = off;
+  off += round_up(th * d->topm * sizeof(float));
+  L.pooled = off;
+  if (d->dv_virt > 0 || d->d_out > 0)
+    off += round_up(static_cast<size_t>(T) * d->expand * d->dv * sizeof(float));
+  L.tmp = off;
+  if (d->dv_virt > 0 && d->d_out > 0) off += round_up(static_cast<size_t>(T) * d->dv_virt * sizeof(float));
+  L.total = off;
+  return L;
+}
+
+umem_status check_ws(const umem_desc* d, int32_t T, const void* ws, size_t ws_bytes) {
+  const Layout L = layout(d, T);
+  if (L.total > 0 && (ws == nullptr || !aligned(ws, kAlign) || ws_bytes < L.total))
+    return UMEM_ERR_WORKSPACE;
+  return UMEM_OK;
+}
+
+umem_status hip_status(hipError_t e) { return e == hipSuccess ? UMEM_OK : UMEM_ERR_HIP; }
+
+umem_status check_gather(int64_t n_values, int32_t dv, int32_t vdtype, const void* values,
+                         int32_t T, int32_t bag, const int32_t* idx, const float* w,
+                         int32_t expand, const float* out) {
+  if (n_values < 1 || dv < 1 || bag < 1 || expand < 1) return UMEM_ERR_INVALID_ARG;
+  if (vdtype != UMEM_F32 && vdtype != UMEM_BF16) return UMEM_ERR_INVALID_ARG;
+  umem_status st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  if (!values || !idx || !w || !out) return UMEM_ERR_INVALID_ARG;
+  if (!aligned(values, 16) || !aligned(out, 16) || !aligned(idx, 4) || !aligned(w, 4))
+    return UMEM_ERR_INVALID_ARG;
+  const int64_t esize = vdtype == UMEM_F32 ? 4 : 2;
+  if (n_values > (INT64_C(1) << 62) / (static_cast<int64_t>(dv) * esize)) return UMEM_ERR_INVALID_ARG;
+  if (n_values * expand > (INT64_C(1) << 31)) return UMEM_ERR_UNSUPPORTED;
+  if (bag > kMaxBag || expand > kMaxExpand) return UMEM_ERR_UNSUPPORTED;
+  if (!gather_row_supported(dv, vdtype)) return UMEM_ERR_UNSUPPORTED;
+  return UMEM_OK;
+}
+
+umem_status check_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
+                          const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
+                          const float* out, const void* ws, size_t ws_bytes) {
+  if (expand < 1 || dv < 1 || dv_virt < 0 || d_out < 0) return UMEM_ERR_INVALID_ARG;
+  umem_status st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  if (expand < 1 || dv < 1 || dv_virt < 0 || d_out < 0) return UMEM_ERR_INVALID_ARG;
+  if (!pooled || !out) return UMEM_ERR_INVALID_ARG;
+  if (w_proj == nullptr) {
+    // output linear only: [T, dv] by [dv, d_out]
+    if (expand != 1 || dv_virt != 0 || d_out == 0 || w_out == nullptr) return UMEM_ERR_INVALID_ARG;
+  } else {
+    if (dv_virt == 0) return UMEM_ERR_INVALID_ARG;
+    if ((w_out == nullptr) != (d_out == 0)) return UMEM_ERR_INVALID_ARG;
+    if (w_out != nullptr) {
+      const size_t need = static_cast<size_t>(T) * dv_virt * sizeof(float);
+      if (need > 0 && (ws == nullptr || !aligned(ws, 16) || ws_bytes < need)) return UMEM_ERR_WORKSPACE;
+    }
+  }
+  return UMEM_OK;
+}
+
+hipError_t run_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
+                       const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
+                       float* out, void* tmp, hipStream_t s) {
+  if (w_proj == nullptr)   // the output linear alone is the same GEMM with [dv, d_out] weights
+    return launch_project(T, 1, dv, d_out, 0, pooled, w_out, nullptr, out, nullptr, s);
+  return launch_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out,
+                        static_cast<float*>(tmp), s);
+}
+
+}  // namespace
+
+extern "C" {
+
+UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_t* bytes) {
+  if (bytes == nullptr) return UMEM_ERR_INVALID_ARG;
+  *bytes = 0;
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK) return st;
+  *bytes = layout(desc, T).total;
+  return UMEM_OK;
+}
+
+UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const float* q_row,
+                                      const float* q_col, const float* k_row, const float* k_col,
+                                      const float* core, float* sel, hipStream_t stream) {
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  if (st == UMEM_OK) st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
+  if (st == UMEM_OK && (sel == nullptr || !aligned(sel, 4))) st = UMEM_ERR_INVALID_ARG;
+  if (st != UMEM_OK) return st;
+  return hip_status(launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, core, sel, stream));
+}
+
+UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* sel,
+                                 const float* q_row, const float* q_col, const float* k_row,
+                                 const float* k_col, const float* core, int32_t* idx, float* w,
+                                 int32_t* axis_idx, hipStream_t stream) {
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  if (st == UMEM_OK && desc->grid == UMEM_GRID_TUCKER)
+    st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
+  if (st == UMEM_OK && (!sel || !idx || !w || !aligned(sel, 4) || !aligned(idx, 4) || !aligned(w, 4) ||
+                        !aligned(axis_idx, 4)))
+    st = UMEM_ERR_INVALID_ARG;
+  if (st != UMEM_OK) return st;
+  return hip_status(launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx,
+                                  stream));
+}
+
+UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const float* q_row,
+                                     const float* q_col, const float* k_row, const float* k_col,
+                                     const float* core, int32_t* idx, float* w, int32_t* axis_idx,
+                                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  if (st == UMEM_OK) st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
+  if (st == UMEM_OK && (!idx || !w || !aligned(idx, 4) || !aligned(w, 4) || !aligned(axis_idx, 4)))
+    st = UMEM_ERR_INVALID_ARG;
+  if (st == UMEM_OK) st = check_ws(desc, T, ws, ws_bytes);
+  if (st != UMEM_OK) return st;
+  const Layout L = layout(desc, T);
+  float* sel = reinterpret_cast<float*>(static_cast<char*>(ws) + L.sel);
+  hipError_t e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, core, sel, stream);
+  if (e == hipSuccess)
+    e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx, stream);
+  return hip_status(e);
+}
+
+UMEM_API umem_status umem_gather_sum(int64_t n_values, int32_t dv, int32_t vdtype,
+                                     const void* values, int32_t T, int32_t bag,
+                                     const int32_t* idx, const float* w, const int32_t* perm,
+                                     int32_t expand, float* out, hipStream_t stream) {
+  umem_status st = check_gather(n_values, dv, vdtype, values, T, bag, idx, w, expand, out);
+  if (st != UMEM_OK || T == 0) return st;
+  if (st == UMEM_OK && perm != nullptr && !aligned(perm, 4)) st = UMEM_ERR_INVALID_ARG;
+  if (st != UMEM_OK) return st;
+  return hip_status(launch_gather(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, out,
+                                  stream));
+}
+
+UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt,
+                                  int32_t d_out, const float* pooled, const uint16_t* w_proj,
+                                  const uint16_t* w_out, float* out, void* ws, size_t ws_bytes,
+                                  hipStream_t stream) {
+  umem_status st = check_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws,
+                                 ws_bytes);
+  if (st != UMEM_OK || T == 0) return st;
+  return hip_status(run_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws, stream));
+}
+
+UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float* q_row,
+                                  const float* q_col, const float* k_row, const float* k_col,
+                                  const float* core, const void* values, const int32_t* perm,
+                                  const uint16_t* w_proj, const uint16_t* w_out, float* out,
+                                  int32_t* idx_out, float* w_out_scores, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  if (st == UMEM_OK) st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
+  if (st == UMEM_OK) st = check_ws(desc, T, ws, ws_bytes);
+  if (st != UMEM_OK) return st;
+  const bool project = desc->dv_virt > 0 || desc->d_out > 0;
+  if ((desc->expand > 1) != (perm != nullptr)) return UMEM_ERR_INVALID_ARG;
+  if ((desc->dv_virt > 0) != (w_proj != nullptr) || (desc->d_out > 0) != (w_out != nullptr))
+    return UMEM_ERR_INVALID_ARG;
+  if (!aligned(idx_out, 4) || !aligned(w_out_scores, 4) || !aligned(perm, 4))
+    return UMEM_ERR_INVALID_ARG;
+  const int bag = desc->heads * desc->topm;
+  const Layout L = layout(desc, T);
+  char* base = static_cast<char*>(ws);
+  float* sel = reinterpret_cast<float*>(base + L.sel);
+  int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(base + L.idx);
+  float* w = w_out_scores ? w_out_scores : reinterpret_cast<float*>(base + L.w);
+  float* pooled = project ? reinterpret_cast<float*>(base + L.pooled) : out;
+  st = check_gather(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, desc->expand,
+                    out);
+  if (st != UMEM_OK) return st;
+
+  hipError_t e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, core, sel, stream);
+  if (e == hipSuccess)
+    e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, nullptr, stream);
+  if (e == hipSuccess)
+    e = launch_gather(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, perm,
+                      desc->expand, pooled, stream);
+  if (e == hipSuccess && project)
+    e = run_project(T, desc->expand, desc->dv, desc->dv_virt, desc->d_out, pooled, w_proj, w_out,
+                    out, base + L.tmp, stream);
+  return hip_status(e);
+}
+
+UMEM_API const char* umem_status_string(umem_status status) {
+  switch (status) {
+    case UMEM_OK: return "ok";
+    case UMEM_ERR_INVALID_ARG: return "invalid argument";
+    case UMEM_ERR_UNSUPPORTED: return "unsupported by this library";
+    case UMEM_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case UMEM_ERR_HIP: return "HIP launch error";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,186 @@
+// Internal declarations and device helpers of libumem (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "umem.h"
+
+namespace umem {
+
+constexpr int kWave = 64;            // CDNA wavefront width
+constexpr int kMaxSelect = 12288;    // max(n, k*k): one selection's keys in 48 KiB of LDS
+constexpr int kMaxTopK = 110;        // k*k <= kMaxSelect
+constexpr int kMaxTopM = 256;
+constexpr int kMaxRank = 4;
+constexpr int kMaxBag = 2048;
+constexpr int kMaxTokens = 1 << 20;
+constexpr int kMaxHeads = 64;
+constexpr int kMaxExpand = 64;
+constexpr int kMaxDk = 1024;
+
+bool gather_row_supported(int dv, int vdtype);
+constexpr int kMaxRowBytes = 8192;
+
+// ---------------------------------------------------------------- host-side launchers
+
+hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
+                              const float* k_row, const float* k_col, const float* core,
+                              float* sel, hipStream_t s);
+
+hipError_t launch_select(const umem_desc& d, int T, const float* sel, const float* q_row,
+                         const float* q_col, const float* k_row, const float* k_col,
+                         const float* core, int32_t* idx, float* w, int32_t* axis_idx,
+                         hipStream_t s);
+
+hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* values, int T,
+                         int bag, const int32_t* idx, const float* w, const int32_t* perm,
+                         int expand, float* out, hipStream_t s);
+
+hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const float* pooled,
+                          const uint16_t* w_proj, const uint16_t* w_out, float* out, float* tmp,
+                          hipStream_t s);
+
+// ---------------------------------------------------------------- device helpers
+
+// Monotone map of a float to an unsigned key: larger float -> larger key.  -0.0 maps like +0.0
+// and NaN maps to 0, below every number including -inf.
+__device__ __forceinline__ uint32_t order_key(float x) {
+  if (x != x) return 0u;
+  uint32_t u = __float_as_uint(x);
+  if ((u << 1) == 0u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    int y = __shfl_up(v, off, kWave);
+    if (lane >= off) v += y;
+  }
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int lane = threadIdx.x & (kWave - 1);
+  return (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Leading singular pair (u, t) of an r x r core (r <= 4), in fp64: cyclic Jacobi on the
+// symmetric C^T C (padded with zeros to 4 x 4), t1 = its leading eigenvector, u = C t1 / |C t1|,
+// then the sign fixed so that u's largest-magnitude component (lowest index among equals) is
+// positive, and t = C^T u / sigma_1.  Single-thread routine; all indexing is static.
+__device__ inline void rank1_factors(const float* C, int r, float* u_out, float* t_out) {
+  double c[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[i][j] = (i < r && j < r) ? static_cast<double>(C[i * r + j]) : 0.0;
+  double m[4][4], v[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      double acc = 0.0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc += c[k][i] * c[k][j];
+      m[i][j] = acc;
+      v[i][j] = (i == j) ? 1.0 : 0.0;
+    }
+  for (int sweep = 0; sweep < 12; ++sweep) {
+#pragma unroll
+    for (int p = 0; p < 3; ++p)
+#pragma unroll
+      for (int q = p + 1; q < 4; ++q) {
+        const double apq = m[p][q];
+        if (fabs(apq) <= 1e-300) continue;
+        const double theta = (m[q][q] - m[p][p]) / (2.0 * apq);
+        const double tt = (theta >= 0.0 ? 1.0 : -1.0) / (fabs(theta) + sqrt(theta * theta + 1.0));
+        const double cs = 1.0 / sqrt(tt * tt + 1.0);
+        const double sn = tt * cs;
+        // m <- J^T m J with J the (p, q) rotation; v <- v J
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const double mkp = m[k][p], mkq = m[k][q];
+          m[k][p] = cs * mkp - sn * mkq;
+          m[k][q] = sn * mkp + cs * mkq;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const double mpk = m[p][k], mqk = m[q][k];
+          m[p][k] = cs * mpk - sn * mqk;
+          m[q][k] = sn * mpk + cs * mqk;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const double vkp = v[k][p], vkq = v[k][q];
+          v[k][p] = cs * vkp - sn * vkq;
+          v[k][q] = sn * vkp + cs * vkq;
+        }
+      }
+  }
+  int best = 0;
+  double lam = m[0][0];
+#pragma unroll
+  for (int j = 1; j < 4; ++j)
+    if (m[j][j] > lam) { lam = m[j][j]; best = j; }
+  double t1[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    double x = v[i][0];
+#pragma unroll
+    for (int j = 1; j < 4; ++j) x = (j == best) ? v[i][j] : x;
+    t1[i] = x;
+  }
+  double u[4], nu = 0.0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    double acc = 0.0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc += c[i][k] * t1[k];
+    u[i] = acc;
+    nu += acc * acc;
+  }
+  const double sigma = sqrt(nu);
+  int jmax = 0;
+  double amax = fabs(u[0]);
+#pragma unroll
+  for (int i = 1; i < 4; ++i)
+    if (fabs(u[i]) > amax) { amax = fabs(u[i]); jmax = i; }
+  double sgn = 1.0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (i == jmax && u[i] < 0.0) sgn = -1.0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) u[i] = sgn * u[i] / sigma;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    double acc = 0.0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc += c[k][i] * u[k];
+    if (i < r) {
+      u_out[i] = static_cast<float>(u[i]);
+      t_out[i] = static_cast<float>(acc / sigma);
+    }
+  }
+}
+
+}  // namespace umem

@@ -1,0 +1,123 @@
+"""The C ABI on the host: the library loads, exports exactly what include/umem.h declares, and
+rejects bad arguments before it touches the GPU.  No kernel is launched here: every call below
+fails validation (or only sizes the workspace)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2411_12364_amd as U
+from synth import configs as CF
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "umem.h")).read()
+    return set(re.findall(r"UMEM_API\s+[\w\s\*]+?\b(umem_\w+)\s*\(", text))
+
+
+def test_header_and_binding_agree():
+    names = declared_symbols()
+    assert names == set(U.EXPORTED)
+    lib = ctypes.CDLL(U.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_only_abi_symbols_exported():
+    out = os.popen(f"nm -D --defined-only {U.LIB_PATH}").read()
+    exported = {l.split()[-1] for l in out.splitlines() if l.split() and l.split()[1] == "T"}
+    assert {s for s in exported if not s.startswith("_")} == declared_symbols()
+
+
+def desc(**kw):
+    d = U.umem_desc()
+    base = dict(heads=2, dk=128, n_keys=4480, rank=1, topk=32, topm=32, grid=0, weight=0,
+                n_values=4480 * 4480, dv=512, vdtype=1, expand=1, dv_virt=0, d_out=0, reserved=0)
+    base.update(kw)
+    for k, v in base.items():
+        setattr(d, k, v)
+    return d
+
+
+def test_status_strings():
+    for st in (0, -1, -2, -3, -4):
+        assert U.umem_status_string(st)
+    assert U.umem_status_string(7) == "unknown status"
+
+
+def test_workspace_size_layout():
+    st, n = U.umem_workspace_size(desc(), 32)
+    assert st == U.UMEM_OK
+    sel = 2 * 32 * 2 * 4480 * 4
+    assert n >= sel + 2 * 32 * 2 * 32 * 4 and n % 256 == 0
+    st, n0 = U.umem_workspace_size(desc(), 0)
+    assert st == U.UMEM_OK and n0 == 0
+    # Tucker + IVE + projections need the pooled sums and the intermediate
+    c5 = desc(heads=4, n_keys=2048, rank=2, grid=1, topk=64, topm=64, n_values=1 << 20, expand=4,
+              dv_virt=512, d_out=2048)
+    st, n5 = U.umem_workspace_size(c5, 4096)
+    assert st == U.UMEM_OK
+    assert n5 >= 2 * 4096 * 4 * 2048 * 4 + 4096 * 4 * 512 * 4 + 4096 * 512 * 4
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(heads=0), U.UMEM_ERR_INVALID_ARG),
+    (dict(topk=4481), U.UMEM_ERR_INVALID_ARG),
+    (dict(topm=32 * 32 + 1), U.UMEM_ERR_INVALID_ARG),
+    (dict(rank=2), U.UMEM_ERR_INVALID_ARG),                    # additive grid needs rank 1
+    (dict(grid=1, rank=3), U.UMEM_ERR_INVALID_ARG),            # dk % rank != 0
+    (dict(expand=2, n_values=4480 * 2240, dv_virt=8), U.UMEM_ERR_INVALID_ARG),   # not a square
+    (dict(expand=4, n_values=4480 * 1120), U.UMEM_ERR_INVALID_ARG),              # no D'v
+    (dict(n_values=1000), U.UMEM_ERR_INVALID_ARG),             # N_p * E != n^2
+    (dict(vdtype=2), U.UMEM_ERR_INVALID_ARG),
+    (dict(reserved=1), U.UMEM_ERR_INVALID_ARG),
+    (dict(n_keys=20000, n_values=20000 * 20000), U.UMEM_ERR_UNSUPPORTED),
+    (dict(topk=111, topm=8), U.UMEM_ERR_UNSUPPORTED),
+    (dict(topm=300, topk=32), U.UMEM_ERR_UNSUPPORTED),
+    (dict(grid=1, rank=8), U.UMEM_ERR_UNSUPPORTED),
+    (dict(dv=100), U.UMEM_ERR_UNSUPPORTED),                    # 200-byte rows
+    (dict(heads=64, topm=64), U.UMEM_ERR_UNSUPPORTED),         # bag 4096
+])
+def test_descriptor_validation(kw, want):
+    st, n = U.umem_workspace_size(desc(**kw), 8)
+    assert st == want and n == 0
+
+
+def test_entry_points_reject_before_launch():
+    d = desc()
+    fake = 1 << 20          # an aligned non-null address; never dereferenced (validation fails)
+    assert U.umem_score_topk(d, 8, None, fake, fake, fake, None, fake, fake, None, fake, 1 << 30, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_score_topk(d, 8, fake + 4, fake, fake, fake, None, fake, fake, None, fake, 1 << 30, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_score_topk(d, 8, fake, fake, fake, fake, None, fake, fake, None, fake, 16, 0) == U.UMEM_ERR_WORKSPACE
+    assert U.umem_score_topk(d, 8, fake, fake, fake, fake, None, fake, fake, None, fake + 64, 1 << 30, 0) == U.UMEM_ERR_WORKSPACE
+    assert U.umem_score_topk(d, -1, fake, fake, fake, fake, None, fake, fake, None, fake, 1 << 30, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_score_topk(d, (1 << 20) + 1, fake, fake, fake, fake, None, fake, fake, None, fake, 1 << 40, 0) == U.UMEM_ERR_UNSUPPORTED
+    tucker = desc(grid=1, rank=2)
+    assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, None, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_select(d, 8, None, None, None, None, None, None, fake, fake, None, 0) == U.UMEM_ERR_INVALID_ARG
+    # gather: bad sizes, misaligned values, bag beyond the limit, unsupported row
+    assert U.umem_gather_sum(100, 512, 1, fake, 4, 0, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_gather_sum(100, 512, 1, fake + 8, 4, 64, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_gather_sum(100, 512, 1, fake, 4, 4096, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_gather_sum(100, 100, 1, fake, 4, 64, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_gather_sum(100, 512, 3, fake, 4, 64, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    # projection: missing weights / workspace
+    assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, fake, fake, fake, 64, 0) == U.UMEM_ERR_WORKSPACE
+    # forward: perm required iff expand > 1, projection weights iff D'v / d_out
+    ive = desc(heads=4, n_keys=2048, rank=2, grid=1, topk=64, topm=64, n_values=1 << 20, expand=4,
+               dv_virt=512, d_out=2048)
+    big = 1 << 36
+    assert U.umem_forward(ive, 8, fake, fake, fake, fake, fake, fake, None, fake, fake, fake, None, None, fake, big, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_forward(ive, 8, fake, fake, fake, fake, fake, fake, fake, None, fake, fake, None, None, fake, big, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_forward(d, 8, fake, fake, fake, fake, None, fake, fake, None, None, fake, None, None, fake, big, 0) == U.UMEM_ERR_INVALID_ARG
+
+
+def test_zero_tokens_is_a_noop():
+    d = desc()
+    assert U.umem_score_topk(d, 0, None, None, None, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
+    assert U.umem_forward(d, 0, None, None, None, None, None, None, None, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
+    assert U.umem_gather_sum(100, 512, 1, None, 0, 64, None, None, None, 1, None, 0) == U.UMEM_OK

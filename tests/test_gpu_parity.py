@@ -1,0 +1,225 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, on the same seeded inputs."""
+from __future__ import annotations
+
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():     # collected on CPU hosts too; every test here is gpu-marked
+    pytest.skip("no GPU", allow_module_level=True)
+
+import oracle.umem_oracle as O                      # noqa: E402
+import paper_2411_12364_amd as U                    # noqa: E402
+import synth as S                                   # noqa: E402
+from synth import configs as CF                     # noqa: E402
+from synth import device as SD                      # noqa: E402
+from tests import gpu_util as G                     # noqa: E402
+from tests import parity as P                       # noqa: E402
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def small(name, **kw):
+    base = dict(T=8, heads=1, dk=64, n_keys=64, topk=8, topm=8, dv=256, vdtype=CF.F32, seed=11)
+    base.update(kw)
+    return CF.Layer(name, **base)
+
+
+def run_and_check(cfg, batch=0, tokens=None, gap=P.GAP, expect_no_exempt=False, dl=None):
+    """Full staged check of one configuration; ``tokens`` samples the tokens the oracle checks."""
+    log(f"[case] {cfg.name} T={cfg.T} H={cfg.heads} n={cfg.n_keys} k={cfg.topk} m={cfg.topm} "
+        f"dv={cfg.dv} E={cfg.expand} grid={cfg.grid}")
+    dl = dl or SD.make_layer(cfg, batches=batch + 1)
+    T = cfg.T
+    idx, w, ax = G.score_topk(dl, T, batch)
+    pooled = G.gather(dl, idx, w, T)
+    out_f, idx_f, w_f = G.forward(dl, T, batch)
+    torch.cuda.synchronize()
+    idx_h, w_h, ax_h = G.host(idx), G.host(w), G.host(ax)
+    # umem_forward runs the same kernels: identical bits
+    assert np.array_equal(G.host(idx_f), idx_h) and np.array_equal(G.host(w_f), w_h)
+    t_sel = np.arange(T) if tokens is None else np.asarray(tokens)
+    qr, qc = CF.queries(cfg, batch=batch, tokens=t_sel)
+    kr, kc = CF.keys(cfg)
+    core = CF.core(cfg)
+    _, rep = P.check_selection(cfg, qr, qc, kr, kc, core, idx_h[t_sel], w_h[t_sel], ax_h[:, t_sel],
+                               gap=gap)
+    perm = CF.perm(cfg)
+    ref_pooled, err = P.check_pooled(cfg, G.value_rows_fn(cfg), idx_h[t_sel], w_h[t_sel],
+                                     G.host(pooled)[t_sel], perm)
+    rep["pooled_err"] = err
+    if cfg.dv_virt or cfg.d_out:
+        wp, wo = CF.projections(cfg)
+        y_ref = O.ive_project(ref_pooled, S.bf16_bits_to_f32(wp).reshape(wp.shape),
+                              None if wo is None else S.bf16_bits_to_f32(wo).reshape(wo.shape))
+        got = G.host(out_f)[t_sel].astype(np.float64)
+        perr = np.abs(got - y_ref).max(axis=1) / np.abs(y_ref).max(axis=1)
+        rep["proj_err"] = float(perr.max())
+        assert perr.max() <= 2e-2, ("projection", perr.max())
+    else:
+        assert np.array_equal(G.host(out_f).reshape(G.host(pooled).shape), G.host(pooled))
+    log(f"[report] {cfg.name}: {rep}")
+    if expect_no_exempt:
+        assert rep["axis_exempt"] == 0 and rep["grid_exempt"] == 0 and rep["e2e_slot_mismatch"] == 0
+    return rep
+
+
+# ---------------------------------------------------------------- generator twin
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_device_generator_matches_host(dtype):
+    rows, width = 1003, 72
+    t = torch.empty((rows, width), dtype=torch.float32 if dtype == "f32" else torch.bfloat16, device="cuda")
+    SD.fill_normal_(t, 5, S.TID_VALUES, 0.125, chunk=4096 * 7 + 8)
+    torch.cuda.synchronize()
+    pick = np.array([0, 1, 500, 999, 1002])
+    want = S.rows_f32(5, S.TID_VALUES, pick, width, 0.125)
+    if dtype == "f32":
+        got = t.cpu().numpy()[pick]
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    else:
+        got = t.view(torch.int16).cpu().numpy()[pick].view(np.uint16)
+        assert np.array_equal(got, S.f32_to_bf16_bits(want).reshape(got.shape))
+
+
+# ---------------------------------------------------------------- small shapes, every token
+
+def test_c1_tiny_pkm():
+    rep = run_and_check(CF.C1)
+    assert rep["pooled_err"] <= 1e-5
+
+
+def test_c1_softmax():
+    run_and_check(dataclasses.replace(CF.C1, weight=CF.W_SOFTMAX, name="tiny-softmax"))
+
+
+def test_tiles_and_ragged_tails():
+    # 3 token tiles (ragged), 4 key tiles (ragged), 3 heads, bag not a multiple of 64
+    run_and_check(small("ragged", T=70, heads=3, n_keys=200, topk=16, topm=24, dv=256,
+                        vdtype=CF.BF16, seed=12))
+
+
+@pytest.mark.parametrize("kw", [
+    dict(T=1, n_keys=1, topk=1, topm=1, dk=4),
+    dict(T=5, n_keys=7, topk=7, topm=49, dk=8),             # k = n, m = k^2: the whole grid
+    dict(T=3, n_keys=33, topk=1, topm=1),                   # argmax only
+    dict(T=9, n_keys=130, topk=20, topm=3, heads=2, dk=12),
+    dict(T=33, n_keys=64, topk=8, topm=8, dv=64, vdtype=CF.BF16),   # 128-byte rows
+    dict(T=4, n_keys=64, topk=8, topm=8, dv=8, vdtype=CF.BF16),     # 16-byte rows
+], ids=["n1", "whole-grid", "argmax", "odd-sizes", "row128B", "row16B"])
+def test_edge_shapes(kw):
+    run_and_check(small("edge", **kw))
+
+
+def _tie_layer(cfg):
+    """Integer-valued queries and keys (0, +-1, +-2): many exact ties in fp32 and fp64 alike."""
+    dl = SD.make_layer(cfg)
+    q = [np.round(CF.queries(cfg)[a] * 8).clip(-2, 2).astype(np.float32) for a in (0, 1)]
+    kr, kc = [np.round(k * 8).clip(-2, 2).astype(np.float32) for k in CF.keys(cfg)]
+    dl.q_row = torch.from_numpy(q[0][None]).cuda()
+    dl.q_col = torch.from_numpy(q[1][None]).cuda()
+    dl.k_row, dl.k_col = torch.from_numpy(kr).cuda(), torch.from_numpy(kc).cuda()
+    return dl, q, kr, kc
+
+
+@pytest.mark.parametrize("kw", [dict(T=16, n_keys=300, topk=24, topm=40, heads=2, dk=8),
+                                dict(T=8, n_keys=64, topk=8, topm=8, dk=4)], ids=["wide", "narrow"])
+def test_exact_ties_lower_index(kw):
+    cfg = small("ties", **kw)
+    dl, q, kr, kc = _tie_layer(cfg)
+    idx, w, ax = G.score_topk(dl, cfg.T)
+    torch.cuda.synchronize()
+    _, rep = P.check_selection(cfg, q[0], q[1], kr, kc, None, G.host(idx), G.host(w), G.host(ax),
+                               gap=0.0)
+    log(f"[report] ties: {rep}")
+    assert rep["e2e_slot_mismatch"] == 0
+
+
+# ---------------------------------------------------------------- gather and projection alone
+
+@pytest.mark.parametrize("dv,vdtype,expand,bag", [
+    (512, CF.BF16, 1, 64), (1024, CF.BF16, 1, 77), (256, CF.F32, 1, 5), (512, CF.BF16, 4, 256),
+    (128, CF.BF16, 9, 40), (3072, CF.BF16, 1, 33), (8, CF.BF16, 4, 130)])
+def test_gather_standalone(dv, vdtype, expand, bag):
+    rng = np.random.default_rng(dv + bag)
+    Np, T = 5000, 37
+    vdt = torch.float32 if vdtype == CF.F32 else torch.bfloat16
+    values = torch.empty((Np, dv), dtype=vdt, device="cuda")
+    SD.fill_normal_(values, 21, S.TID_VALUES, 1 / np.sqrt(dv))
+    idx = rng.integers(0, Np * expand, size=(T, bag)).astype(np.int32)
+    idx[:, 1] = idx[:, 0]
+    w = rng.standard_normal((T, bag)).astype(np.float32)
+    perm = rng.permutation(Np * expand).astype(np.int32) if expand > 1 else None
+    out = torch.empty((T, expand, dv), dtype=torch.float32, device="cuda")
+    U.check(U.umem_gather_sum(Np, dv, vdtype, values, T, bag, torch.from_numpy(idx).cuda(),
+                              torch.from_numpy(w).cuda(),
+                              None if perm is None else torch.from_numpy(perm).cuda(), expand, out))
+    torch.cuda.synchronize()
+    vals = values.float().cpu().numpy().astype(np.float64)
+    ref = O.gather_sum(lambda r: vals[r], idx, w, perm, Np, expand)
+    err = np.abs(out.cpu().numpy() - ref).max() / np.abs(ref).max()
+    log(f"[report] gather dv={dv} E={expand} bag={bag}: err={err:.2e}")
+    assert err <= 1e-5
+
+
+@pytest.mark.parametrize("T,E,dv,dvv,dout", [(70, 4, 512, 512, 2048), (5, 1, 256, 0, 96),
+                                              (130, 9, 64, 80, 0)])
+def test_project_standalone(T, E, dv, dvv, dout):
+    rng = np.random.default_rng(T)
+    pooled = rng.standard_normal((T, E, dv)).astype(np.float32)
+    kin = dv if dvv == 0 else dvv
+    wp = S.f32_to_bf16_bits(rng.standard_normal((E, dv, dvv)) / np.sqrt(dv)).reshape(E, dv, dvv) if dvv else None
+    wo = S.f32_to_bf16_bits(rng.standard_normal((kin, dout)) / np.sqrt(kin)).reshape(kin, dout) if dout else None
+    width = dout if dout else dvv
+    out = torch.empty((T, width), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(T * max(dvv, 1) * 4, 256), dtype=torch.uint8, device="cuda")
+    dev = lambda a: None if a is None else torch.from_numpy(a.view(np.int16)).cuda()
+    U.check(U.umem_project(T, E, dv, dvv, dout, torch.from_numpy(pooled).cuda(), dev(wp), dev(wo), out,
+                           ws, ws.numel()))
+    torch.cuda.synchronize()
+    f = lambda a: None if a is None else S.bf16_bits_to_f32(a).reshape(a.shape)
+    ref = O.ive_project(pooled, f(wp), f(wo)) if dvv else pooled[:, 0, :].astype(np.float64) @ f(wo)
+    err = (np.abs(out.cpu().numpy() - ref).max(axis=1) / np.abs(ref).max(axis=1)).max()
+    log(f"[report] project T={T} E={E}: err={err:.2e}")
+    assert err <= 2e-2
+
+
+# ---------------------------------------------------------------- the paper-scale workloads
+
+def test_c2_prefill_sampled():
+    rng = np.random.default_rng(2)
+    run_and_check(CF.C2, tokens=np.sort(rng.choice(CF.C2.T, 48, replace=False)))
+
+
+def test_c3_decode_20m_full_size():
+    run_and_check(CF.C3)          # every token of the 32-token decode batch, 20.07M-slot table
+
+
+@pytest.mark.parametrize("T", [1, 1024])
+def test_c4_decode_batches(T):
+    rng = np.random.default_rng(T)
+    tokens = None if T <= 64 else np.sort(rng.choice(T, 32, replace=False))
+    run_and_check(CF.C3.with_tokens(T), batch=1, tokens=tokens)
+
+
+def test_c5_tucker_ive_sampled():
+    rng = np.random.default_rng(5)
+    run_and_check(CF.C5, tokens=np.sort(rng.choice(CF.C5.T, 12, replace=False)))
+
+
+def test_deterministic():
+    dl = SD.make_layer(CF.C1)
+    a = G.forward(dl, CF.C1.T)
+    b = G.forward(dl, CF.C1.T)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
