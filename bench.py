@@ -7,8 +7,10 @@ before timing starts.  Successive steps take distinct query batches from a rotat
 enough (over 1 GiB of distinct value rows) that the gathered rows are not cache-resident.
 
 Prints one JSON line.  Besides the headline it carries the roofline of the dominant kernel
-(per-launch durations from HIP events recorded on the launch stream), the value-gather
-bandwidth, a decode batch sweep, and the CPU oracle's throughput on a bounded sample.
+(the average duration of its launches replayed back to back from a HIP graph, between two HIP
+events on the launch stream), the value-gather bandwidth, a decode batch sweep, and the CPU
+oracle's throughput on a bounded sample.  The timed steps are replayed from a captured HIP graph
+(--eager launches them one by one from Python instead).
 """
 from __future__ import annotations
 
@@ -42,7 +44,8 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--graph", action="store_true", help="replay the steps from a HIP graph")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch each step from Python instead of replaying a captured HIP graph")
     return ap.parse_args()
 
 
@@ -127,59 +130,95 @@ class Runner:
         if st:
             U.check(st, "umem_forward")
 
-    def stages(self, b, ev):
-        """The same kernels through the per-stage entry points, with an event after each."""
+    def scores(self, b):
         U, dl, c = self.U, self.dl, self.cfg
-        ev[0].record()
-        U.check(U.umem_axis_scores(self.desc, c.T, dl.q_row[b], dl.q_col[b], dl.k_row, dl.k_col,
-                                   dl.core, self.sel))
-        ev[1].record()
-        U.check(U.umem_select(self.desc, c.T, self.sel, dl.q_row[b], dl.q_col[b], dl.k_row,
-                              dl.k_col, dl.core, self.idx, self.w, None))
-        ev[2].record()
-        U.check(U.umem_gather_sum(c.n_values, c.dv, c.vdtype, dl.values, c.T, c.bag, self.idx,
-                                  self.w, dl.perm, c.expand, self.out))
-        ev[3].record()
+        st = U.umem_axis_scores(self.desc, c.T, dl.q_row[b], dl.q_col[b], dl.k_row, dl.k_col,
+                                dl.core, self.sel, self.ws, self.ws.numel())
+        if st:
+            U.check(st, "umem_axis_scores")
 
-    def time_forward(self, steps, warmup, graph=False):
+    def select(self, sel, idx, w):
+        U, dl, c = self.U, self.dl, self.cfg
+        st = U.umem_select(self.desc, c.T, sel, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col,
+                           dl.core, idx, w, None)
+        if st:
+            U.check(st, "umem_select")
+
+    def gather(self, idx, w):
+        U, dl, c = self.U, self.dl, self.cfg
+        st = U.umem_gather_sum(c.n_values, c.dv, c.vdtype, dl.values, c.T, c.bag, idx, w, dl.perm,
+                               c.expand, self.out)
+        if st:
+            U.check(st, "umem_gather_sum")
+
+    def _graph_time(self, launches):
+        """Average seconds per call of ``launches`` (a list of thunks) replayed from a HIP graph,
+        between two events on the replay stream."""
+        torch = self.torch
+        for f in launches[:8]:
+            f()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for f in launches:
+                f()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / len(launches)
+
+    def time_forward(self, steps, warmup, graph=True):
+        """Wall time of exactly ``steps`` forwards (inputs rotating over the query batches)."""
         torch = self.torch
         for s in range(warmup):
             self.forward(s % self.R)
         torch.cuda.synchronize()
         if graph:
             g = torch.cuda.CUDAGraph()
-            n_cap = min(self.R, steps)
             with torch.cuda.graph(g):
-                for s in range(n_cap):
+                for s in range(steps):
                     self.forward(s % self.R)
+            g.replay()                              # untimed replay: graph upload and warm-up
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
             g.replay()
             torch.cuda.synchronize()
-            reps = max(1, steps // n_cap)
-            t0 = time.perf_counter()
-            for _ in range(reps):
-                g.replay()
-            torch.cuda.synchronize()
-            return (time.perf_counter() - t0), reps * n_cap
+            return time.perf_counter() - t0, steps
         t0 = time.perf_counter()
         for s in range(steps):
             self.forward(s % self.R)
         torch.cuda.synchronize()
         return time.perf_counter() - t0, steps
 
-    def time_stages(self, steps, warmup):
+    def time_kernels(self, launches_per_kernel):
+        """Average duration (us) of each kernel of the forward, launched back to back from a HIP
+        graph with distinct inputs per launch: the scoring over rotating query batches, the
+        selection over precomputed score sets, the gather over precomputed selections."""
         torch = self.torch
-        for s in range(warmup):
-            self.stages(s % self.R, [torch.cuda.Event(enable_timing=True) for _ in range(4)])
+        c, n = self.cfg, launches_per_kernel
+        n_sel = min(self.R, 64)
+        sels = torch.empty((n_sel,) + tuple(self.sel.shape), dtype=torch.float32, device="cuda")
+        idxs = torch.empty((self.R,) + tuple(self.idx.shape), dtype=torch.int32, device="cuda")
+        ws_ = torch.empty((self.R,) + tuple(self.w.shape), dtype=torch.float32, device="cuda")
+        for b in range(self.R):
+            self.scores(b)
+            if b < n_sel:
+                sels[b].copy_(self.sel)
+            self.select(self.sel, idxs[b], ws_[b])
         torch.cuda.synchronize()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
-        for s in range(steps):
-            self.stages(s % self.R, evs[s])
-        torch.cuda.synchronize()
-        names = ["axis_scores_kernel", "select_kernel", "gather_kernel"]
-        avg = {}
-        for i, nm in enumerate(names):
-            avg[nm] = sum(e[i].elapsed_time(e[i + 1]) for e in evs) / steps * 1e3   # us
-        return avg
+        out = {
+            "axis_scores_kernel": self._graph_time([lambda b=b: self.scores(b % self.R) for b in range(n)]),
+            "select_kernel": self._graph_time([lambda b=b: self.select(sels[b % n_sel], self.idx, self.w)
+                                               for b in range(n)]),
+            "gather_kernel": self._graph_time([lambda b=b: self.gather(idxs[b % self.R], ws_[b % self.R])
+                                               for b in range(n)]),
+        }
+        del sels, idxs, ws_
+        return {k: v * 1e6 for k, v in out.items()}
 
 
 def roofline_for(cfg, T, name, avg_us, workload):
@@ -201,14 +240,14 @@ def distinct_batches(T, row_bytes_per_token):
     return int(min(4096, max(1, math.ceil((1 << 30) / (T * row_bytes_per_token)))))
 
 
-def sweep(base_cfg, values, steps=300, warmup=30):
+def sweep(base_cfg, values, steps=512, warmup=30):
     res = []
     for T in (1, 4, 16, 64, 256, 1024):
         cfg = base_cfg.with_tokens(T)
         R = distinct_batches(T, cfg.bag * cfg.dv * cfg.vbytes)
         r = Runner(cfg, R, values)
         secs, n = r.time_forward(steps, warmup)
-        st = r.time_stages(steps, warmup)
+        st = r.time_kernels(min(steps, 512))
         g = kernel_work(cfg, T)["gather_kernel"]
         res.append(dict(tokens=T, query_batches=R, ms_per_step=round(secs / n * 1e3, 4),
                         tokens_per_s=round(T * n / secs, 1),
@@ -266,11 +305,14 @@ def main():
     cfg = CF.C3
     torch.cuda.set_device(0)
     r = Runner(cfg, args.batches)
-    secs, n = r.time_forward(args.steps, args.warmup, graph=args.graph)
+    secs, n = r.time_forward(args.steps, args.warmup, graph=not args.eager)
     ms = secs / n * 1e3
-    log(f"forward: {n} steps in {secs:.3f}s = {ms * 1e3:.2f} us/step")
-    stage_us = r.time_stages(min(args.steps, 1000), args.warmup)
-    log(f"per-kernel (events): {stage_us}")
+    log(f"forward: {n} steps in {secs:.4f}s = {ms * 1e3:.2f} us/step")
+    e_secs, e_n = r.time_forward(min(args.steps, 1000), 10, graph=False)
+    eager_us = e_secs / e_n * 1e6
+    log(f"eager forward (one launch sequence per step from Python): {eager_us:.2f} us/step")
+    stage_us = r.time_kernels(512)
+    log(f"per-kernel (graph replay, events): {stage_us}")
     dominant = max(stage_us, key=stage_us.get)
     work = kernel_work(cfg, cfg.T)
     g_us = stage_us["gather_kernel"]
@@ -290,9 +332,10 @@ def main():
         "config": {"workload": cfg.name, "tokens": cfg.T, "heads": cfg.heads, "dk": cfg.dk,
                    "n_keys": cfg.n_keys, "slots": cfg.n_slots, "dv": cfg.dv, "values": "bf16",
                    "topk": cfg.topk, "topm": cfg.topm, "query_batches": args.batches,
-                   "graph": bool(args.graph)},
+                   "launch": "eager" if args.eager else "hip-graph"},
         "roofline": roofline_for(cfg, cfg.T, dominant, stage_us[dominant], cfg.name),
         "kernel_us": {k: round(v, 3) for k, v in stage_us.items()},
+        "eager_us_per_step": round(eager_us, 3),
         "gather": gather,
         "batch_sweep": sw,
         "cpu_baseline": cpu,

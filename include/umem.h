@@ -57,8 +57,8 @@ enum { UMEM_W_RAW = 0, UMEM_W_SOFTMAX = 1 };      /* Trick 1 (raw scores) / eq. 
  * Requirements (UMEM_ERR_INVALID_ARG otherwise): every count >= 1; dk % rank == 0;
  *   rank == 1 for UMEM_GRID_ADD; topk <= n_keys; topm <= topk^2; expand a perfect square with
  *   n_values * expand == n_keys^2; dv_virt > 0 when expand > 1; reserved == 0.
- * Limits of this library (UMEM_ERR_UNSUPPORTED beyond them): max(n_keys, topk^2) <= 12288;
- *   topk <= 110; topm <= 256; rank <= 4; (dk / rank) % 4 == 0; dk <= 1024; heads <= 64;
+ * Limits of this library (UMEM_ERR_UNSUPPORTED beyond them): max(n_keys, topk^2) <= 8192;
+ *   topk <= 90; topm <= 256; rank <= 4; (dk / rank) % 4 == 0; dk <= 1024; heads <= 64;
  *   heads * topm <= 2048; expand <= 64; a value row (dv * element size) of 16 * 2^j <= 1024
  *   bytes or a multiple of 1024 up to 8192 bytes; T <= 2^20. */
 typedef struct umem_desc {
@@ -87,14 +87,17 @@ UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_
 /* a1 + a2: per-axis selection scores -- eq. (2) for the additive grid; u^T S_row and
  * t^T S_col of eqs. (6), (8), (9) for the Tucker grid, with (u, t) the leading singular pair of
  * each head's core (eq. (11)), the sign fixed so that u's largest-magnitude component is
- * positive and t = C^T u / sigma_1.
+ * positive and t = C^T u / sigma_1.  The singular pair is computed on the device, in fp64.
  *   q_row, q_col  fp32 [T, H, dk]  the two queries; may be the same pointer (Trick 5)
  *   k_row, k_col  fp32 [H, n, dk]  keys; with rank r each dk row holds r contiguous slices
  *   core          fp32 [H, r, r]   Tucker cores (NULL for UMEM_GRID_ADD)
- *   sel           fp32 [2, T, H, n] out: [0] row scores, [1] column scores */
+ *   sel           fp32 [2, T, H, n] out: [0] row scores, [1] column scores
+ *   ws            scratch for the singular vectors, Tucker grid only (2 KiB, 256-byte aligned;
+ *                 a workspace sized by umem_workspace_size suffices); may be NULL otherwise */
 UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const float* q_row,
-                             const float* q_col, const float* k_row, const float* k_col,
-                             const float* core, float* sel, hipStream_t stream);
+                                      const float* q_col, const float* k_row, const float* k_col,
+                                      const float* core, float* sel, void* ws, size_t ws_bytes,
+                                      hipStream_t stream);
 
 /* a3 + a4 + a5 from selection scores: per-axis top-k, grid scores of the k*k candidates
  * (additive eq. (3); Tucker eq. (10) with the per-slice scores recomputed exactly for the

@@ -52,7 +52,7 @@ def _load() -> ctypes.CDLL:
     D = ctypes.POINTER(umem_desc)
     sig = {
         "umem_workspace_size": [D, I32, ctypes.POINTER(SZ)],
-        "umem_axis_scores": [D, I32, P, P, P, P, P, P, P],
+        "umem_axis_scores": [D, I32, P, P, P, P, P, P, P, SZ, P],
         "umem_select": [D, I32, P, P, P, P, P, P, P, P, P, P],
         "umem_score_topk": [D, I32, P, P, P, P, P, P, P, P, P, SZ, P],
         "umem_gather_sum": [I64, I32, I32, P, I32, I32, P, P, P, I32, P, P],
@@ -113,9 +113,10 @@ def umem_workspace_size(desc: umem_desc, T: int):
     return st, out.value
 
 
-def umem_axis_scores(desc, T, q_row, q_col, k_row, k_col, core, sel, stream=None) -> int:
+def umem_axis_scores(desc, T, q_row, q_col, k_row, k_col, core, sel, ws=None, ws_bytes=0,
+                     stream=None) -> int:
     return _lib.umem_axis_scores(_d(desc), T, _p(q_row), _p(q_col), _p(k_row), _p(k_col), _p(core),
-                                 _p(sel), _s(stream))
+                                 _p(sel), _p(ws), ws_bytes, _s(stream))
 
 
 def umem_select(desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx=None,

@@ -5,9 +5,15 @@
 // score is sum_rho f[rho] S_rho[t, i] with f = u (rows) or t (columns), the leading singular pair
 // of the head's Tucker core (eqs. (6), (8), (9)); for the additive grid f = [1].
 //
-// Tiling: one workgroup computes a TT x TN block (tokens x keys) of one (head, axis), streaming
-// the key and query tiles through LDS in chunks of DC dims.  Each key is read from HBM once per
-// token tile; at decode (T <= TT) once in total.
+// Two kernels compute the same scores:
+//  * axis_scores_mfma (slices of 16-multiple width, dk <= 256): scores as a GEMM on
+//    v_mfma_f32_16x16x4_f32.  A workgroup covers 64 keys x 16*MT tokens of one (head, axis): each
+//    of its 4 waves owns 16 keys and loads their key rows straight into registers (every load
+//    issued up front: one memory round trip), while the query tile is staged once in LDS and
+//    shared by the waves.  Each key is read from HBM once per token tile; at decode (T <= 64)
+//    once in total.
+//  * axis_scores_valu (any shape): a TT x TN tile on the vector ALUs, key and query tiles
+//    streamed through LDS in chunks of DC dims.
 #include "umem_internal.h"
 
 namespace umem {
@@ -19,10 +25,10 @@ constexpr int DC = 32;       // dims per LDS chunk
 constexpr int LDS_STRIDE = DC + 4;   // floats per LDS row: float4-aligned, conflict-free b128 reads
 constexpr int THREADS = 256;
 
-__global__ __launch_bounds__(THREADS) void axis_scores_kernel(
+__global__ __launch_bounds__(THREADS) void axis_scores_valu(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
-    const float* __restrict__ core, float* __restrict__ sel, int T, int H, int n, int dk,
+    const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
     int rank) {
   const int axis = blockIdx.z & 1;
   const int h = blockIdx.z >> 1;
@@ -38,15 +44,7 @@ __global__ __launch_bounds__(THREADS) void axis_scores_kernel(
   float* sk = reinterpret_cast<float*>(sk4);
   float* sq = reinterpret_cast<float*>(sq4);
 
-  if (tid == 0) {
-    if (core != nullptr) {
-      float u[kMaxRank], tv[kMaxRank];
-      rank1_factors(core + static_cast<size_t>(h) * rank * rank, rank, u, tv);
-      for (int j = 0; j < rank; ++j) fvec[j] = axis ? tv[j] : u[j];
-    } else {
-      fvec[0] = 1.0f;
-    }
-  }
+  if (tid < kMaxRank) fvec[tid] = factors ? factors[(h * 2 + axis) * kMaxRank + tid] : 1.0f;
 
   // micro-tile: keys kx + 16 c (c < 4), tokens 2 ty + {0, 1}
   const int kx = tid & 15;
@@ -112,7 +110,7 @@ __global__ __launch_bounds__(THREADS) void axis_scores_kernel(
           }
       }
     }
-    if (core != nullptr) {
+    if (factors != nullptr) {
       const float f = fvec[rho];
 #pragma unroll
       for (int a = 0; a < 2; ++a)
@@ -139,15 +137,134 @@ __global__ __launch_bounds__(THREADS) void axis_scores_kernel(
   }
 }
 
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int MT, int NCH>
+__global__ __launch_bounds__(THREADS) void axis_scores_mfma(
+    const float* __restrict__ q_row, const float* __restrict__ q_col,
+    const float* __restrict__ k_row, const float* __restrict__ k_col,
+    const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
+    int rank) {
+  constexpr int TM = 16 * MT;
+  extern __shared__ __align__(16) float qs[];    // [TM][dk + 4]
+  __shared__ float fvec[kMaxRank];
+  const int axis = blockIdx.z & 1;
+  const int h = blockIdx.z >> 1;
+  const float* __restrict__ q = axis ? q_col : q_row;
+  const float* __restrict__ K = axis ? k_col : k_row;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int j = lane & 15;        // key within the wave's 16 (B column, D column)
+  const int g = lane >> 4;        // 4-dim group within a 16-dim chunk
+  const int key0 = blockIdx.x * 64 + wave * 16;
+  const int t0 = blockIdx.y * TM;
+  const int ldq = dk + 4;
+  const int width = dk / rank;
+
+  // this lane's key-row fragments: dims 16 c + 4 g .. + 3 of key key0 + j, all chunks
+  const int key = key0 + j;
+  const float* krow = K + (static_cast<size_t>(h) * n + (key < n ? key : 0)) * dk + 4 * g;
+  float4 kf[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+    kf[c] = (key < n) ? *reinterpret_cast<const float4*>(krow + 16 * c)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+  // the query tile, shared by the four waves
+  const int vec_per_row = dk / 4;
+  for (int v = tid; v < TM * vec_per_row; v += THREADS) {
+    const int r = v / vec_per_row, c4 = v - r * vec_per_row;
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t0 + r < T) x = *reinterpret_cast<const float4*>(q + (static_cast<size_t>(t0 + r) * H + h) * dk + 4 * c4);
+    *reinterpret_cast<float4*>(qs + r * ldq + 4 * c4) = x;
+  }
+  if (tid < kMaxRank) fvec[tid] = factors ? factors[(h * 2 + axis) * kMaxRank + tid] : 1.0f;
+  __syncthreads();
+
+  f32x4 out[MT], acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    out[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  int rho = 0;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    {
+      if (c > 0 && (16 * c) % width == 0) {     // a slice ends: fold it with its factor
+        const float f = fvec[rho++];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          out[mt] += f * acc[mt];
+          acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const float4 qf = *reinterpret_cast<const float4*>(qs + (mt * 16 + j) * ldq + 16 * c + 4 * g);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf.x, kf[c].x, acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf.y, kf[c].y, acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf.z, kf[c].z, acc[mt], 0, 0, 0);
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf.w, kf[c].w, acc[mt], 0, 0, 0);
+      }
+    }
+  }
+  const float f = fvec[rho];
+  // lane holds D[4 g + r][j]: token t0 + 16 mt + 4 g + r, key key0 + j
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    out[mt] += f * acc[mt];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = t0 + mt * 16 + 4 * g + r;
+      if (t < T && key < n) sel[((static_cast<size_t>(axis) * T + t) * H + h) * n + key] = out[mt][r];
+    }
+  }
+}
+
 }  // namespace
 
+__global__ void rank1_kernel(const float* __restrict__ core, int H, int r, float* __restrict__ factors) {
+  const int h = threadIdx.x;
+  if (h < H) {
+    float* f = factors + h * 2 * kMaxRank;
+    rank1_factors(core + static_cast<size_t>(h) * r * r, r, f, f + kMaxRank);
+  }
+}
+
+hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, hipStream_t s) {
+  hipLaunchKernelGGL(rank1_kernel, dim3(1), dim3(kWave), 0, s, core, d.heads, d.rank, factors);
+  return hipGetLastError();
+}
+
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
-                              const float* k_row, const float* k_col, const float* core,
+                              const float* k_row, const float* k_col, const float* factors,
                               float* sel, hipStream_t s) {
   if (T == 0) return hipSuccess;
+  const float* c = (d.grid == UMEM_GRID_TUCKER) ? factors : nullptr;
+  const int width = d.dk / d.rank;
+  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && width % 16 == 0) {
+    int mt = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
+    while (mt > 1 && static_cast<size_t>(16 * mt) * (d.dk + 4) * 4 > 65536) mt /= 2;
+    const size_t lds = static_cast<size_t>(16 * mt) * (d.dk + 4) * 4;
+    dim3 grid((d.n_keys + 63) / 64, (T + 16 * mt - 1) / (16 * mt), d.heads * 2);
+#define UMEM_SCORE(MT, NCH)                                                                      \
+  hipLaunchKernelGGL((axis_scores_mfma<MT, NCH>), grid, dim3(THREADS), lds, s, q_row, q_col,     \
+                     k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank)
+#define UMEM_SCORE_DK(MT)                  \
+  if (d.dk == 64) UMEM_SCORE(MT, 4);       \
+  else if (d.dk == 128) UMEM_SCORE(MT, 8); \
+  else UMEM_SCORE(MT, 16)
+    if (mt == 1) { UMEM_SCORE_DK(1); }
+    else if (mt == 2) { UMEM_SCORE_DK(2); }
+    else { UMEM_SCORE_DK(4); }
+#undef UMEM_SCORE_DK
+#undef UMEM_SCORE
+    return hipGetLastError();
+  }
   dim3 grid((d.n_keys + TN - 1) / TN, (T + TT - 1) / TT, d.heads * 2);
-  const float* c = (d.grid == UMEM_GRID_TUCKER) ? core : nullptr;
-  hipLaunchKernelGGL(axis_scores_kernel, grid, dim3(THREADS), 0, s, q_row, q_col, k_row, k_col, c,
+  hipLaunchKernelGGL(axis_scores_valu, grid, dim3(THREADS), 0, s, q_row, q_col, k_row, k_col, c,
                      sel, T, d.heads, d.n_keys, d.dk, d.rank);
   return hipGetLastError();
 }

@@ -65,13 +65,16 @@ umem_status check_scoring_ptrs(const umem_desc* d, const float* q_row, const flo
 }
 
 struct Layout {
-  size_t sel, idx, w, pooled, tmp, total;
+  size_t factors, sel, idx, w, pooled, tmp, total;
 };
 
+// Workspace: [rank-1 factors (Tucker)] [selection scores] [idx] [w] [pooled] [intermediate]
 Layout layout(const umem_desc* d, int32_t T) {
   Layout L{};
   const size_t th = static_cast<size_t>(T) * d->heads;
   size_t off = 0;
+  L.factors = off;
+  if (d->grid == UMEM_GRID_TUCKER) off += round_up(kFactorBytes);
   L.sel = off;
   off += round_up(2 * th * d->n_keys * sizeof(float));
   L.idx = off;
@@ -161,14 +164,22 @@ UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_
 
 UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const float* q_row,
                                       const float* q_col, const float* k_row, const float* k_col,
-                                      const float* core, float* sel, hipStream_t stream) {
+                                      const float* core, float* sel, void* ws, size_t ws_bytes,
+                                      hipStream_t stream) {
   umem_status st = check_desc(desc);
   if (st == UMEM_OK) st = check_tokens(T);
   if (st != UMEM_OK || T == 0) return st;
   if (st == UMEM_OK) st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
   if (st == UMEM_OK && (sel == nullptr || !aligned(sel, 4))) st = UMEM_ERR_INVALID_ARG;
+  const bool tucker = desc->grid == UMEM_GRID_TUCKER;
+  if (st == UMEM_OK && tucker && (ws == nullptr || !aligned(ws, kAlign) || ws_bytes < kFactorBytes))
+    st = UMEM_ERR_WORKSPACE;
   if (st != UMEM_OK) return st;
-  return hip_status(launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, core, sel, stream));
+  float* factors = tucker ? static_cast<float*>(ws) : nullptr;
+  hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
+  if (e == hipSuccess)
+    e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, factors, sel, stream);
+  return hip_status(e);
 }
 
 UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* sel,
@@ -202,7 +213,12 @@ UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const flo
   if (st != UMEM_OK) return st;
   const Layout L = layout(desc, T);
   float* sel = reinterpret_cast<float*>(static_cast<char*>(ws) + L.sel);
-  hipError_t e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, core, sel, stream);
+  float* factors = reinterpret_cast<float*>(static_cast<char*>(ws) + L.factors);
+  const bool tucker = desc->grid == UMEM_GRID_TUCKER;
+  hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
+  if (e == hipSuccess)
+    e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, tucker ? factors : nullptr, sel,
+                           stream);
   if (e == hipSuccess)
     e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx, stream);
   return hip_status(e);
@@ -259,7 +275,12 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
                     out);
   if (st != UMEM_OK) return st;
 
-  hipError_t e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, core, sel, stream);
+  float* factors = reinterpret_cast<float*>(base + L.factors);
+  const bool tucker = desc->grid == UMEM_GRID_TUCKER;
+  hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
+  if (e == hipSuccess)
+    e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, tucker ? factors : nullptr, sel,
+                           stream);
   if (e == hipSuccess)
     e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, nullptr, stream);
   if (e == hipSuccess)

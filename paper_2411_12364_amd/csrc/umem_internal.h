@@ -9,8 +9,8 @@
 namespace umem {
 
 constexpr int kWave = 64;            // CDNA wavefront width
-constexpr int kMaxSelect = 12288;    // max(n, k*k): one selection's keys in 48 KiB of LDS
-constexpr int kMaxTopK = 110;        // k*k <= kMaxSelect
+constexpr int kMaxSelect = 8192;     // max(n, k*k): one selection's keys in 32 KiB of LDS
+constexpr int kMaxTopK = 90;         // k*k <= kMaxSelect
 constexpr int kMaxTopM = 256;
 constexpr int kMaxRank = 4;
 constexpr int kMaxBag = 2048;
@@ -18,14 +18,22 @@ constexpr int kMaxTokens = 1 << 20;
 constexpr int kMaxHeads = 64;
 constexpr int kMaxExpand = 64;
 constexpr int kMaxDk = 1024;
+constexpr size_t kFactorBytes = static_cast<size_t>(kMaxHeads) * 2 * 4 * sizeof(float);
 
 bool gather_row_supported(int dv, int vdtype);
+size_t select_lds_bytes(int n, int k);
+int additive_candidates(int k, int m);
 constexpr int kMaxRowBytes = 8192;
 
 // ---------------------------------------------------------------- host-side launchers
 
+// Tucker grid: leading singular pair of every head's core, factors[h][0] = u, factors[h][1] = t,
+// each padded to kMaxRank floats.
+hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, hipStream_t s);
+
+// Selection scores; factors is the output of launch_rank1 (Tucker) or NULL (additive).
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
-                              const float* k_row, const float* k_col, const float* core,
+                              const float* k_row, const float* k_col, const float* factors,
                               float* sel, hipStream_t s);
 
 hipError_t launch_select(const umem_desc& d, int T, const float* sel, const float* q_row,
@@ -87,7 +95,8 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float x) {
 // Leading singular pair (u, t) of an r x r core (r <= 4), in fp64: cyclic Jacobi on the
 // symmetric C^T C (padded with zeros to 4 x 4), t1 = its leading eigenvector, u = C t1 / |C t1|,
 // then the sign fixed so that u's largest-magnitude component (lowest index among equals) is
-// positive, and t = C^T u / sigma_1.  Single-thread routine; all indexing is static.
+// positive, and t = C^T u / sigma_1.  Writes u and t to u_out[0, r) and t_out[0, r).
+// Single-thread routine; all indexing is static.
 __device__ inline void rank1_factors(const float* C, int r, float* u_out, float* t_out) {
   double c[4][4];
 #pragma unroll

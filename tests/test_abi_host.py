@@ -96,7 +96,8 @@ def test_entry_points_reject_before_launch():
     assert U.umem_score_topk(d, -1, fake, fake, fake, fake, None, fake, fake, None, fake, 1 << 30, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_score_topk(d, (1 << 20) + 1, fake, fake, fake, fake, None, fake, fake, None, fake, 1 << 40, 0) == U.UMEM_ERR_UNSUPPORTED
     tucker = desc(grid=1, rank=2)
-    assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, None, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, fake, fake, None, 0, 0) == U.UMEM_ERR_WORKSPACE
     assert U.umem_select(d, 8, None, None, None, None, None, None, fake, fake, None, 0) == U.UMEM_ERR_INVALID_ARG
     # gather: bad sizes, misaligned values, bag beyond the limit, unsupported row
     assert U.umem_gather_sum(100, 512, 1, fake, 4, 0, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG

@@ -223,3 +223,41 @@ def test_deterministic():
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+def test_hip_graph_replay_matches_eager():
+    """Forwards captured in a HIP graph, replayed several times with eager work in between, give
+    the eager results bit for bit."""
+    cfg = CF.C1
+    dl = SD.make_layer(cfg, batches=3)
+    desc = G.desc_for(cfg)
+    T = cfg.T
+    ws = G.workspace(desc, T)
+    outs = [torch.empty((T, cfg.dv), dtype=torch.float32, device="cuda") for _ in range(3)]
+    idxs = [torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda") for _ in range(3)]
+    wts = [torch.empty((T, cfg.heads, cfg.topm), dtype=torch.float32, device="cuda") for _ in range(3)]
+
+    def step(b):
+        U.check(U.umem_forward(desc, T, dl.q_row[b], dl.q_col[b], dl.k_row, dl.k_col, None, dl.values,
+                               None, None, None, outs[b], idxs[b], wts[b], ws, ws.numel()))
+
+    for b in range(3):
+        step(b)
+    torch.cuda.synchronize()
+    want = [(o.clone(), i.clone(), w.clone()) for o, i, w in zip(outs, idxs, wts)]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for b in range(3):
+            step(b)
+    for rep in range(4):
+        for t in outs + wts:
+            t.fill_(-1.0)
+        for t in idxs:
+            t.fill_(-1)
+        g.replay()
+        torch.cuda.synchronize()
+        for b in range(3):
+            assert torch.equal(outs[b], want[b][0]) and torch.equal(idxs[b], want[b][1])
+            assert torch.equal(wts[b], want[b][2])
+        step(0)                     # eager work between replays
+        torch.cuda.synchronize()
