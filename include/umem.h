@@ -58,7 +58,7 @@ enum { UMEM_W_RAW = 0, UMEM_W_SOFTMAX = 1 };      /* Trick 1 (raw scores) / eq. 
  *   rank == 1 for UMEM_GRID_ADD; topk <= n_keys; topm <= topk^2; expand a perfect square with
  *   n_values * expand == n_keys^2; dv_virt > 0 when expand > 1; reserved == 0.
  * Limits of this library (UMEM_ERR_UNSUPPORTED beyond them): max(n_keys, topk^2) <= 8192;
- *   topk <= 90; topm <= 256; rank <= 4; (dk / rank) % 4 == 0; dk <= 1024; heads <= 64;
+ *   topk <= 90 (64 for the Tucker grid); topm <= 256; rank <= 4; (dk / rank) % 4 == 0; dk <= 1024; heads <= 64;
  *   heads * topm <= 2048; expand <= 64; a value row (dv * element size) of 16 * 2^j <= 1024
  *   bytes or a multiple of 1024 up to 8192 bytes; T <= 2^20. */
 typedef struct umem_desc {
@@ -102,7 +102,7 @@ UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const fl
 /* a3 + a4 + a5 from selection scores: per-axis top-k, grid scores of the k*k candidates
  * (additive eq. (3); Tucker eq. (10) with the per-slice scores recomputed exactly for the
  * candidates, non-candidates excluded), global top-m and weights.
- *   sel       fp32 [2, T, H, n] as written by umem_axis_scores
+ *   sel       fp32 [2, T, H, n] as written by umem_axis_scores, 16-byte aligned
  *   q_*, k_*, core  as above; read only for UMEM_GRID_TUCKER (may be NULL for ADD)
  *   idx       int32 [T, H, m] out: logical slot i*n + j, sorted by (score desc, index asc)
  *   w         fp32 [T, H, m] out: the weight of each slot (raw grid score, or SoftMax)

@@ -1,51 +1,52 @@
 // a3 + a4 + a5: per-axis top-k, grid scores of the candidates, global top-m and weights.
 //
-// One workgroup (256 threads) per (token, head).  Every selection is exact under the order
-// (score desc, index asc):
+// One workgroup of eight waves per (token, head): waves 0-3 select on the row axis and waves
+// 4-7 on the column axis, at the same time.  Every selection is exact under the order
+// (score desc, index asc), in three steps:
 //
-//  1. Threshold.  Each thread holds its elements in registers and takes their maximum.  The k-th
-//     largest of the 256 thread maxima, L, is found by a 32-step ballot search in one wave.  The
-//     k largest maxima are k distinct elements >= L, so the k-th largest element is >= L and
-//     every element of the top-k (ties included) is >= L.
-//  2. Survivors {x >= L} (typically a few dozen) are appended to LDS with one atomic per wave.
-//  3. Each survivor's rank is the number of survivors ordered before it; ranks < k are the
-//     answer, already sorted.
-//  If the survivors overflow their buffer (massive ties), a radix select on the 32-bit keys
-//  with lowest-position tie-break takes over.
+//  1. Threshold.  Each thread holds its elements in registers and takes their maximum.  The
+//     k-th largest of the group's thread maxima, L, comes from a 32-step ballot search in one
+//     wave.  They are maxima of disjoint sets, so at least k elements are >= L: the k-th largest
+//     element is >= L, and every element of the top-k is >= L.
+//  2. Survivors {x >= L} (typically a few dozen) are compacted into LDS (wave scans in DPP).
+//  3. A survivor's rank is the number of survivors ordered before it; ranks < k are the answer,
+//     already sorted.
+//  If the survivors overflow their buffer (massive ties), an exact threshold search over all
+//  elements (32 steps of group-wide counts) takes over.
 //
 // Additive grid (eq. (3)): with both axis lists sorted, candidate (a, b) (a-th best row, b-th
 // best column) is preceded in the order by the (a+1)(b+1)-1 candidates (a' <= a, b' <= b), so
 // only (a+1)(b+1) <= m can reach the top-m.  Candidate scores are summed in fp64, where the sum
-// of two fp32 scores is exact, so this dominance holds exactly.
-// Tucker grid (eq. (10)): all k*k candidates, exact per-slice scores recomputed for the selected
-// keys, scores in fp64, the threshold filter of step 1 on their fp32 roundings.
+// of two fp32 scores is exact (or monotone), so this dominance holds.
+// Tucker grid (eq. (10)): all k*k candidates, the exact per-slice scores recomputed for the
+// selected keys, candidate scores in fp64; the threshold of step 1 runs on their fp32 roundings
+// (rounding is monotone, so the survivors still contain the top-m) and the ranks on fp64.
 #include "umem_internal.h"
 
 namespace umem {
 namespace {
 
-constexpr int THREADS = 256;
+constexpr int THREADS = 512;
 constexpr int NWAVES = THREADS / kWave;
-constexpr int SMAX = 2048;        // survivor buffer
+constexpr int GROUP = 256;          // threads per axis
+constexpr int SMAX_AX = 512;        // survivors per axis
+constexpr int SMAX_S = 512;         // grid survivors (Tucker)
+constexpr int KK_MAX = 4096;        // Tucker: k*k candidates
+constexpr int CPT = KK_MAX / THREADS;   // Tucker candidates per thread
 
 struct SelectShared {
-  uint32_t mx[THREADS];               // thread maxima
-  int hist[256];                      // fallback radix histogram
-  int wave_cnt[NWAVES][2];
-  int digit, remaining, count;
-  uint32_t thr;
+  uint32_t mx[THREADS];               // thread maxima (both axes, or the grid)
+  int wave_tot[NWAVES];
+  uint32_t thr[2];
+  int cnt2[2];
   int32_t ax_idx[2][kMaxTopK];        // axis top-k, sorted by (score desc, index asc)
   float ax_sc[2][kMaxTopK];
-  uint64_t tmp_comp[kMaxTopK];        // fallback: the k picked positions, re-ranked
-  int32_t tmp_pos[kMaxTopM];
-  int32_t inv[2][kMaxTopK];           // Tucker fallback: index-sorted position -> sorted position
   float s_ex[2][kMaxRank][kMaxTopK];  // Tucker: exact per-slice scores of the selected keys
   double p_col[kMaxRank][kMaxTopK];   // Tucker: (C S_col)[rho, b] in fp64
   float core[kMaxRank * kMaxRank];
   int32_t out_flat[kMaxTopM];         // final top-m, by rank
   double out_g[kMaxTopM];
   float e[kMaxTopM];
-  double gmax;
   float esum;
 };
 
@@ -56,243 +57,276 @@ __device__ __forceinline__ uint64_t order_key64(double x) {
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-// Slot for an appended element: all lanes of the wave call this; returns -1 where !pred.
-__device__ __forceinline__ int wave_append(bool pred, int* counter) {
-  const uint64_t m = __ballot(pred);
-  if (m == 0ull) return -1;
-  int base = 0;
-  if ((threadIdx.x & (kWave - 1)) == 0) base = atomicAdd(counter, static_cast<int>(__popcll(m)));
-  base = __shfl(base, 0, kWave);
-  return pred ? base + static_cast<int>(__popcll(m & lanemask_lt())) : -1;
+__device__ __forceinline__ double key64_value(uint64_t k) {
+  const uint64_t raw = (k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
+  return __longlong_as_double(static_cast<long long>(raw));
 }
 
-// k-th largest of the 256 thread maxima (wave 0 only; 4 values per lane).
-__device__ __forceinline__ uint32_t kth_largest_of_maxima(const uint32_t* mx, int k) {
+__device__ __forceinline__ float key32_value(uint32_t k) {
+  return __uint_as_float((k >> 31) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+// Composite key of an axis element: larger = earlier in (score desc, index asc).
+__device__ __forceinline__ uint64_t axis_comp(uint32_t key, int idx) {
+  return (static_cast<uint64_t>(key) << 32) |
+         static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(idx));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts and row broadcasts).
+__device__ __forceinline__ int wave_scan_dpp(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
+
+// Exclusive offset of each thread's count within waves [w0, w0 + nw), and their total.
+// Called by every thread of the workgroup (it holds two barriers).
+__device__ __forceinline__ int2 group_offsets(int cnt, int w0, int nw, SelectShared& sh) {
   const int lane = threadIdx.x & (kWave - 1);
-  const uint32_t v0 = mx[lane], v1 = mx[lane + 64], v2 = mx[lane + 128], v3 = mx[lane + 192];
+  const int wave = threadIdx.x / kWave;
+  const int incl = wave_scan_dpp(cnt);
+  if (lane == kWave - 1) sh.wave_tot[wave] = incl;
+  __syncthreads();
+  int base = 0, total = 0;
+  for (int w = w0; w < w0 + nw; ++w) {
+    const int tw = sh.wave_tot[w];
+    base += (w < wave) ? tw : 0;
+    total += tw;
+  }
+  __syncthreads();
+  return make_int2(base + incl - cnt, total);
+}
+
+// Largest L with at least k of the values vals[0, 64 V) >= L (run by one wave).
+template <int V>
+__device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t* vals, int k) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint32_t v[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) v[q] = vals[lane + kWave * q];
   uint32_t prefix = 0u;
   for (int b = 31; b >= 0; --b) {
     const uint32_t c = prefix | (1u << b);
-    const int cnt = __popcll(__ballot(v0 >= c)) + __popcll(__ballot(v1 >= c)) +
-                    __popcll(__ballot(v2 >= c)) + __popcll(__ballot(v3 >= c));
+    int cnt = 0;
+#pragma unroll
+    for (int q = 0; q < V; ++q) cnt += __popcll(__ballot(v[q] >= c));
     if (cnt >= k) prefix = c;
   }
   return prefix;
 }
 
-// Positions (ascending) of the k largest of keys[0, len); ties go to the lower position.
-// Radix select, four 8-bit digits.  Used only when the threshold filter overflows.
-__device__ void radix_select(const uint32_t* keys, int len, int k, int32_t* out, SelectShared& sh) {
+// ---------------------------------------------------------------- per-axis top-k
+
+// Element i of an axis is held by thread g of its group (g = threadIdx.x % 256) as key[j]:
+// VEC == 4 (n % 4 == 0): i = 1024 j + 4 g + e, key[4 j + e]; VEC == 1: i = 256 j + g.
+template <int VEC>
+__device__ __forceinline__ int elem_index(int g, int j, int e) {
+  return VEC == 4 ? 1024 * j + 4 * g + e : GROUP * j + g;
+}
+
+template <int NV, int VEC>
+__device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, int h, int n, int k,
+                            uint64_t* comp_all, SelectShared& sh) {
+  constexpr int NE = NV * VEC;
   const int tid = threadIdx.x;
+  const int axis = tid / GROUP;
+  const int g = tid % GROUP;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
-  uint32_t prefix = 0u, mask = 0u;
-  int remaining = k;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    sh.hist[tid] = 0;
-    __syncthreads();
-    for (int i = tid; i < len; i += THREADS) {
-      const uint32_t x = keys[i];
-      if ((x & mask) == prefix) atomicAdd(&sh.hist[(x >> shift) & 255u], 1);
+  const float* src = sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n;
+  uint64_t* comp = comp_all + axis * SMAX_AX;
+  uint32_t key[NE];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    if (VEC == 4) {
+      const float4 v = *reinterpret_cast<const float4*>(src + min(1024 * j + 4 * g, n - 4));
+      key[4 * j + 0] = order_key(v.x);
+      key[4 * j + 1] = order_key(v.y);
+      key[4 * j + 2] = order_key(v.z);
+      key[4 * j + 3] = order_key(v.w);
+    } else {
+      key[j] = order_key(src[min(GROUP * j + g, n - 1)]);
     }
-    __syncthreads();
-    if (wave == 0) {
-      const int b0 = 255 - 4 * lane;
-      const int c0 = sh.hist[b0], c1 = sh.hist[b0 - 1], c2 = sh.hist[b0 - 2], c3 = sh.hist[b0 - 3];
-      const int sum = c0 + c1 + c2 + c3;
-      const int incl = wave_inclusive_scan(sum);
-      const int excl = incl - sum;
-      if (excl < remaining && remaining <= incl) {
-        int acc = excl, dig;
-        if (remaining <= acc + c0) {
-          dig = b0;
-        } else if (remaining <= acc + c0 + c1) {
-          acc += c0;
-          dig = b0 - 1;
-        } else if (remaining <= acc + c0 + c1 + c2) {
-          acc += c0 + c1;
-          dig = b0 - 2;
-        } else {
-          acc += c0 + c1 + c2;
-          dig = b0 - 3;
-        }
-        sh.digit = dig;
-        sh.remaining = remaining - acc;
-      }
-    }
-    __syncthreads();
-    prefix |= static_cast<uint32_t>(sh.digit) << shift;
-    mask |= 255u << shift;
-    remaining = sh.remaining;
-    __syncthreads();
   }
-  const uint32_t thr = prefix;
-  const int need_eq = remaining;
-  const int seg = ((len + NWAVES - 1) / NWAVES + kWave - 1) / kWave * kWave;
-  const int beg = wave * seg;
-  const int end = min(len, beg + seg);
-  int gt_cnt = 0, eq_cnt = 0;
-  for (int base = beg; base < end; base += kWave) {
-    const int i = base + lane;
-    const uint32_t x = (i < end) ? keys[i] : 0u;
-    gt_cnt += __popcll(__ballot(i < end && x > thr));
-    eq_cnt += __popcll(__ballot(i < end && x == thr));
-  }
-  if (lane == 0) {
-    sh.wave_cnt[wave][0] = gt_cnt;
-    sh.wave_cnt[wave][1] = eq_cnt;
-  }
-  __syncthreads();
-  int eq_base = 0, taken_base = 0;
-  for (int v = 0; v < wave; ++v) {
-    const int g = sh.wave_cnt[v][0], e = sh.wave_cnt[v][1];
-    taken_base += g + min(max(need_eq - eq_base, 0), e);
-    eq_base += e;
-  }
-  const uint64_t lt = lanemask_lt();
-  for (int base = beg; base < end; base += kWave) {
-    const int i = base + lane;
-    const uint32_t x = (i < end) ? keys[i] : 0u;
-    const bool gt = i < end && x > thr;
-    const bool eq = i < end && x == thr;
-    const uint64_t m_eq = __ballot(eq);
-    const int eq_rank = eq_base + __popcll(m_eq & lt);
-    const bool take = gt || (eq && eq_rank < need_eq);
-    const uint64_t m_take = __ballot(take);
-    if (take) out[taken_base + __popcll(m_take & lt)] = i;
-    eq_base += __popcll(m_eq);
-    taken_base += __popcll(m_take);
-  }
-  __syncthreads();
-}
-
-// Composite 64-bit key of an axis element: larger = earlier in (score desc, index asc).
-__device__ __forceinline__ uint64_t axis_comp(uint32_t key, int idx) {
-  return (static_cast<uint64_t>(key) << 32) | static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(idx));
-}
-
-// Top-k of one axis whose n scores sit in registers (element tid + 256 j in x[j]).
-template <int NPT>
-__device__ void select_axis(const float (&x)[NPT], int n, int k, int axis, SelectShared& sh,
-                            unsigned char* dyn) {
-  const int tid = threadIdx.x;
-  uint64_t* comp = reinterpret_cast<uint64_t*>(dyn);     // [SMAX] survivors
   uint32_t mx = 0u;
-  uint32_t key[NPT];
 #pragma unroll
-  for (int j = 0; j < NPT; ++j) {
-    const int i = tid + THREADS * j;
-    key[j] = (i < n) ? order_key(x[j]) : 0u;
-    if (i < n) mx = max(mx, key[j]);
-  }
+  for (int j = 0; j < NV; ++j)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const bool ok = elem_index<VEC>(g, j, e) < n;
+      key[j * VEC + e] = ok ? key[j * VEC + e] : 0u;      // masked tail: below every element
+      mx = ok ? max(mx, key[j * VEC + e]) : mx;
+    }
   sh.mx[tid] = mx;
-  if (tid == 0) sh.count = 0;
   __syncthreads();
-  if (tid < kWave) {
-    const uint32_t L = kth_largest_of_maxima(sh.mx, k);
-    if (tid == 0) sh.thr = L;
+  if (g < kWave) {                                        // first wave of each group
+    const uint32_t L = wave_kth_largest<4>(sh.mx + axis * GROUP, k);
+    if (lane == 0) sh.thr[axis] = L;
   }
   __syncthreads();
-  const uint32_t L = sh.thr;
+  const uint32_t L = sh.thr[axis];
+  int cnt = 0;
 #pragma unroll
-  for (int j = 0; j < NPT; ++j) {
-    const int i = tid + THREADS * j;
-    const bool pred = i < n && key[j] >= L;
-    const int pos = wave_append(pred, &sh.count);
-    if (pos >= 0 && pos < SMAX) comp[pos] = axis_comp(key[j], i);
-  }
-  __syncthreads();
-  const int S = sh.count;
-  if (S <= SMAX) {
-    for (int s = tid; s < S; s += THREADS) {
-      const uint64_t c = comp[s];
-      int r = 0;
-      for (int t = 0; t < S; ++t) r += comp[t] > c;
-      if (r < k) {
-        const int idx = static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(c & 0xFFFFFFFFull));
-        sh.ax_idx[axis][r] = idx;
+  for (int j = 0; j < NV; ++j)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) cnt += (elem_index<VEC>(g, j, e) < n) & (key[j * VEC + e] >= L);
+  const int2 ot = group_offsets(cnt, axis * 4, 4, sh);      // both groups at once
+  const bool overflow = ot.y > SMAX_AX;
+  if (g == 0) sh.cnt2[axis] = ot.y;
+  if (!overflow) {
+    int pos = ot.x;
+#pragma unroll
+    for (int j = 0; j < NV; ++j)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int i = elem_index<VEC>(g, j, e);
+        if ((i < n) & (key[j * VEC + e] >= L)) comp[pos++] = axis_comp(key[j * VEC + e], i);
       }
-    }
-  } else {
-    // fallback: exact radix select over all n keys, then order the k picked
-    uint32_t* keys = reinterpret_cast<uint32_t*>(dyn);
-    __syncthreads();
+  }
+  if (__syncthreads_or(overflow)) {
+    // Massive ties on one axis: the exact k-th largest key theta over all its elements, then
+    // the elements above it and the lowest-indexed elements equal to it.  Both groups run the
+    // loop (its barriers are shared); only an overflowing axis writes.
+    uint32_t prefix = 0u;
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t c = prefix | (1u << b);
+      int cl = 0;
 #pragma unroll
-    for (int j = 0; j < NPT; ++j) {
-      const int i = tid + THREADS * j;
-      if (i < n) keys[i] = key[j];
+      for (int j = 0; j < NE; ++j) cl += key[j] >= c;       // masked keys are 0
+      if (group_offsets(cl, axis * 4, 4, sh).y >= k) prefix = c;
     }
-    __syncthreads();
-    radix_select(keys, n, k, sh.tmp_pos, sh);
-    for (int a = tid; a < k; a += THREADS) sh.tmp_comp[a] = axis_comp(keys[sh.tmp_pos[a]], sh.tmp_pos[a]);
-    __syncthreads();
-    for (int a = tid; a < k; a += THREADS) {
-      const uint64_t c = sh.tmp_comp[a];
-      int r = 0;
-      for (int b = 0; b < k; ++b) r += sh.tmp_comp[b] > c;
-      sh.ax_idx[axis][r] = sh.tmp_pos[a];
+    const uint32_t theta = prefix;
+    int gl = 0;
+#pragma unroll
+    for (int j = 0; j < NE; ++j) gl += key[j] > theta;
+    const int need = k - group_offsets(gl, axis * 4, 4, sh).y;
+    int pos = 0, eq_seen = 0;
+    // element order: chunk j, then thread g, then e
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      int eq_l = 0;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) eq_l += (elem_index<VEC>(g, j, e) < n) & (key[j * VEC + e] == theta);
+      const int2 oe = group_offsets(eq_l, axis * 4, 4, sh);
+      int eq_rank = eq_seen + oe.x;
+      int take_l = 0;
+      bool take[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const bool ok = elem_index<VEC>(g, j, e) < n;
+        const bool eq = ok & (key[j * VEC + e] == theta);
+        take[e] = (ok & (key[j * VEC + e] > theta)) | (eq & (eq_rank < need));
+        eq_rank += eq;
+        take_l += take[e];
+      }
+      const int2 otk = group_offsets(take_l, axis * 4, 4, sh);
+      if (overflow) {
+        int p = pos + otk.x;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+          if (take[e]) comp[p++] = axis_comp(key[j * VEC + e], elem_index<VEC>(g, j, e));
+      }
+      pos += otk.y;
+      eq_seen += oe.y;
+    }
+    if (overflow && g == 0) sh.cnt2[axis] = k;
+  }
+  __syncthreads();
+  const int S = sh.cnt2[axis];
+  for (int s = g; s < S; s += GROUP) {
+    const uint64_t c = comp[s];
+    int r = 0;
+    int u = 0;
+    for (; u + 8 <= S; u += 8) {
+#pragma unroll
+      for (int v = 0; v < 8; ++v) r += comp[u + v] > c;
+    }
+    for (; u < S; ++u) r += comp[u] > c;
+    if (r < k) {
+      sh.ax_idx[axis][r] = static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(c & 0xFFFFFFFFull));
+      sh.ax_sc[axis][r] = key32_value(static_cast<uint32_t>(c >> 32));
     }
   }
   __syncthreads();
 }
 
-template <int NPT>
+// ---------------------------------------------------------------- top-m of candidates
+
+// Rank the S candidates (ckey desc, cid asc) with the whole workgroup; ranks < m by rank.
+__device__ __forceinline__ void rank_candidates(const uint64_t* ckey, const int32_t* cid, int S,
+                                                int m, SelectShared& sh) {
+  for (int s = threadIdx.x; s < S; s += THREADS) {
+    const uint64_t ks = ckey[s];
+    const int is = cid[s];
+    int r = 0;
+    int u = 0;
+    for (; u + 8 <= S; u += 8) {
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const uint64_t ku = ckey[u + v];
+        r += static_cast<int>(ku > ks) + static_cast<int>((ku == ks) & (cid[u + v] < is));
+      }
+    }
+    for (; u < S; ++u) {
+      const uint64_t ku = ckey[u];
+      r += static_cast<int>(ku > ks) + static_cast<int>((ku == ks) & (cid[u] < is));
+    }
+    if (r < m) {
+      sh.out_flat[r] = is;
+      sh.out_g[r] = key64_value(ks);
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- the kernel
+
+template <int NV, int VEC>
 __global__ __launch_bounds__(THREADS) void select_kernel(
     const float* __restrict__ sel, const float* __restrict__ q_row,
     const float* __restrict__ q_col, const float* __restrict__ k_row,
     const float* __restrict__ k_col, const float* __restrict__ core_all,
     int32_t* __restrict__ idx_out, float* __restrict__ w_out, int32_t* __restrict__ axis_out,
-    int T, int H, int n, int dk, int rank, int k, int m, int tucker, int softmax) {
+    int T, int H, int n, int dk, int rank, int k, int m, int tucker, int softmax, int n_cand) {
   extern __shared__ __align__(16) unsigned char dyn[];
   __shared__ SelectShared sh;
   const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
   const int t = blockIdx.x / H;
   const int h = blockIdx.x % H;
 
-  // both axes' selection scores, one memory round trip
-  float xr[NPT], xc[NPT];
-  const float* src_r = sel + ((static_cast<size_t>(0) * T + t) * H + h) * n;
-  const float* src_c = sel + ((static_cast<size_t>(1) * T + t) * H + h) * n;
-#pragma unroll
-  for (int j = 0; j < NPT; ++j) {
-    const int i = tid + THREADS * j;
-    xr[j] = (i < n) ? src_r[i] : 0.0f;
-    xc[j] = (i < n) ? src_c[i] : 0.0f;
-  }
+  // ---- a3: the two axes, four waves each
   if (tucker && tid < rank * rank) sh.core[tid] = core_all[static_cast<size_t>(h) * rank * rank + tid];
+  select_axes<NV, VEC>(sel, T, H, t, h, n, k, reinterpret_cast<uint64_t*>(dyn), sh);
+  if (axis_out != nullptr)
+    for (int a = tid; a < 2 * k; a += THREADS)
+      axis_out[((static_cast<size_t>(a / k) * T + t) * H + h) * k + a % k] = sh.ax_idx[a / k][a % k];
 
-  // ---- a3: per-axis top-k
-  select_axis<NPT>(xr, n, k, 0, sh, dyn);
-  select_axis<NPT>(xc, n, k, 1, sh, dyn);
-  for (int a = tid; a < 2 * k; a += THREADS) {
-    const int axis = a / k, r = a % k;
-    const float* src = axis ? src_c : src_r;
-    sh.ax_sc[axis][r] = src[sh.ax_idx[axis][r]];
-    if (axis_out != nullptr)
-      axis_out[((static_cast<size_t>(axis) * T + t) * H + h) * k + r] = sh.ax_idx[axis][r];
-  }
-  __syncthreads();
-
-  uint64_t* ckey = reinterpret_cast<uint64_t*>(dyn);                 // [SMAX] candidate keys
-  int32_t* cflat = reinterpret_cast<int32_t*>(dyn + SMAX * 8);       // [SMAX] candidate slots
-  if (tid == 0) sh.count = 0;
-  __syncthreads();
-
+  uint64_t* ckey = reinterpret_cast<uint64_t*>(dyn);         // candidates, after the axes
+  const int cap = tucker ? SMAX_S : n_cand;
+  int32_t* cid = reinterpret_cast<int32_t*>(ckey + cap);
+  int S;
   if (!tucker) {
-    // ---- a4 (additive): candidates with (a+1)(b+1) <= m, scores summed exactly in fp64
-    const int kk = k * k;
-    for (int c0 = 0; c0 < kk; c0 += THREADS) {
-      const int c = c0 + tid;
+    // ---- a4 (additive): (a, b) with a, b < k and (a+1)(b+1) <= m, scores exact in fp64
+    const int kk = min(k, m);
+    int cnt = 0;
+    for (int c = tid; c < kk * k; c += THREADS) cnt += ((c / k) + 1) * ((c % k) + 1) <= m;
+    const int2 o = group_offsets(cnt, 0, NWAVES, sh);
+    int pos = o.x;
+    for (int c = tid; c < kk * k; c += THREADS) {
       const int a = c / k, b = c - (c / k) * k;
-      const bool pred = c < kk && (a + 1) * (b + 1) <= m;
-      const int pos = wave_append(pred, &sh.count);
-      if (pos >= 0 && pos < SMAX) {   // at most m * H(k) < SMAX candidates (host-checked)
-        const double g = static_cast<double>(sh.ax_sc[0][a]) + static_cast<double>(sh.ax_sc[1][b]);
-        ckey[pos] = order_key64(g);
-        cflat[pos] = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
+      if ((a + 1) * (b + 1) <= m) {
+        ckey[pos] = order_key64(static_cast<double>(sh.ax_sc[0][a]) + static_cast<double>(sh.ax_sc[1][b]));
+        cid[pos] = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
+        ++pos;
       }
     }
     __syncthreads();
+    S = o.y;
   } else {
     // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32
     const int width = dk / rank;
@@ -324,89 +358,113 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       sh.p_col[rho][b] = p;
     }
     __syncthreads();
-    auto gscore = [&](int a, int b) {
-      double g = 0.0;
-      for (int rho = 0; rho < rank; ++rho) g += static_cast<double>(sh.s_ex[0][rho][a]) * sh.p_col[rho][b];
-      return g;
-    };
+    // candidate c = tid + 512 j (j < CPT) of the k*k grid, held in registers
     const int kk = k * k;
+    uint64_t k64[CPT];
+    uint32_t k32[CPT];
     uint32_t mx = 0u;
-    for (int c = tid; c < kk; c += THREADS) mx = max(mx, order_key(static_cast<float>(gscore(c / k, c % k))));
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int c = tid + THREADS * j;
+      k64[j] = 0ull;
+      k32[j] = 0u;
+      if (c < kk) {
+        const int a = c / k, b = c - (c / k) * k;
+        double gv = 0.0;
+        for (int rho = 0; rho < rank; ++rho) gv += static_cast<double>(sh.s_ex[0][rho][a]) * sh.p_col[rho][b];
+        k64[j] = order_key64(gv);
+        k32[j] = order_key(static_cast<float>(gv));
+        mx = max(mx, k32[j]);
+      }
+    }
     sh.mx[tid] = mx;
     __syncthreads();
-    if (tid < kWave) {
-      const uint32_t L = kth_largest_of_maxima(sh.mx, m);
-      if (tid == 0) sh.thr = L;
+    if (wave == 0) {
+      const uint32_t L = wave_kth_largest<8>(sh.mx, m);
+      if (lane == 0) sh.thr[0] = L;
     }
     __syncthreads();
-    const uint32_t L = sh.thr;
-    for (int c0 = 0; c0 < kk; c0 += THREADS) {
-      const int c = c0 + tid;
-      const int a = c / k, b = c - (c / k) * k;
-      double g = 0.0;
-      bool pred = false;
-      if (c < kk) {
-        g = gscore(a, b);
-        pred = order_key(static_cast<float>(g)) >= L;
-      }
-      const int pos = wave_append(pred, &sh.count);
-      if (pos >= 0 && pos < SMAX) {
-        ckey[pos] = order_key64(g);
-        cflat[pos] = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
-      }
-    }
-    __syncthreads();
-    if (sh.count > SMAX) {
-      // fallback: radix select on the fp32-rounded scores laid out in flat-index order
-      uint32_t* keys = reinterpret_cast<uint32_t*>(dyn);
-      for (int a = tid; a < 2 * k; a += THREADS) {
-        const int axis = a / k, r = a % k;
-        int p = 0;
-        for (int b = 0; b < k; ++b) p += sh.ax_idx[axis][b] < sh.ax_idx[axis][r];
-        sh.inv[axis][p] = r;
+    const uint32_t L = sh.thr[0];
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) cnt += (tid + THREADS * j < kk) & (k32[j] >= L);
+    const int2 o = group_offsets(cnt, 0, NWAVES, sh);
+    if (o.y <= SMAX_S) {
+      int pos = o.x;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        const int c = tid + THREADS * j;
+        if ((c < kk) & (k32[j] >= L)) {
+          ckey[pos] = k64[j];
+          cid[pos] = sh.ax_idx[0][c / k] * n + sh.ax_idx[1][c % k];
+          ++pos;
+        }
       }
       __syncthreads();
-      for (int c = tid; c < kk; c += THREADS)
-        keys[c] = order_key(static_cast<float>(gscore(sh.inv[0][c / k], sh.inv[1][c % k])));
-      __syncthreads();
-      radix_select(keys, kk, m, sh.tmp_pos, sh);
-      if (tid == 0) sh.count = m;
-      __syncthreads();
-      for (int j = tid; j < m; j += THREADS) {
-        const int c = sh.tmp_pos[j];
-        const int a = sh.inv[0][c / k], b = sh.inv[1][c % k];
-        ckey[j] = order_key64(gscore(a, b));
-        cflat[j] = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
+      S = o.y;
+    } else {
+      // Massive ties: exact m-th largest fp64 key theta, then the lowest flat indices among
+      // the candidates equal to it.
+      int32_t fl[CPT];
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        const int c = tid + THREADS * j;
+        fl[j] = c < kk ? sh.ax_idx[0][c / k] * n + sh.ax_idx[1][c % k] : 0x7FFFFFFF;
+      }
+      uint64_t prefix = 0ull;
+      for (int b = 63; b >= 0; --b) {
+        const uint64_t cb = prefix | (1ull << b);
+        int cl = 0;
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) cl += (tid + THREADS * j < kk) & (k64[j] >= cb);
+        if (group_offsets(cl, 0, NWAVES, sh).y >= m) prefix = cb;
+      }
+      const uint64_t theta = prefix;
+      int gl = 0;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) gl += (tid + THREADS * j < kk) & (k64[j] > theta);
+      const int need = m - group_offsets(gl, 0, NWAVES, sh).y;
+      uint32_t ylim = 0u;     // the need-th smallest flat index among the keys equal to theta
+      for (int b = 31; b >= 0; --b) {
+        const uint32_t cb = ylim | (1u << b);
+        int cl = 0;
+#pragma unroll
+        for (int j = 0; j < CPT; ++j)
+          cl += (tid + THREADS * j < kk) & (k64[j] == theta) & (static_cast<uint32_t>(fl[j]) < cb);
+        if (group_offsets(cl, 0, NWAVES, sh).y < need) ylim = cb;
+      }
+      int tk = 0;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        const bool ok = tid + THREADS * j < kk;
+        tk += ok & ((k64[j] > theta) | ((k64[j] == theta) & (static_cast<uint32_t>(fl[j]) <= ylim)));
+      }
+      const int2 ot = group_offsets(tk, 0, NWAVES, sh);
+      int pos = ot.x;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        const bool ok = tid + THREADS * j < kk;
+        if (ok & ((k64[j] > theta) | ((k64[j] == theta) & (static_cast<uint32_t>(fl[j]) <= ylim)))) {
+          ckey[pos] = k64[j];
+          cid[pos] = fl[j];
+          ++pos;
+        }
       }
       __syncthreads();
+      S = m;
     }
   }
 
   // ---- a5: rank the candidates by (score desc, flat index asc); ranks < m are the answer
-  const int C = sh.count;
-  for (int s = tid; s < C; s += THREADS) {
-    const uint64_t ks = ckey[s];
-    const int fs = cflat[s];
-    int r = 0;
-    for (int u = 0; u < C; ++u) {
-      const uint64_t ku = ckey[u];
-      r += (ku > ks) || (ku == ks && cflat[u] < fs);
-    }
-    if (r < m) {
-      sh.out_flat[r] = fs;
-      const uint64_t raw = (ks >> 63) ? (ks & 0x7FFFFFFFFFFFFFFFull) : ~ks;
-      sh.out_g[r] = __longlong_as_double(static_cast<long long>(raw));
-    }
-  }
-  __syncthreads();
+  rank_candidates(ckey, cid, S, m, sh);
   if (softmax) {
-    if (tid < m) sh.e[tid] = __expf(static_cast<float>(sh.out_g[tid] - sh.out_g[0]));
+    for (int j = tid; j < m; j += THREADS) sh.e[j] = __expf(static_cast<float>(sh.out_g[j] - sh.out_g[0]));
     __syncthreads();
-    if (tid < kWave) {
+    if (wave == 0) {
       float s = 0.0f;
-      for (int j = tid; j < m; j += kWave) s += sh.e[j];
+      for (int j = lane; j < m; j += kWave) s += sh.e[j];
       s = wave_sum(s);
-      if (tid == 0) sh.esum = s;
+      if (lane == 0) sh.esum = s;
     }
     __syncthreads();
   }
@@ -421,13 +479,14 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
 
 int additive_candidates(int k, int m) {
   int c = 0;
-  for (int a = 0; a < k; ++a) c += min(k, m / (a + 1));
+  for (int a = 0; a < k && a < m; ++a) c += min(k, m / (a + 1));
   return c;
 }
 
-size_t select_lds_bytes(int n, int k) {
-  size_t a = static_cast<size_t>(n) * 4, b = static_cast<size_t>(SMAX) * 12, c = static_cast<size_t>(k) * k * 4;
-  return a > b ? (a > c ? a : c) : (b > c ? b : c);
+size_t select_lds_bytes(int n_cand, int tucker) {
+  const size_t axes = 2 * static_cast<size_t>(SMAX_AX) * 8;
+  const size_t grid = static_cast<size_t>(tucker ? SMAX_S : n_cand) * (8 + 4);
+  return axes > grid ? axes : grid;
 }
 
 hipError_t launch_select(const umem_desc& d, int T, const float* sel, const float* q_row,
@@ -435,22 +494,37 @@ hipError_t launch_select(const umem_desc& d, int T, const float* sel, const floa
                          const float* core, int32_t* idx, float* w, int32_t* axis_idx,
                          hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (d.grid == UMEM_GRID_ADD && additive_candidates(d.topk, d.topm) > SMAX) return hipErrorInvalidValue;
-  const size_t lds = select_lds_bytes(d.n_keys, d.topk);
   const int tucker = d.grid == UMEM_GRID_TUCKER;
+  const int n_cand = tucker ? d.topk * d.topk : additive_candidates(d.topk, d.topm);
+  if (tucker && n_cand > KK_MAX) return hipErrorInvalidValue;
+  const size_t lds = select_lds_bytes(n_cand, tucker);
   const dim3 grid(static_cast<unsigned>(T) * d.heads), block(THREADS);
-#define UMEM_SELECT(NPT)                                                                          \
-  hipLaunchKernelGGL(select_kernel<NPT>, grid, block, lds, s, sel, q_row, q_col, k_row, k_col,   \
-                     core, idx, w, axis_idx, T, d.heads, d.n_keys, d.dk, d.rank, d.topk, d.topm,  \
-                     tucker, d.weight == UMEM_W_SOFTMAX)
-  const int npt = (d.n_keys + THREADS - 1) / THREADS;
-  if (npt <= 1) UMEM_SELECT(1);
-  else if (npt <= 2) UMEM_SELECT(2);
-  else if (npt <= 4) UMEM_SELECT(4);
-  else if (npt <= 8) UMEM_SELECT(8);
-  else if (npt <= 16) UMEM_SELECT(16);
-  else if (npt <= 32) UMEM_SELECT(32);
-  else return hipErrorInvalidValue;
+#define UMEM_SELECT(NV, VEC)                                                                      \
+  hipLaunchKernelGGL((select_kernel<NV, VEC>), grid, block, lds, s, sel, q_row, q_col, k_row,    \
+                     k_col, core, idx, w, axis_idx, T, d.heads, d.n_keys, d.dk, d.rank, d.topk,  \
+                     d.topm, tucker, d.weight == UMEM_W_SOFTMAX, n_cand)
+  const int n = d.n_keys;
+  if (n % 4 == 0) {
+    const int nv = (n + 1023) / 1024;
+    if (nv <= 1) UMEM_SELECT(1, 4);
+    else if (nv <= 2) UMEM_SELECT(2, 4);
+    else if (nv <= 3) UMEM_SELECT(3, 4);
+    else if (nv <= 4) UMEM_SELECT(4, 4);
+    else if (nv <= 5) UMEM_SELECT(5, 4);
+    else if (nv <= 6) UMEM_SELECT(6, 4);
+    else if (nv <= 8) UMEM_SELECT(8, 4);
+    else return hipErrorInvalidValue;
+  } else {
+    const int nv = (n + GROUP - 1) / GROUP;
+    if (nv <= 1) UMEM_SELECT(1, 1);
+    else if (nv <= 2) UMEM_SELECT(2, 1);
+    else if (nv <= 4) UMEM_SELECT(4, 1);
+    else if (nv <= 8) UMEM_SELECT(8, 1);
+    else if (nv <= 16) UMEM_SELECT(16, 1);
+    else if (nv <= 24) UMEM_SELECT(24, 1);
+    else if (nv <= 32) UMEM_SELECT(32, 1);
+    else return hipErrorInvalidValue;
+  }
 #undef UMEM_SELECT
   return hipGetLastError();
 }

@@ -42,6 +42,8 @@ umem_status check_desc(const umem_desc* d) {
     return UMEM_ERR_INVALID_ARG;
   if (d->topk > kMaxTopK || d->topk * d->topk > kMaxSelect || d->topm > kMaxTopM)
     return UMEM_ERR_UNSUPPORTED;
+  if (d->grid == UMEM_GRID_TUCKER && d->topk > kMaxTopKTucker) return UMEM_ERR_UNSUPPORTED;
+  if (d->grid == UMEM_GRID_ADD && additive_candidates(d->topk, d->topm) > 2048) return UMEM_ERR_UNSUPPORTED;
   if (d->rank > kMaxRank || (d->dk / d->rank) % 4 != 0 || d->dk > kMaxDk) return UMEM_ERR_UNSUPPORTED;
   if (d->heads > kMaxHeads || d->heads * d->topm > kMaxBag) return UMEM_ERR_UNSUPPORTED;
   if (d->expand > kMaxExpand) return UMEM_ERR_UNSUPPORTED;
@@ -191,7 +193,7 @@ UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* 
   if (st != UMEM_OK || T == 0) return st;
   if (st == UMEM_OK && desc->grid == UMEM_GRID_TUCKER)
     st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
-  if (st == UMEM_OK && (!sel || !idx || !w || !aligned(sel, 4) || !aligned(idx, 4) || !aligned(w, 4) ||
+  if (st == UMEM_OK && (!sel || !idx || !w || !aligned(sel, 16) || !aligned(idx, 4) || !aligned(w, 4) ||
                         !aligned(axis_idx, 4)))
     st = UMEM_ERR_INVALID_ARG;
   if (st != UMEM_OK) return st;

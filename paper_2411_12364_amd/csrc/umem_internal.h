@@ -11,6 +11,7 @@ namespace umem {
 constexpr int kWave = 64;            // CDNA wavefront width
 constexpr int kMaxSelect = 8192;     // max(n, k*k): one selection's keys in 32 KiB of LDS
 constexpr int kMaxTopK = 90;         // k*k <= kMaxSelect
+constexpr int kMaxTopKTucker = 64;   // Tucker: the k*k candidate keys in 16 KiB of LDS
 constexpr int kMaxTopM = 256;
 constexpr int kMaxRank = 4;
 constexpr int kMaxBag = 2048;
@@ -21,7 +22,7 @@ constexpr int kMaxDk = 1024;
 constexpr size_t kFactorBytes = static_cast<size_t>(kMaxHeads) * 2 * 4 * sizeof(float);
 
 bool gather_row_supported(int dv, int vdtype);
-size_t select_lds_bytes(int n, int k);
+size_t select_lds_bytes(int n_cand, int tucker);
 int additive_candidates(int k, int m);
 constexpr int kMaxRowBytes = 8192;
 

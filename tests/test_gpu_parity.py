@@ -261,3 +261,28 @@ def test_hip_graph_replay_matches_eager():
             assert torch.equal(wts[b], want[b][2])
         step(0)                     # eager work between replays
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("kw", [
+    dict(T=3, heads=2, n_keys=2048, topk=32, topm=32, dv=8, vdtype=CF.BF16),        # float4 loads
+    dict(T=2, heads=1, n_keys=1001, topk=20, topm=50, dv=8, vdtype=CF.BF16),        # scalar loads
+    dict(T=2, heads=2, n_keys=200, dk=64, rank=2, grid=CF.GRID_TUCKER, topk=40, topm=64, dv=8,
+         vdtype=CF.BF16),                                                            # 1600 tied candidates
+], ids=["axis-vec4", "axis-scalar", "tucker-grid"])
+def test_massive_ties_fallbacks(kw):
+    """All-zero queries: every score ties (as +0.0 or -0.0), far more survivors than the
+    threshold filter's buffers hold, so the exact fallbacks decide; ties go to lower indices."""
+    cfg = small("massive-ties", **kw)
+    dl = SD.make_layer(cfg)
+    z = np.zeros((cfg.T, cfg.heads, cfg.dk), np.float32)
+    dl.q_row = torch.from_numpy(z[None]).cuda()
+    dl.q_col = torch.from_numpy(z[None]).cuda()
+    idx, w, ax = G.score_topk(dl, cfg.T)
+    torch.cuda.synchronize()
+    kr, kc = CF.keys(cfg)
+    _, rep = P.check_selection(cfg, z, z, kr, kc, CF.core(cfg), G.host(idx), G.host(w), G.host(ax),
+                               gap=0.0)
+    log(f"[report] massive ties {kw}: {rep}")
+    assert rep["e2e_slot_mismatch"] == 0
+    # the lowest indices win: axis lists are 0..k-1
+    assert np.array_equal(G.host(ax)[:, :, :, :], np.broadcast_to(np.arange(cfg.topk), G.host(ax).shape))
