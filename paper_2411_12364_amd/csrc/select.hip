@@ -5,8 +5,8 @@
 // (score desc, index asc), in three steps:
 //
 //  1. Threshold.  Each thread holds its elements in registers and takes their maximum.  The
-//     k-th largest of the group's thread maxima, L, comes from a 32-step ballot search in one
-//     wave.  They are maxima of disjoint sets, so at least k elements are >= L: the k-th largest
+//     k-th largest of maxima of the group's threads (merged into one or two per lane), L, comes
+//     from a 32-step ballot search in one wave.  They are maxima of disjoint sets, so at least k elements are >= L: the k-th largest
 //     element is >= L, and every element of the top-k is >= L.
 //  2. Survivors {x >= L} (typically a few dozen) are compacted into LDS (wave scans in DPP).
 //  3. A survivor's rank is the number of survivors ordered before it; ranks < k are the answer,
@@ -101,22 +101,45 @@ __device__ __forceinline__ int2 group_offsets(int cnt, int w0, int nw, SelectSha
   return make_int2(base + incl - cnt, total);
 }
 
-// Largest L with at least k of the values vals[0, 64 V) >= L (run by one wave).
-template <int V>
-__device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t* vals, int k) {
-  const int lane = threadIdx.x & (kWave - 1);
-  uint32_t v[V];
-#pragma unroll
-  for (int q = 0; q < V; ++q) v[q] = vals[lane + kWave * q];
+// Largest L with at least k of the wave's 64 G values v[] >= L: a 32-step ballot search.
+template <int G>
+__device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&v)[G], int k) {
   uint32_t prefix = 0u;
   for (int b = 31; b >= 0; --b) {
     const uint32_t c = prefix | (1u << b);
     int cnt = 0;
 #pragma unroll
-    for (int q = 0; q < V; ++q) cnt += __popcll(__ballot(v[q] >= c));
+    for (int g = 0; g < G; ++g) cnt += __popcll(__ballot(v[g] >= c));
     if (cnt >= k) prefix = c;
   }
   return prefix;
+}
+
+// A valid threshold for a top-k from V maxima per lane (maxima of disjoint sets) in LDS:
+// lane-wise they are merged into G = ceil(k / 64) maxima of unions (still disjoint sets), and
+// L is the k-th largest of those 64 G values, so at least k elements are >= L.  One wave.
+template <int V>
+__device__ __forceinline__ uint32_t threshold_from_maxima(const uint32_t* vals, int k) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint32_t v[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) v[q] = vals[lane + kWave * q];
+  if (k <= kWave) {
+    uint32_t r[1] = {0u};
+#pragma unroll
+    for (int q = 0; q < V; ++q) r[0] = max(r[0], v[q]);
+    return wave_kth_largest<1>(r, k);
+  }
+  if (V >= 4 && k <= 2 * kWave) {
+    uint32_t r[2] = {0u, 0u};
+#pragma unroll
+    for (int q = 0; q < V; ++q) r[q & 1] = max(r[q & 1], v[q]);
+    return wave_kth_largest<2>(r, k);
+  }
+  uint32_t r[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int q = 0; q < V; ++q) r[q & 3] = max(r[q & 3], v[q]);
+  return wave_kth_largest<4>(r, k);
 }
 
 // ---------------------------------------------------------------- per-axis top-k
@@ -163,7 +186,7 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
   sh.mx[tid] = mx;
   __syncthreads();
   if (g < kWave) {                                        // first wave of each group
-    const uint32_t L = wave_kth_largest<4>(sh.mx + axis * GROUP, k);
+    const uint32_t L = threshold_from_maxima<4>(sh.mx + axis * GROUP, k);
     if (lane == 0) sh.thr[axis] = L;
   }
   __syncthreads();
@@ -241,8 +264,11 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
     int r = 0;
     int u = 0;
     for (; u + 8 <= S; u += 8) {
+      uint64_t b[8];
 #pragma unroll
-      for (int v = 0; v < 8; ++v) r += comp[u + v] > c;
+      for (int v = 0; v < 8; ++v) b[v] = comp[u + v];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) r += b[v] > c;
     }
     for (; u < S; ++u) r += comp[u] > c;
     if (r < k) {
@@ -255,25 +281,32 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
 
 // ---------------------------------------------------------------- top-m of candidates
 
-// Rank the S candidates (ckey desc, cid asc) with the whole workgroup; ranks < m by rank.
-__device__ __forceinline__ void rank_candidates(const uint64_t* ckey, const int32_t* cid, int S,
-                                                int m, SelectShared& sh) {
+// A candidate: its fp64 order key and its flat slot, in one 16-byte LDS record.
+struct Cand {
+  uint64_t key;
+  int32_t id;
+  int32_t pad;
+};
+
+__device__ __forceinline__ int before(const Cand& a, uint64_t ks, int is) {
+  return static_cast<int>(a.key > ks) + static_cast<int>((a.key == ks) & (a.id < is));
+}
+
+// Rank the S candidates (key desc, id asc) with the whole workgroup; ranks < m by rank.
+__device__ __forceinline__ void rank_candidates(const Cand* cand, int S, int m, SelectShared& sh) {
   for (int s = threadIdx.x; s < S; s += THREADS) {
-    const uint64_t ks = ckey[s];
-    const int is = cid[s];
+    const uint64_t ks = cand[s].key;
+    const int is = cand[s].id;
     int r = 0;
     int u = 0;
     for (; u + 8 <= S; u += 8) {
+      Cand b[8];
 #pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        const uint64_t ku = ckey[u + v];
-        r += static_cast<int>(ku > ks) + static_cast<int>((ku == ks) & (cid[u + v] < is));
-      }
+      for (int v = 0; v < 8; ++v) b[v] = cand[u + v];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) r += before(b[v], ks, is);
     }
-    for (; u < S; ++u) {
-      const uint64_t ku = ckey[u];
-      r += static_cast<int>(ku > ks) + static_cast<int>((ku == ks) & (cid[u] < is));
-    }
+    for (; u < S; ++u) r += before(cand[u], ks, is);
     if (r < m) {
       sh.out_flat[r] = is;
       sh.out_g[r] = key64_value(ks);
@@ -306,9 +339,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     for (int a = tid; a < 2 * k; a += THREADS)
       axis_out[((static_cast<size_t>(a / k) * T + t) * H + h) * k + a % k] = sh.ax_idx[a / k][a % k];
 
-  uint64_t* ckey = reinterpret_cast<uint64_t*>(dyn);         // candidates, after the axes
-  const int cap = tucker ? SMAX_S : n_cand;
-  int32_t* cid = reinterpret_cast<int32_t*>(ckey + cap);
+  Cand* cand = reinterpret_cast<Cand*>(dyn);                 // candidates, after the axes
   int S;
   if (!tucker) {
     // ---- a4 (additive): (a, b) with a, b < k and (a+1)(b+1) <= m, scores exact in fp64
@@ -320,13 +351,34 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     for (int c = tid; c < kk * k; c += THREADS) {
       const int a = c / k, b = c - (c / k) * k;
       if ((a + 1) * (b + 1) <= m) {
-        ckey[pos] = order_key64(static_cast<double>(sh.ax_sc[0][a]) + static_cast<double>(sh.ax_sc[1][b]));
-        cid[pos] = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
+        cand[pos].key = order_key64(static_cast<double>(sh.ax_sc[0][a]) + static_cast<double>(sh.ax_sc[1][b]));
+        cand[pos].id = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
         ++pos;
       }
     }
     __syncthreads();
     S = o.y;
+    // threshold on the fp32 roundings: per-thread maxima over candidates s = tid + 512 q
+    uint32_t mx = 0u;
+    for (int c = tid; c < S; c += THREADS) mx = max(mx, order_key(static_cast<float>(key64_value(cand[c].key))));
+    sh.mx[tid] = mx;
+    __syncthreads();
+    if (wave == 0) {
+      const uint32_t L = threshold_from_maxima<8>(sh.mx, m);
+      if (lane == 0) sh.thr[0] = L;
+    }
+    __syncthreads();
+    const uint32_t L = sh.thr[0];
+    Cand* surv = cand + S;
+    int sc = 0;
+    for (int c = tid; c < S; c += THREADS) sc += order_key(static_cast<float>(key64_value(cand[c].key))) >= L;
+    const int2 os = group_offsets(sc, 0, NWAVES, sh);
+    int sp = os.x;
+    for (int c = tid; c < S; c += THREADS)
+      if (order_key(static_cast<float>(key64_value(cand[c].key))) >= L) surv[sp++] = cand[c];
+    __syncthreads();
+    cand = surv;
+    S = os.y;
   } else {
     // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32
     const int width = dk / rank;
@@ -380,7 +432,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     sh.mx[tid] = mx;
     __syncthreads();
     if (wave == 0) {
-      const uint32_t L = wave_kth_largest<8>(sh.mx, m);
+      const uint32_t L = threshold_from_maxima<8>(sh.mx, m);
       if (lane == 0) sh.thr[0] = L;
     }
     __syncthreads();
@@ -395,8 +447,8 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       for (int j = 0; j < CPT; ++j) {
         const int c = tid + THREADS * j;
         if ((c < kk) & (k32[j] >= L)) {
-          ckey[pos] = k64[j];
-          cid[pos] = sh.ax_idx[0][c / k] * n + sh.ax_idx[1][c % k];
+          cand[pos].key = k64[j];
+          cand[pos].id = sh.ax_idx[0][c / k] * n + sh.ax_idx[1][c % k];
           ++pos;
         }
       }
@@ -445,8 +497,8 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       for (int j = 0; j < CPT; ++j) {
         const bool ok = tid + THREADS * j < kk;
         if (ok & ((k64[j] > theta) | ((k64[j] == theta) & (static_cast<uint32_t>(fl[j]) <= ylim)))) {
-          ckey[pos] = k64[j];
-          cid[pos] = fl[j];
+          cand[pos].key = k64[j];
+          cand[pos].id = fl[j];
           ++pos;
         }
       }
@@ -456,7 +508,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
   }
 
   // ---- a5: rank the candidates by (score desc, flat index asc); ranks < m are the answer
-  rank_candidates(ckey, cid, S, m, sh);
+  rank_candidates(cand, S, m, sh);
   if (softmax) {
     for (int j = tid; j < m; j += THREADS) sh.e[j] = __expf(static_cast<float>(sh.out_g[j] - sh.out_g[0]));
     __syncthreads();
@@ -485,7 +537,7 @@ int additive_candidates(int k, int m) {
 
 size_t select_lds_bytes(int n_cand, int tucker) {
   const size_t axes = 2 * static_cast<size_t>(SMAX_AX) * 8;
-  const size_t grid = static_cast<size_t>(tucker ? SMAX_S : n_cand) * (8 + 4);
+  const size_t grid = static_cast<size_t>(tucker ? SMAX_S : 2 * n_cand) * sizeof(Cand);
   return axes > grid ? axes : grid;
 }
 
