@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 256 MiB device copy three times (a known-size kernel "
+                         "for scaling HBM traffic counters)")
     ap.add_argument("--eager", action="store_true",
                     help="launch each step from Python instead of replaying a captured HIP graph")
     return ap.parse_args()
@@ -304,6 +307,14 @@ def main():
     from synth import configs as CF
     cfg = CF.C3
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 x 256 MiB device copies done")
+        del a, b
     r = Runner(cfg, args.batches)
     secs, n = r.time_forward(args.steps, args.warmup, graph=not args.eager)
     ms = secs / n * 1e3
