@@ -18,7 +18,9 @@
  *     (`ws`, sized by umem_workspace_size).
  *   - Calls are asynchronous.  The returned status covers argument validation and launch
  *     errors only.  On any error nothing is enqueued and no output is written.  Device-side
- *     faults (e.g. an index out of range in a caller-supplied bag) are not detected.
+ *     faults (e.g. an index out of range in a caller-supplied bag) are not detected.  A HIP
+ *     error that an earlier call left pending in the calling thread is cleared, unreported,
+ *     before a call launches its kernels.
  *   - Ties: every selection orders by (score desc, index asc) -- the per-axis key index, or the
  *     logical flat index i*n + j on the grid; -0.0 equals +0.0; NaN ranks below -inf.
  *     Selections are returned sorted in that order.

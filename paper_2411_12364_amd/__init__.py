@@ -12,6 +12,12 @@ from __future__ import annotations
 import ctypes
 import os
 
+# torch first: its HIP runtime (libamdhip64.so, SONAME libamdhip64.so.7) must be the one in the
+# process before libumem.so is loaded, so that libumem.so binds to it.  Loaded the other way
+# round, torch would bring in a second copy of the runtime, and the two would not share
+# devices, streams or allocations.
+import torch  # noqa: F401
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libumem.so")
 
@@ -86,7 +92,6 @@ def _p(x):
 
 def _s(stream):
     if stream is None:
-        import torch
         return torch.cuda.current_stream().cuda_stream
     if isinstance(stream, int):
         return stream

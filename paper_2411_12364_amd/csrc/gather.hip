@@ -1,12 +1,13 @@
 // a6 + a7: score-weighted gather-sum of value rows (embedding bag), eq. (1) and eq. (15).
 //
-// One workgroup per token.  A value row is read with 16-byte loads, L lanes per row and CPL
-// 16-byte chunks per lane (row bytes = 16 * L * CPL); a wave keeps U rows in flight, so a
-// workgroup has 4 * U rows outstanding.  Accumulation is fp32 in registers; partial sums of the
-// sub-rows of a wave are combined with shuffles and those of the 4 waves in LDS, in a fixed
-// order (the result does not depend on timing).  With implicit value expansion the bag is first
-// split by virtual block p (a stable partition, order within a block kept) and each block's
-// rows are pooled into out[t, p, :].
+// One workgroup of four waves per token; each wave pools a contiguous quarter of the bag.  A
+// value row is read once, with 16-byte nontemporal loads (the rows are not reused), L lanes per
+// row and CPL 16-byte chunks per lane (row bytes = 16 * L * CPL); a wave keeps U rows in
+// flight.  Accumulation is fp32 in registers; the sub-rows of a wave are combined with
+// shuffles, and the four waves' partial rows in LDS behind one barrier, always in wave order
+// (the result does not depend on timing).  With implicit value expansion the bag is first
+// mapped through the shuffle and split by virtual block p (a stable partition), and each
+// block's rows are pooled into out[t, p, :].
 #include "umem_internal.h"
 
 namespace umem {
@@ -43,128 +44,161 @@ struct ElemTraits<uint16_t> {   // bf16 bit patterns
   }
 };
 
+// Rows of one bag (or of one virtual block of it) are split into NWAVES contiguous ranges, one
+// per wave; sub-group `sub` of a wave (L lanes) reads entries beg + SUB * i + sub of its range.
+// `slot(j)` gives entry j's position in idx / w (after the block partition, if any).
+template <typename Elem, int L, int CPL, typename Slot>
+__device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int dv, int cnt,
+                                          const Slot& slot, const int32_t* __restrict__ rows_of,
+                                          const float* __restrict__ w_of, float* red,
+                                          float* __restrict__ dst) {
+  using TR = ElemTraits<Elem>;
+  constexpr int EPC = TR::kPerChunk;
+  constexpr int SUB = kWave / L;                   // rows a wave reads at once
+  constexpr int U = (CPL >= 16) ? 1 : 16 / CPL;    // row batches in flight per wave
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int sub = lane / L;
+  const int cl = lane % L;
+  const int per_wave = (cnt + NWAVES - 1) / NWAVES;
+  const int wbeg = wave * per_wave;
+  const int wend = min(cnt, wbeg + per_wave);
+
+  float acc[CPL][EPC];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[c][e] = 0.0f;
+  for (int j0 = wbeg; j0 < wend; j0 += SUB * U) {
+    u32x4 raw[U][CPL];
+    float wt[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + SUB * u + sub;
+      if (j < wend) {
+        const int s = slot(j);
+        wt[u] = w_of[s];
+        const Elem* src = values + static_cast<int64_t>(rows_of[s]) * dv;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+          raw[u][c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + (cl + L * c) * EPC));
+      } else {
+        wt[u] = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) raw[u][c] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        float x[EPC];
+        TR::widen(raw[u][c], x);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[c][e] = fmaf(wt[u], x[e], acc[c][e]);
+      }
+  }
+  // combine the SUB sub-rows of this wave (lanes cl, cl + L, ...) with shuffles
+#pragma unroll
+  for (int off = L; off < kWave; off <<= 1)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[c][e] += __shfl_xor(acc[c][e], off, kWave);
+  // The waves' partial rows meet in LDS and every thread adds, in wave order, the partials of
+  // its columns, then stores them.  Rows of up to 2048 elements use NWAVES partial rows; longer
+  // rows (up to 4096) first fold waves 2, 3 into 0, 1, within half the space.
+  const bool one_stage = dv <= 2048;
+  if (sub == 0 && (one_stage || wave >= 2)) {
+    float* r = red + (one_stage ? wave : wave - 2) * dv;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4)
+        *reinterpret_cast<float4*>(r + (cl + L * c) * EPC + e) =
+            make_float4(acc[c][e], acc[c][e + 1], acc[c][e + 2], acc[c][e + 3]);
+  }
+  __syncthreads();
+  if (!one_stage) {
+    if (sub == 0 && wave < 2) {
+      float* r = red + wave * dv;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+#pragma unroll
+        for (int e = 0; e < EPC; e += 4) {
+          float4* q = reinterpret_cast<float4*>(r + (cl + L * c) * EPC + e);
+          const float4 x = *q;
+          *q = make_float4(acc[c][e] + x.x, acc[c][e + 1] + x.y, acc[c][e + 2] + x.z, acc[c][e + 3] + x.w);
+        }
+    }
+    __syncthreads();
+  }
+  const int parts = one_stage ? NWAVES : 2;
+  for (int col = tid * 4; col < dv; col += THREADS * 4) {
+    float4 r = *reinterpret_cast<const float4*>(red + col);
+    for (int v = 1; v < parts; ++v) {
+      const float4 x = *reinterpret_cast<const float4*>(red + v * dv + col);
+      r.x += x.x;
+      r.y += x.y;
+      r.z += x.z;
+      r.w += x.w;
+    }
+    *reinterpret_cast<float4*>(dst + col) = r;
+  }
+}
+
+// Without expansion the bag is read straight from idx / w (for rows of 64 lanes a wave's row
+// index is uniform and lives in scalar registers).  With expansion the bag is first mapped
+// through perm and stably partitioned by virtual block in LDS.
 template <typename Elem, int L, int CPL>
 __global__ __launch_bounds__(THREADS) void gather_kernel(
     const Elem* __restrict__ values, int64_t n_values, int dv, int bag,
     const int32_t* __restrict__ idx, const float* __restrict__ w, const int32_t* __restrict__ perm,
     int expand, float* __restrict__ out) {
-  using TR = ElemTraits<Elem>;
-  constexpr int EPC = TR::kPerChunk;
-  constexpr int SUB = kWave / L;                   // rows a wave reads at once
-  constexpr int U = (CPL >= 16) ? 1 : 16 / CPL;    // row batches in flight per wave
-  extern __shared__ int32_t smem[];
-  int32_t* rows = smem;                            // [bag]
-  float* wts = reinterpret_cast<float*>(smem + bag);   // [bag]
-  int32_t* blk = smem + 2 * bag;                   // [bag]
-  int32_t* order = smem + 3 * bag;                 // [bag]
-  float* red = reinterpret_cast<float*>(smem + 4 * bag);   // [dv]
-  __shared__ int bstart[65], bcount[64];
-
+  extern __shared__ __align__(16) float red[];               // [red_rows][dv], then the bag
   const int t = blockIdx.x;
+  const int32_t* __restrict__ idx_t = idx + static_cast<size_t>(t) * bag;
+  const float* __restrict__ w_t = w + static_cast<size_t>(t) * bag;
+  if (expand == 1) {
+    pool_rows<Elem, L, CPL>(values, dv, bag, [](int j) { return j; }, idx_t, w_t, red,
+                            out + static_cast<size_t>(t) * dv);
+    return;
+  }
+  int32_t* rows = reinterpret_cast<int32_t*>(red + (dv <= 2048 ? NWAVES : 2) * dv);   // [bag]
+  int32_t* blk = rows + bag;                                       // [bag]
+  int32_t* order = blk + bag;                                      // [bag]
+  __shared__ int bstart[kMaxExpand + 1], bcount[kMaxExpand];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
-  const int sub = lane / L;
-  const int cl = lane % L;
-
   for (int s = tid; s < bag; s += THREADS) {
-    const int64_t x = idx[static_cast<size_t>(t) * bag + s];
-    const int64_t v = perm ? static_cast<int64_t>(perm[x]) : x;
-    const int p = expand > 1 ? static_cast<int>(v / n_values) : 0;
+    const int64_t v = static_cast<int64_t>(perm[idx_t[s]]);
+    const int p = static_cast<int>(v / n_values);
     rows[s] = static_cast<int32_t>(v - static_cast<int64_t>(p) * n_values);
-    wts[s] = w[static_cast<size_t>(t) * bag + s];
     blk[s] = p;
   }
   __syncthreads();
-  if (expand > 1) {
-    if (wave == 0) {
-      const uint64_t lt = lanemask_lt();
-      int pos = 0;
-      for (int p = 0; p < expand; ++p) {
-        if (lane == 0) bstart[p] = pos;
-        for (int base = 0; base < bag; base += kWave) {
-          const int s = base + lane;
-          const bool hit = s < bag && blk[s] == p;
-          const uint64_t m = __ballot(hit);
-          if (hit) order[pos + __popcll(m & lt)] = s;
-          pos += __popcll(m);
-        }
-        if (lane == 0) bcount[p] = pos - bstart[p];
+  if (wave == 0) {
+    const uint64_t lt = lanemask_lt();
+    int pos = 0;
+    for (int p = 0; p < expand; ++p) {
+      if (lane == 0) bstart[p] = pos;
+      for (int base = 0; base < bag; base += kWave) {
+        const int s = base + lane;
+        const bool hit = s < bag && blk[s] == p;
+        const uint64_t m = __ballot(hit);
+        if (hit) order[pos + __popcll(m & lt)] = s;
+        pos += __popcll(m);
       }
-    }
-  } else {
-    for (int s = tid; s < bag; s += THREADS) order[s] = s;
-    if (tid == 0) {
-      bstart[0] = 0;
-      bcount[0] = bag;
+      if (lane == 0) bcount[p] = pos - bstart[p];
     }
   }
   __syncthreads();
-
-  const int row_elems = dv;
   for (int p = 0; p < expand; ++p) {
     const int beg = bstart[p];
-    const int cnt = bcount[p];
-    float acc[CPL][EPC];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c)
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[c][e] = 0.0f;
-
-    // rows j = wave*SUB + sub + (NWAVES*SUB) * i
-    constexpr int STEP = NWAVES * SUB;
-    for (int j0 = wave * SUB + sub; j0 < cnt; j0 += STEP * U) {
-      u32x4 raw[U][CPL];
-      float wt[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int j = j0 + u * STEP;
-        if (j < cnt) {
-          const int s = order[beg + j];
-          wt[u] = wts[s];
-          const Elem* src = values + static_cast<int64_t>(rows[s]) * row_elems;
-#pragma unroll
-          for (int c = 0; c < CPL; ++c)
-            raw[u][c] = *reinterpret_cast<const u32x4*>(src + (cl + L * c) * EPC);
-        } else {
-          wt[u] = 0.0f;
-#pragma unroll
-          for (int c = 0; c < CPL; ++c) raw[u][c] = u32x4{0u, 0u, 0u, 0u};
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-          float x[EPC];
-          TR::widen(raw[u][c], x);
-#pragma unroll
-          for (int e = 0; e < EPC; ++e) acc[c][e] = fmaf(wt[u], x[e], acc[c][e]);
-        }
-    }
-    // combine the SUB sub-rows of this wave (lanes cl, cl + L, ...) with shuffles
-#pragma unroll
-    for (int off = L; off < kWave; off <<= 1)
-#pragma unroll
-      for (int c = 0; c < CPL; ++c)
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) acc[c][e] += __shfl_xor(acc[c][e], off, kWave);
-    // combine the waves in LDS, wave 0 first
-    for (int v = 0; v < NWAVES; ++v) {
-      if (wave == v && sub == 0) {
-#pragma unroll
-        for (int c = 0; c < CPL; ++c)
-#pragma unroll
-          for (int e = 0; e < EPC; ++e) {
-            const int col = (cl + L * c) * EPC + e;
-            red[col] = (v == 0) ? acc[c][e] : red[col] + acc[c][e];
-          }
-      }
-      __syncthreads();
-    }
-    float* dst = out + (static_cast<size_t>(t) * expand + p) * dv;
-    for (int col = tid * 4; col < dv; col += THREADS * 4)
-      *reinterpret_cast<float4*>(dst + col) = *reinterpret_cast<const float4*>(red + col);
+    pool_rows<Elem, L, CPL>(values, dv, bcount[p], [=](int j) { return order[beg + j]; }, rows,
+                            w_t, red, out + (static_cast<size_t>(t) * expand + p) * dv);
     __syncthreads();
   }
 }
@@ -174,7 +208,8 @@ hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int
                         const int32_t* idx, const float* w, const int32_t* perm, int expand,
                         float* out, hipStream_t s) {
   const int chunks = dv * static_cast<int>(sizeof(Elem)) / 16;
-  const size_t lds = static_cast<size_t>(bag) * 16 + static_cast<size_t>(dv) * 4;
+  const size_t lds = static_cast<size_t>(dv <= 2048 ? NWAVES : 2) * dv * 4 +
+                    (expand > 1 ? static_cast<size_t>(bag) * 12 : 0);
   const dim3 grid(T), block(THREADS);
 #define UMEM_GATHER(LL, CC)                                                                  \
   hipLaunchKernelGGL((gather_kernel<Elem, LL, CC>), grid, block, lds, s, values, n_values, dv, \
@@ -213,6 +248,7 @@ bool gather_row_supported(int dv, int vdtype) {
 hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* values, int T,
                          int bag, const int32_t* idx, const float* w, const int32_t* perm,
                          int expand, float* out, hipStream_t s) {
+  clear_stale_error();
   if (T == 0) return hipSuccess;
   if (vdtype == UMEM_F32)
     return launch_typed(static_cast<const float*>(values), n_values, dv, T, bag, idx, w, perm,

@@ -101,6 +101,7 @@ hipError_t gemm(const float* A, const uint16_t* B, float* C, int M, int N, int K
 hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const float* pooled,
                           const uint16_t* w_proj, const uint16_t* w_out, float* out, float* tmp,
                           hipStream_t s) {
+  clear_stale_error();
   if (T == 0) return hipSuccess;
   if (w_out == nullptr) return gemm(pooled, w_proj, out, T, dv_virt, expand * dv, s);
   hipError_t e = gemm(pooled, w_proj, tmp, T, dv_virt, expand * dv, s);

@@ -234,6 +234,7 @@ __global__ void rank1_kernel(const float* __restrict__ core, int H, int r, float
 }
 
 hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, hipStream_t s) {
+  clear_stale_error();
   hipLaunchKernelGGL(rank1_kernel, dim3(1), dim3(kWave), 0, s, core, d.heads, d.rank, factors);
   return hipGetLastError();
 }
@@ -241,6 +242,7 @@ hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, h
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
                               const float* k_row, const float* k_col, const float* factors,
                               float* sel, hipStream_t s) {
+  clear_stale_error();
   if (T == 0) return hipSuccess;
   const float* c = (d.grid == UMEM_GRID_TUCKER) ? factors : nullptr;
   const int width = d.dk / d.rank;

@@ -545,6 +545,7 @@ hipError_t launch_select(const umem_desc& d, int T, const float* sel, const floa
                          const float* q_col, const float* k_row, const float* k_col,
                          const float* core, int32_t* idx, float* w, int32_t* axis_idx,
                          hipStream_t s) {
+  clear_stale_error();
   if (T == 0) return hipSuccess;
   const int tucker = d.grid == UMEM_GRID_TUCKER;
   const int n_cand = tucker ? d.topk * d.topk : additive_candidates(d.topk, d.topm);

@@ -30,6 +30,10 @@ constexpr int kMaxRowBytes = 8192;
 
 // Tucker grid: leading singular pair of every head's core, factors[h][0] = u, factors[h][1] = t,
 // each padded to kMaxRank floats.
+// Launchers report hipGetLastError() after their launches; an error that an earlier, unrelated
+// HIP call left in the calling thread is cleared first, so that it is not taken for theirs.
+inline void clear_stale_error() { (void)hipGetLastError(); }
+
 hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, hipStream_t s);
 
 // Selection scores; factors is the output of launch_rank1 (Tucker) or NULL (additive).

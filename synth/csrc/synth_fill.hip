@@ -47,6 +47,7 @@ __global__ void fill_kernel(uint64_t key, float scale, uint64_t start, int64_t c
 
 }  // namespace
 
+// Returns 0, -1 for bad arguments, or -(1000 + hipError_t) when the launch fails.
 extern "C" __attribute__((visibility("default"))) int synth_fill_normal(
     uint64_t key, float scale, uint64_t start, int64_t count, int bf16, void* dst,
     hipStream_t stream) {
@@ -54,7 +55,9 @@ extern "C" __attribute__((visibility("default"))) int synth_fill_normal(
   if (count == 0) return 0;
   const int64_t groups = (count + 7) / 8;
   const int64_t blocks = (groups + 255) / 256 < 65536 ? (groups + 255) / 256 : 65536;
+  (void)hipGetLastError();     // an error left pending by an earlier call is not this launch's
   hipLaunchKernelGGL(fill_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, key,
                      scale, start, count, bf16, dst);
-  return hipGetLastError() == hipSuccess ? 0 : -4;
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? 0 : -(1000 + static_cast<int>(e));
 }

@@ -51,7 +51,8 @@ def fill_normal_(t: torch.Tensor, seed: int, tensor_id: int, std: float, start: 
         cnt = min(chunk, n - off)
         st = lib.synth_fill_normal(key, scale, start + off, cnt, bf16, t.data_ptr() + off * esize, stream)
         if st != 0:
-            raise RuntimeError(f"synth_fill_normal failed ({st})")
+            what = f"HIP error {-st - 1000}" if st <= -1000 else "invalid arguments"
+            raise RuntimeError(f"synth_fill_normal failed: {what} (status {st})")
     return t
 
 

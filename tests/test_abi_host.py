@@ -122,3 +122,11 @@ def test_zero_tokens_is_a_noop():
     assert U.umem_score_topk(d, 0, None, None, None, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
     assert U.umem_forward(d, 0, None, None, None, None, None, None, None, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
     assert U.umem_gather_sum(100, 512, 1, None, 0, 64, None, None, None, 1, None, 0) == U.UMEM_OK
+
+
+def test_one_hip_runtime_in_process():
+    """The binding loads torch's HIP runtime before libumem.so, so the process maps a single
+    libamdhip64 (two copies would not share devices, streams or memory)."""
+    with open("/proc/self/maps") as f:
+        paths = {line.split()[-1] for line in f if "libamdhip64" in line}
+    assert len({os.path.realpath(p) for p in paths}) == 1, paths
