@@ -220,8 +220,40 @@ class Runner:
             "gather_kernel": self._graph_time([lambda b=b: self.gather(idxs[b % self.R], ws_[b % self.R])
                                                for b in range(n)]),
         }
+        self.queue = self._time_gather_queue(idxs, ws_)
         del sels, idxs, ws_
         return {k: v * 1e6 for k, v in out.items()}
+
+    def _time_gather_queue(self, idxs, ws_):
+        """The gather of many queued decode steps in one launch: the selections of R/2 distinct
+        query batches (R/2 * T tokens) pooled by one umem_gather_sum, alternating between the
+        two halves of the R batches so that consecutive launches read different rows."""
+        torch, U, dl, c = self.torch, self.U, self.dl, self.cfg
+        half = self.R // 2
+        if half < 2:
+            return None
+        Tq = half * c.T
+        stacks = [(idxs[i * half:(i + 1) * half].reshape(Tq, c.bag), ws_[i * half:(i + 1) * half].reshape(Tq, c.bag))
+                  for i in (0, 1)]
+        outq = torch.empty((Tq, c.expand, c.dv), dtype=torch.float32, device="cuda")
+
+        def launch(i):
+            st = U.umem_gather_sum(c.n_values, c.dv, c.vdtype, dl.values, Tq, c.bag, stacks[i][0],
+                                   stacks[i][1], dl.perm, c.expand, outq)
+            if st:
+                U.check(st, "umem_gather_sum")
+        secs = self._graph_time([lambda i=i: launch(i % 2) for i in range(16)])
+        rows = Tq * c.bag * c.dv * c.vbytes
+        algo = kernel_work(c.with_tokens(Tq), Tq)["gather_kernel"]["bytes"]   # + bag, + output
+        uniq = int(torch.unique(stacks[0][0]).numel())
+        del outq, stacks
+        return dict(tokens_per_launch=Tq, decode_steps_per_launch=half,
+                    row_bytes_per_launch=rows, unique_row_bytes=uniq * c.dv * c.vbytes,
+                    algorithmic_bytes_per_launch=algo,
+                    avg_us=round(secs * 1e6, 3), GBps=round(rows / secs / 1e9, 1),
+                    frac_of_peak=round(rows / secs / 1e9 / HBM_PEAK_GBS, 4),
+                    algorithmic_GBps=round(algo / secs / 1e9, 1),
+                    algorithmic_frac_of_peak=round(algo / secs / 1e9 / HBM_PEAK_GBS, 4))
 
 
 def roofline_for(cfg, T, name, avg_us, workload):
@@ -330,6 +362,8 @@ def main():
     gather = dict(row_bytes_per_launch=work["gather_kernel"]["row_bytes"], avg_us=round(g_us, 3),
                   GBps=round(work["gather_kernel"]["row_bytes"] / (g_us * 1e-6) / 1e9, 1))
     gather["frac_of_peak"] = round(gather["GBps"] / HBM_PEAK_GBS, 4)
+    queue = r.queue
+    log(f"gather of queued decode steps: {queue}")
     values = r.dl.values
     del r
     sw = None if args.no_sweep else sweep(cfg, values)
@@ -348,6 +382,7 @@ def main():
         "kernel_us": {k: round(v, 3) for k, v in stage_us.items()},
         "eager_us_per_step": round(eager_us, 3),
         "gather": gather,
+        "gather_queue": queue,
         "batch_sweep": sw,
         "cpu_baseline": cpu,
     }

@@ -5,9 +5,11 @@
 // row and CPL 16-byte chunks per lane (row bytes = 16 * L * CPL); a wave keeps U rows in
 // flight.  Accumulation is fp32 in registers; the sub-rows of a wave are combined with
 // shuffles, and the four waves' partial rows in LDS behind one barrier, always in wave order
-// (the result does not depend on timing).  With implicit value expansion the bag is first
-// mapped through the shuffle and split by virtual block p (a stable partition), and each
-// block's rows are pooled into out[t, p, :].
+// (the result does not depend on timing).  Pooled rows are written with nontemporal stores:
+// they are not read again here, and the read stream suffers less from them.  With implicit
+// value expansion the bag is first mapped through the shuffle and split by virtual block p (a
+// stable partition), and each block's rows are pooled into out[t, p, :].  From 2048 tokens on
+// (without expansion) a wave per token does the same work without LDS or barriers.
 #include "umem_internal.h"
 
 namespace umem {
@@ -15,7 +17,16 @@ namespace {
 
 constexpr int THREADS = 256;
 constexpr int NWAVES = THREADS / kWave;
+#ifndef UMEM_GATHER_WAVE_TOKENS
+#define UMEM_GATHER_WAVE_TOKENS 2048
+#endif
+constexpr int kWaveTokensMin = UMEM_GATHER_WAVE_TOKENS;   // from here on, a wave per token
+#ifndef UMEM_GATHER_WAVE_BATCH
+#define UMEM_GATHER_WAVE_BATCH 8
+#endif
+constexpr int kWaveBatch = UMEM_GATHER_WAVE_BATCH;       // 16-byte loads per lane per batch
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <typename Elem>
 struct ElemTraits;
@@ -144,7 +155,7 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
       r.z += x.z;
       r.w += x.w;
     }
-    *reinterpret_cast<float4*>(dst + col) = r;
+    __builtin_nontemporal_store(f32x4{r.x, r.y, r.z, r.w}, reinterpret_cast<f32x4*>(dst + col));
   }
 }
 
@@ -203,6 +214,101 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
   }
 }
 
+// Many tokens without expansion: one wave per token, which reads the token's whole bag itself
+// and needs no LDS and no barrier.  The bag's indices and weights are loaded 64 at a time, one
+// per lane, and each row's index taken from its lane (readlane; a shuffle for sub-rows); the
+// row loads run double-buffered, batch b + 1 in flight while batch b accumulates.  With
+// thousands of tokens the CUs hold many such waves at once.
+template <typename Elem, int L, int CPL>
+__global__ __launch_bounds__(THREADS) void gather_wave_kernel(
+    const Elem* __restrict__ values, int dv, int T, int bag, const int32_t* __restrict__ idx,
+    const float* __restrict__ w, float* __restrict__ out) {
+  using TR = ElemTraits<Elem>;
+  constexpr int EPC = TR::kPerChunk;
+  constexpr int SUB = kWave / L;
+  constexpr int U = (CPL >= kWaveBatch) ? 1 : kWaveBatch / CPL;   // row steps per batch
+  constexpr int BATCH = SUB * U;                       // rows per batch (divides 64)
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t = blockIdx.x * NWAVES + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  if (t >= T) return;
+  const int sub = lane / L;
+  const int cl = lane % L;
+  const int32_t* __restrict__ idx_t = idx + static_cast<size_t>(t) * bag;
+  const float* __restrict__ w_t = w + static_cast<size_t>(t) * bag;
+  float acc[CPL][EPC];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[c][e] = 0.0f;
+
+  u32x4 buf0[U][CPL], buf1[U][CPL];
+  float wt0[U], wt1[U];
+  for (int base = 0; base < bag; base += kWave) {
+    const int n_here = min(kWave, bag - base);           // entries of this chunk
+    const int my_row = lane < n_here ? idx_t[base + lane] : 0;
+    const float my_w = lane < n_here ? w_t[base + lane] : 0.0f;
+    const int nb = (n_here + BATCH - 1) / BATCH;
+    // rows of batch b: chunk entries b * BATCH + SUB * u + sub
+    auto issue = [&](int b, u32x4 (&bb)[U][CPL], float (&ww)[U]) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jl = b * BATCH + SUB * u;               // uniform part of the entry
+        int row;
+        float wj;
+        if (SUB == 1) {
+          row = __builtin_amdgcn_readlane(my_row, jl);
+          wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_w), jl));
+        } else {
+          row = __shfl(my_row, jl + sub, kWave);
+          wj = __shfl(my_w, jl + sub, kWave);
+        }
+        const bool ok = jl + sub < n_here;
+        ww[u] = ok ? wj : 0.0f;
+        const Elem* src = values + static_cast<int64_t>(ok ? row : 0) * dv;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+          bb[u][c] = ok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + (cl + L * c) * EPC))
+                        : u32x4{0u, 0u, 0u, 0u};
+      }
+    };
+    auto consume = [&](const u32x4 (&bb)[U][CPL], const float (&ww)[U]) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          float x[EPC];
+          TR::widen(bb[u][c], x);
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) acc[c][e] = fmaf(ww[u], x[e], acc[c][e]);
+        }
+    };
+    issue(0, buf0, wt0);
+    for (int b = 0; b < nb; b += 2) {
+      if (b + 1 < nb) issue(b + 1, buf1, wt1);
+      consume(buf0, wt0);
+      if (b + 1 < nb) {
+        if (b + 2 < nb) issue(b + 2, buf0, wt0);
+        consume(buf1, wt1);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = L; off < kWave; off <<= 1)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[c][e] += __shfl_xor(acc[c][e], off, kWave);
+  if (sub == 0) {
+    float* dst = out + static_cast<size_t>(t) * dv;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4)
+        __builtin_nontemporal_store(f32x4{acc[c][e], acc[c][e + 1], acc[c][e + 2], acc[c][e + 3]},
+                                    reinterpret_cast<f32x4*>(dst + (cl + L * c) * EPC + e));
+  }
+}
+
 template <typename Elem>
 hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int bag,
                         const int32_t* idx, const float* w, const int32_t* perm, int expand,
@@ -210,10 +316,17 @@ hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int
   const int chunks = dv * static_cast<int>(sizeof(Elem)) / 16;
   const size_t lds = static_cast<size_t>(dv <= 2048 ? NWAVES : 2) * dv * 4 +
                     (expand > 1 ? static_cast<size_t>(bag) * 12 : 0);
-  const dim3 grid(T), block(THREADS);
-#define UMEM_GATHER(LL, CC)                                                                  \
-  hipLaunchKernelGGL((gather_kernel<Elem, LL, CC>), grid, block, lds, s, values, n_values, dv, \
-                     bag, idx, w, perm, expand, out)
+  const dim3 block(THREADS);
+  // thousands of tokens without expansion: a wave per token
+  const bool per_wave = expand == 1 && T >= kWaveTokensMin;
+  const dim3 grid(per_wave ? (T + NWAVES - 1) / NWAVES : T);
+#define UMEM_GATHER(LL, CC)                                                                      \
+  if (per_wave)                                                                                  \
+    hipLaunchKernelGGL((gather_wave_kernel<Elem, LL, CC>), grid, block, 0, s, values, dv, T, bag, \
+                       idx, w, out);                                                             \
+  else                                                                                           \
+    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC>), grid, block, lds, s, values, n_values, dv,   \
+                       bag, idx, w, perm, expand, out)
   switch (chunks) {
     case 1: UMEM_GATHER(1, 1); break;
     case 2: UMEM_GATHER(2, 1); break;

@@ -12,6 +12,11 @@
 //    issued up front: one memory round trip), while the query tile is staged once in LDS and
 //    shared by the waves.  Each key is read from HBM once per token tile; at decode (T <= 64)
 //    once in total.
+//  * axis_scores_split (the same shapes, decode-sized T <= 64): a workgroup covers only 16 keys
+//    x 16*MT tokens, and its 4 waves split the key/query dim into quarters.  Each lane loads its
+//    key and query fragments straight into registers, so nothing waits on a barrier before the
+//    MFMAs; the four partial tiles meet once in LDS.  With 4x the workgroups of the kernel above
+//    every CU has several in flight, which hides the memory latency that bounds small T.
 //  * axis_scores_valu (any shape): a TT x TN tile on the vector ALUs, key and query tiles
 //    streamed through LDS in chunks of DC dims.
 #include "umem_internal.h"
@@ -223,6 +228,75 @@ __global__ __launch_bounds__(THREADS) void axis_scores_mfma(
   }
 }
 
+template <int MT, int CPW>
+__global__ __launch_bounds__(THREADS) void axis_scores_split(
+    const float* __restrict__ q_row, const float* __restrict__ q_col,
+    const float* __restrict__ k_row, const float* __restrict__ k_col,
+    const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
+    int rank) {
+  constexpr int TM = 16 * MT;
+  __shared__ f32x4 part[3][MT][kWave];       // partial D fragments of waves 1..3
+  const int axis = blockIdx.z & 1;
+  const int h = blockIdx.z >> 1;
+  const float* __restrict__ q = axis ? q_col : q_row;
+  const float* __restrict__ K = axis ? k_col : k_row;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int j = lane & 15;        // key within the 16 (B and D column); token within 16 for A
+  const int g = lane >> 4;        // 4-dim group within a 16-dim chunk
+  const int key = blockIdx.x * 16 + j;
+  const int t0 = blockIdx.y * TM;
+  const int d0 = wave * 16 * CPW + 4 * g;    // this lane's first dim
+
+  // fragments: key rows of the 16 keys and query rows of the TM tokens, this wave's dims only
+  f32x4 kf[CPW], qf[MT][CPW];
+  const float* krow = K + (static_cast<size_t>(h) * n + (key < n ? key : n - 1)) * dk + d0;
+#pragma unroll
+  for (int c = 0; c < CPW; ++c) kf[c] = *reinterpret_cast<const f32x4*>(krow + 16 * c);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int t = t0 + 16 * mt + j;
+    const float* qrow = q + (static_cast<size_t>(t < T ? t : T - 1) * H + h) * dk + d0;
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) qf[mt][c] = *reinterpret_cast<const f32x4*>(qrow + 16 * c);
+  }
+  f32x4 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) {
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[mt][c].x, kf[c].x, acc[mt], 0, 0, 0);
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[mt][c].y, kf[c].y, acc[mt], 0, 0, 0);
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[mt][c].z, kf[c].z, acc[mt], 0, 0, 0);
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[mt][c].w, kf[c].w, acc[mt], 0, 0, 0);
+    }
+  }
+  // a wave's quarter of the dims lies in one slice (the launcher checks 4 % rank == 0): fold it
+  if (factors != nullptr) {
+    const float f = factors[(h * 2 + axis) * kMaxRank + (wave * 16 * CPW) / (dk / rank)];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] *= f;
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) part[wave - 1][mt][lane] = acc[mt];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // lane holds D[4 g + r][j]: token t0 + 16 mt + 4 g + r, key blockIdx.x * 16 + j
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const f32x4 o = ((acc[mt] + part[0][mt][lane]) + part[1][mt][lane]) + part[2][mt][lane];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = t0 + mt * 16 + 4 * g + r;
+        if (t < T && key < n) sel[((static_cast<size_t>(axis) * T + t) * H + h) * n + key] = o[r];
+      }
+    }
+  }
+}
+
 }  // namespace
 
 __global__ void rank1_kernel(const float* __restrict__ core, int H, int r, float* __restrict__ factors) {
@@ -246,6 +320,25 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
   if (T == 0) return hipSuccess;
   const float* c = (d.grid == UMEM_GRID_TUCKER) ? factors : nullptr;
   const int width = d.dk / d.rank;
+  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && width % 16 == 0 && T <= 64 &&
+      4 % d.rank == 0) {
+    const int mt = T <= 16 ? 1 : 2;
+    dim3 grid((d.n_keys + 15) / 16, (T + 16 * mt - 1) / (16 * mt), d.heads * 2);
+#define UMEM_SPLIT(MT, CPW)                                                                      \
+  hipLaunchKernelGGL((axis_scores_split<MT, CPW>), grid, dim3(THREADS), 0, s, q_row, q_col,      \
+                     k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank)
+    if (mt == 1) {
+      if (d.dk == 64) UMEM_SPLIT(1, 1);
+      else if (d.dk == 128) UMEM_SPLIT(1, 2);
+      else UMEM_SPLIT(1, 4);
+    } else {
+      if (d.dk == 64) UMEM_SPLIT(2, 1);
+      else if (d.dk == 128) UMEM_SPLIT(2, 2);
+      else UMEM_SPLIT(2, 4);
+    }
+#undef UMEM_SPLIT
+    return hipGetLastError();
+  }
   if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && width % 16 == 0) {
     int mt = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
     while (mt > 1 && static_cast<size_t>(16 * mt) * (d.dk + 4) * 4 > 65536) mt /= 2;

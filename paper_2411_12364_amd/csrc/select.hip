@@ -4,20 +4,27 @@
 // 4-7 on the column axis, at the same time.  Every selection is exact under the order
 // (score desc, index asc), in three steps:
 //
-//  1. Threshold.  Each thread holds its elements in registers and takes their maximum.  The
-//     k-th largest of maxima of the group's threads (merged into one or two per lane), L, comes
-//     from a 32-step ballot search in one wave.  They are maxima of disjoint sets, so at least k elements are >= L: the k-th largest
-//     element is >= L, and every element of the top-k is >= L.
-//  2. Survivors {x >= L} (typically a few dozen) are compacted into LDS (wave scans in DPP).
-//  3. A survivor's rank is the number of survivors ordered before it; ranks < k are the answer,
-//     already sorted.
-//  If the survivors overflow their buffer (massive ties), an exact threshold search over all
-//  elements (32 steps of group-wide counts) takes over.
+//  1. Threshold.  Each thread holds its elements in registers and takes their maximum; the
+//     maxima of four threads are merged per lane, and L is the largest value whose low 16 key
+//     bits are zero such that at least k of those 64 merged maxima are >= L (8 radix-4 steps of
+//     ballots, which each wave of the axis runs for itself).  They are maxima of disjoint sets, so at least k elements are >= L:
+//     the whole top-k is >= L.
+//  2. Survivors {x >= L} (typically a few dozen) are compacted into LDS: a DPP wave scan places
+//     them within the wave's range, which one LDS atomic reserves (the ranks below do not depend
+//     on the order of the ranges, so the result is deterministic).
+//  3. A survivor's rank is the number of survivors ordered before it, counted by P threads per
+//     survivor (as many as the group has to spare) and summed over those lanes; ranks < k are
+//     the answer, already sorted.
+//  If an axis's survivors overflow their buffer (massive ties), an exact threshold search over
+//  all elements of the axis (32 steps of group-wide counts) takes over.
 //
 // Additive grid (eq. (3)): with both axis lists sorted, candidate (a, b) (a-th best row, b-th
 // best column) is preceded in the order by the (a+1)(b+1)-1 candidates (a' <= a, b' <= b), so
 // only (a+1)(b+1) <= m can reach the top-m.  Candidate scores are summed in fp64, where the sum
-// of two fp32 scores is exact (or monotone), so this dominance holds.
+// of two fp32 scores is exact (or monotone), so this dominance holds.  Further, for r <= k rows
+// and c = ceil(m / r) <= k columns the r x c corner of the grid holds at least m pairs, all
+// scoring >= A[r-1] + B[c-1]: theta, the largest such bound over r, is <= the m-th best score,
+// and only candidates >= theta are ranked (typically a third of them).
 // Tucker grid (eq. (10)): all k*k candidates, the exact per-slice scores recomputed for the
 // selected keys, candidate scores in fp64; the threshold of step 1 runs on their fp32 roundings
 // (rounding is monotone, so the survivors still contain the top-m) and the ranks on fp64.
@@ -37,10 +44,11 @@ constexpr int CPT = KK_MAX / THREADS;   // Tucker candidates per thread
 struct SelectShared {
   uint32_t mx[THREADS];               // thread maxima (both axes, or the grid)
   int wave_tot[NWAVES];
+  int ax_cnt[2];                      // survivors of each axis (LDS-atomic ranges per wave)
   uint32_t thr[2];
-  int cnt2[2];
   int32_t ax_idx[2][kMaxTopK];        // axis top-k, sorted by (score desc, index asc)
   float ax_sc[2][kMaxTopK];
+  int grid_cnt;                       // additive grid: candidates kept for ranking
   float s_ex[2][kMaxRank][kMaxTopK];  // Tucker: exact per-slice scores of the selected keys
   double p_col[kMaxRank][kMaxTopK];   // Tucker: (C S_col)[rho, b] in fp64
   float core[kMaxRank * kMaxRank];
@@ -83,6 +91,28 @@ __device__ __forceinline__ int wave_scan_dpp(int x) {
   return x;
 }
 
+// Maximum of a 64-bit value over the 64 lanes of a wave (DPP row shifts and row broadcasts on
+// both halves; lanes outside a step's source read 0, the identity), returned to every lane.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+#define UMEM_MAX_STEP(CTRL, ROWS, BC)                                                        \
+  {                                                                                          \
+    const uint32_t lo = __builtin_amdgcn_update_dpp(0, static_cast<uint32_t>(x), CTRL, ROWS, 0xF, BC);  \
+    const uint32_t hi = __builtin_amdgcn_update_dpp(0, static_cast<uint32_t>(x >> 32), CTRL, ROWS, 0xF, BC); \
+    const uint64_t y = (static_cast<uint64_t>(hi) << 32) | lo;                               \
+    x = y > x ? y : x;                                                                       \
+  }
+  UMEM_MAX_STEP(0x111, 0xF, true)    // row_shr:1
+  UMEM_MAX_STEP(0x112, 0xF, true)    // row_shr:2
+  UMEM_MAX_STEP(0x114, 0xF, true)    // row_shr:4
+  UMEM_MAX_STEP(0x118, 0xF, true)    // row_shr:8
+  UMEM_MAX_STEP(0x142, 0xA, false)   // row_bcast:15
+  UMEM_MAX_STEP(0x143, 0xC, false)   // row_bcast:31
+#undef UMEM_MAX_STEP
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), kWave - 1);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(x >> 32), kWave - 1);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
 // Exclusive offset of each thread's count within waves [w0, w0 + nw), and their total.
 // Called by every thread of the workgroup (it holds two barriers).
 __device__ __forceinline__ int2 group_offsets(int cnt, int w0, int nw, SelectShared& sh) {
@@ -101,23 +131,29 @@ __device__ __forceinline__ int2 group_offsets(int cnt, int w0, int nw, SelectSha
   return make_int2(base + incl - cnt, total);
 }
 
-// Largest L with at least k of the wave's 64 G values v[] >= L: a 32-step ballot search.
+// Largest L with zero low 16 bits such that at least k of the wave's 64 G values v[] are
+// >= L (k <= 64 G): eight radix-4 steps, each of three independent ballots.
 template <int G>
-__device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&v)[G], int k) {
-  uint32_t prefix = 0u;
-  for (int b = 31; b >= 0; --b) {
-    const uint32_t c = prefix | (1u << b);
-    int cnt = 0;
+__device__ __forceinline__ uint32_t wave_kth_largest16(const uint32_t (&v)[G], int k) {
+  uint32_t p = 0u;
+  for (int b = 30; b >= 16; b -= 2) {
+    const uint32_t c1 = p | (1u << b), c2 = p | (2u << b), c3 = p | (3u << b);
+    int n1 = 0, n2 = 0, n3 = 0;
 #pragma unroll
-    for (int g = 0; g < G; ++g) cnt += __popcll(__ballot(v[g] >= c));
-    if (cnt >= k) prefix = c;
+    for (int g = 0; g < G; ++g) {
+      n1 += __popcll(__ballot(v[g] >= c1));
+      n2 += __popcll(__ballot(v[g] >= c2));
+      n3 += __popcll(__ballot(v[g] >= c3));
+    }
+    p = n3 >= k ? c3 : (n2 >= k ? c2 : (n1 >= k ? c1 : p));
   }
-  return prefix;
+  return p;
 }
 
 // A valid threshold for a top-k from V maxima per lane (maxima of disjoint sets) in LDS:
 // lane-wise they are merged into G = ceil(k / 64) maxima of unions (still disjoint sets), and
-// L is the k-th largest of those 64 G values, so at least k elements are >= L.  One wave.
+// L, the k-th largest of those 64 G values with its low 16 bits cleared, has at least k
+// elements >= L.  One wave.
 template <int V>
 __device__ __forceinline__ uint32_t threshold_from_maxima(const uint32_t* vals, int k) {
   const int lane = threadIdx.x & (kWave - 1);
@@ -128,18 +164,18 @@ __device__ __forceinline__ uint32_t threshold_from_maxima(const uint32_t* vals, 
     uint32_t r[1] = {0u};
 #pragma unroll
     for (int q = 0; q < V; ++q) r[0] = max(r[0], v[q]);
-    return wave_kth_largest<1>(r, k);
+    return wave_kth_largest16<1>(r, k);
   }
   if (V >= 4 && k <= 2 * kWave) {
     uint32_t r[2] = {0u, 0u};
 #pragma unroll
     for (int q = 0; q < V; ++q) r[q & 1] = max(r[q & 1], v[q]);
-    return wave_kth_largest<2>(r, k);
+    return wave_kth_largest16<2>(r, k);
   }
   uint32_t r[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
   for (int q = 0; q < V; ++q) r[q & 3] = max(r[q & 3], v[q]);
-  return wave_kth_largest<4>(r, k);
+  return wave_kth_largest16<4>(r, k);
 }
 
 // ---------------------------------------------------------------- per-axis top-k
@@ -151,6 +187,38 @@ __device__ __forceinline__ int elem_index(int g, int j, int e) {
   return VEC == 4 ? 1024 * j + 4 * g + e : GROUP * j + g;
 }
 
+// Rank the S survivors of one axis in comp[0, S) with the axis's 256 threads: P = 2^lp threads
+// per survivor (consecutive lanes), each counting the survivors before it among every P-th
+// entry; ranks < k go to the axis list.
+__device__ __forceinline__ void rank_axis(const uint64_t* comp, int S, int axis, int k, int g,
+                                          SelectShared& sh) {
+  int lp = 0;
+  while (lp < 6 && (S << (lp + 1)) <= GROUP) ++lp;
+  const int P = 1 << lp;
+  for (int base = 0; base < (S << lp); base += GROUP) {
+    const int slot = base + g;
+    const int e = slot >> lp, part = slot & (P - 1);
+    uint64_t me = 0ull;
+    int r = 0;
+    if (e < S) {
+      me = comp[e];
+      int u = part;
+      for (; u + 3 * P < S; u += 4 * P) {
+        const uint64_t b0 = comp[u], b1 = comp[u + P], b2 = comp[u + 2 * P], b3 = comp[u + 3 * P];
+        r += static_cast<int>(b0 > me) + static_cast<int>(b1 > me) + static_cast<int>(b2 > me) +
+             static_cast<int>(b3 > me);
+      }
+      for (; u < S; u += P) r += comp[u] > me;
+    }
+    for (int o = 1; o < P; o <<= 1) r += __shfl_xor(r, o, kWave);
+    if (part == 0 && e < S && r < k) {
+      sh.ax_idx[axis][r] = static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(me & 0xFFFFFFFFull));
+      sh.ax_sc[axis][r] = key32_value(static_cast<uint32_t>(me >> 32));
+    }
+  }
+}
+
+// Both axes' top-k into sh.ax_idx / sh.ax_sc.
 template <int NV, int VEC>
 __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, int h, int n, int k,
                             uint64_t* comp_all, SelectShared& sh) {
@@ -185,34 +253,34 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
     }
   sh.mx[tid] = mx;
   __syncthreads();
-  if (g < kWave) {                                        // first wave of each group
-    const uint32_t L = threshold_from_maxima<4>(sh.mx + axis * GROUP, k);
-    if (lane == 0) sh.thr[axis] = L;
-  }
-  __syncthreads();
-  const uint32_t L = sh.thr[axis];
-  int cnt = 0;
+  const uint32_t L = threshold_from_maxima<4>(sh.mx + axis * GROUP, k);   // in every wave
+  uint32_t hit = 0u;                                      // bit j*VEC+e: element survives
 #pragma unroll
   for (int j = 0; j < NV; ++j)
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) cnt += (elem_index<VEC>(g, j, e) < n) & (key[j * VEC + e] >= L);
-  const int2 ot = group_offsets(cnt, axis * 4, 4, sh);      // both groups at once
-  const bool overflow = ot.y > SMAX_AX;
-  if (g == 0) sh.cnt2[axis] = ot.y;
-  if (!overflow) {
-    int pos = ot.x;
+    for (int e = 0; e < VEC; ++e)
+      hit |= static_cast<uint32_t>((elem_index<VEC>(g, j, e) < n) & (key[j * VEC + e] >= L)) << (j * VEC + e);
+  const int cnt = __popc(hit);
+  const int incl = wave_scan_dpp(cnt);
+  const int tot = __shfl(incl, kWave - 1, kWave);
+  int wbase = 0;
+  if (lane == 0) wbase = atomicAdd(&sh.ax_cnt[axis], tot);
+  wbase = __shfl(wbase, 0, kWave);
+  if (wbase + tot <= SMAX_AX) {
+    int pos = wbase + incl - cnt;
 #pragma unroll
     for (int j = 0; j < NV; ++j)
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const int i = elem_index<VEC>(g, j, e);
-        if ((i < n) & (key[j * VEC + e] >= L)) comp[pos++] = axis_comp(key[j * VEC + e], i);
-      }
+      for (int e = 0; e < VEC; ++e)
+        if ((hit >> (j * VEC + e)) & 1u) comp[pos++] = axis_comp(key[j * VEC + e], elem_index<VEC>(g, j, e));
   }
-  if (__syncthreads_or(overflow)) {
+  __syncthreads();
+  int S = sh.ax_cnt[axis];
+  if (max(sh.ax_cnt[0], sh.ax_cnt[1]) > SMAX_AX) {
     // Massive ties on one axis: the exact k-th largest key theta over all its elements, then
     // the elements above it and the lowest-indexed elements equal to it.  Both groups run the
     // loop (its barriers are shared); only an overflowing axis writes.
+    const bool overflow = S > SMAX_AX;
     uint32_t prefix = 0u;
     for (int b = 31; b >= 0; --b) {
       const uint32_t c = prefix | (1u << b);
@@ -255,27 +323,10 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
       pos += otk.y;
       eq_seen += oe.y;
     }
-    if (overflow && g == 0) sh.cnt2[axis] = k;
+    if (overflow) S = k;
+    __syncthreads();
   }
-  __syncthreads();
-  const int S = sh.cnt2[axis];
-  for (int s = g; s < S; s += GROUP) {
-    const uint64_t c = comp[s];
-    int r = 0;
-    int u = 0;
-    for (; u + 8 <= S; u += 8) {
-      uint64_t b[8];
-#pragma unroll
-      for (int v = 0; v < 8; ++v) b[v] = comp[u + v];
-#pragma unroll
-      for (int v = 0; v < 8; ++v) r += b[v] > c;
-    }
-    for (; u < S; ++u) r += comp[u] > c;
-    if (r < k) {
-      sh.ax_idx[axis][r] = static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(c & 0xFFFFFFFFull));
-      sh.ax_sc[axis][r] = key32_value(static_cast<uint32_t>(c >> 32));
-    }
-  }
+  rank_axis(comp, S, axis, k, g, sh);
   __syncthreads();
 }
 
@@ -292,22 +343,30 @@ __device__ __forceinline__ int before(const Cand& a, uint64_t ks, int is) {
   return static_cast<int>(a.key > ks) + static_cast<int>((a.key == ks) & (a.id < is));
 }
 
-// Rank the S candidates (key desc, id asc) with the whole workgroup; ranks < m by rank.
+// Rank the S candidates (key desc, id asc) with the whole workgroup: P = 2^lp threads per
+// candidate (consecutive lanes), each counting the candidates before it among every P-th one;
+// ranks < m go to sh.out_flat / sh.out_g.
 __device__ __forceinline__ void rank_candidates(const Cand* cand, int S, int m, SelectShared& sh) {
-  for (int s = threadIdx.x; s < S; s += THREADS) {
-    const uint64_t ks = cand[s].key;
-    const int is = cand[s].id;
-    int r = 0;
-    int u = 0;
-    for (; u + 8 <= S; u += 8) {
-      Cand b[8];
-#pragma unroll
-      for (int v = 0; v < 8; ++v) b[v] = cand[u + v];
-#pragma unroll
-      for (int v = 0; v < 8; ++v) r += before(b[v], ks, is);
+  int lp = 0;
+  while (lp < 6 && (S << (lp + 1)) <= THREADS) ++lp;
+  const int P = 1 << lp;
+  for (int base = 0; base < (S << lp); base += THREADS) {
+    const int slot = base + static_cast<int>(threadIdx.x);
+    const int e = slot >> lp, part = slot & (P - 1);
+    uint64_t ks = 0ull;
+    int is = 0, r = 0;
+    if (e < S) {
+      ks = cand[e].key;
+      is = cand[e].id;
+      int u = part;
+      for (; u + 3 * P < S; u += 4 * P) {
+        const Cand b0 = cand[u], b1 = cand[u + P], b2 = cand[u + 2 * P], b3 = cand[u + 3 * P];
+        r += before(b0, ks, is) + before(b1, ks, is) + before(b2, ks, is) + before(b3, ks, is);
+      }
+      for (; u < S; u += P) r += before(cand[u], ks, is);
     }
-    for (; u < S; ++u) r += before(cand[u], ks, is);
-    if (r < m) {
+    for (int o = 1; o < P; o <<= 1) r += __shfl_xor(r, o, kWave);
+    if (part == 0 && e < S && r < m) {
       sh.out_flat[r] = is;
       sh.out_g[r] = key64_value(ks);
     }
@@ -334,6 +393,8 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
 
   // ---- a3: the two axes, four waves each
   if (tucker && tid < rank * rank) sh.core[tid] = core_all[static_cast<size_t>(h) * rank * rank + tid];
+  if (tid < 2) sh.ax_cnt[tid] = 0;
+  if (tid == 0) sh.grid_cnt = 0;
   select_axes<NV, VEC>(sel, T, H, t, h, n, k, reinterpret_cast<uint64_t*>(dyn), sh);
   if (axis_out != nullptr)
     for (int a = tid; a < 2 * k; a += THREADS)
@@ -342,43 +403,41 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
   Cand* cand = reinterpret_cast<Cand*>(dyn);                 // candidates, after the axes
   int S;
   if (!tucker) {
-    // ---- a4 (additive): (a, b) with a, b < k and (a+1)(b+1) <= m, scores exact in fp64
-    const int kk = min(k, m);
-    int cnt = 0;
-    for (int c = tid; c < kk * k; c += THREADS) cnt += ((c / k) + 1) * ((c % k) + 1) <= m;
-    const int2 o = group_offsets(cnt, 0, NWAVES, sh);
-    int pos = o.x;
-    for (int c = tid; c < kk * k; c += THREADS) {
-      const int a = c / k, b = c - (c / k) * k;
-      if ((a + 1) * (b + 1) <= m) {
-        cand[pos].key = order_key64(static_cast<double>(sh.ax_sc[0][a]) + static_cast<double>(sh.ax_sc[1][b]));
+    // ---- a4 (additive): (a, b) with a, b < k and (a+1)(b+1) <= m, scores exact in fp64; every
+    // wave first takes theta, the corner bound, itself
+    const int R = min(k, m);
+    uint64_t th = 0ull;
+    for (int r0 = 1; r0 <= R; r0 += kWave) {
+      const int r = r0 + lane;
+      const int c = r <= R ? (m + r - 1) / r : k + 1;
+      if (c <= k)
+        th = max(th, order_key64(static_cast<double>(sh.ax_sc[0][r - 1]) + static_cast<double>(sh.ax_sc[1][c - 1])));
+    }
+    th = wave_max_u64(th);
+    const float inv_k = 1.0f / static_cast<float>(k);
+    for (int c0 = wave * kWave; c0 < R * k; c0 += THREADS) {
+      const int c = c0 + lane;
+      // a = c / k: (c + 1/2) / k is at least 1/(2k) away from an integer, far beyond the fp32 error
+      const int a = static_cast<int>((static_cast<float>(c) + 0.5f) * inv_k);
+      const int b = c - a * k;
+      uint64_t key = 0ull;
+      bool keep = false;
+      if (c < R * k && (a + 1) * (b + 1) <= m) {
+        key = order_key64(static_cast<double>(sh.ax_sc[0][a]) + static_cast<double>(sh.ax_sc[1][b]));
+        keep = key >= th;
+      }
+      const uint64_t bal = __ballot(keep);
+      int wbase = 0;
+      if (lane == 0 && bal) wbase = atomicAdd(&sh.grid_cnt, static_cast<int>(__popcll(bal)));
+      wbase = __shfl(wbase, 0, kWave);
+      if (keep) {
+        const int pos = wbase + static_cast<int>(__popcll(bal & lanemask_lt()));
+        cand[pos].key = key;
         cand[pos].id = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
-        ++pos;
       }
     }
     __syncthreads();
-    S = o.y;
-    // threshold on the fp32 roundings: per-thread maxima over candidates s = tid + 512 q
-    uint32_t mx = 0u;
-    for (int c = tid; c < S; c += THREADS) mx = max(mx, order_key(static_cast<float>(key64_value(cand[c].key))));
-    sh.mx[tid] = mx;
-    __syncthreads();
-    if (wave == 0) {
-      const uint32_t L = threshold_from_maxima<8>(sh.mx, m);
-      if (lane == 0) sh.thr[0] = L;
-    }
-    __syncthreads();
-    const uint32_t L = sh.thr[0];
-    Cand* surv = cand + S;
-    int sc = 0;
-    for (int c = tid; c < S; c += THREADS) sc += order_key(static_cast<float>(key64_value(cand[c].key))) >= L;
-    const int2 os = group_offsets(sc, 0, NWAVES, sh);
-    int sp = os.x;
-    for (int c = tid; c < S; c += THREADS)
-      if (order_key(static_cast<float>(key64_value(cand[c].key))) >= L) surv[sp++] = cand[c];
-    __syncthreads();
-    cand = surv;
-    S = os.y;
+    S = sh.grid_cnt;
   } else {
     // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32
     const int width = dk / rank;

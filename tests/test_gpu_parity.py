@@ -144,14 +144,58 @@ def test_exact_ties_lower_index(kw):
     assert rep["e2e_slot_mismatch"] == 0
 
 
+# ---------------------------------------------------------------- a1 + a2 alone, every kernel
+
+@pytest.mark.parametrize("kw", [
+    dict(T=40, heads=2, dk=128, n_keys=200),                                  # split, 2 tiles
+    dict(T=40, heads=2, dk=128, n_keys=200, rank=2, grid=CF.GRID_TUCKER),     # split + fold
+    dict(T=9, heads=1, dk=64, n_keys=70, rank=4, grid=CF.GRID_TUCKER),        # split, 1 chunk
+    dict(T=64, heads=1, dk=256, n_keys=33),                                   # split, 4 chunks
+    dict(T=100, heads=1, dk=256, n_keys=130, rank=2, grid=CF.GRID_TUCKER),    # tiled MFMA
+    dict(T=70, heads=3, dk=64, n_keys=200),                                   # tiled MFMA
+    dict(T=5, heads=2, dk=12, n_keys=33, rank=3, grid=CF.GRID_TUCKER),        # vector ALU
+], ids=["split", "split-tucker2", "split-tucker4", "split-dk256", "tiled-tucker2", "tiled",
+        "valu-tucker3"])
+def test_axis_scores_kernels(kw):
+    cfg = small("scores", topk=4, topm=4, **kw)
+    log(f"[case] axis scores {kw}")
+    dl = SD.make_layer(cfg)
+    desc = G.desc_for(cfg)
+    T, H, n = cfg.T, cfg.heads, cfg.n_keys
+    sel = torch.empty((2, T, H, n), dtype=torch.float32, device="cuda")
+    ws = G.workspace(desc, T)
+    U.check(U.umem_axis_scores(desc, T, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core, sel,
+                               ws, ws.numel()), "umem_axis_scores")
+    torch.cuda.synchronize()
+    got = G.host(sel).astype(np.float64)
+    qr, qc = CF.queries(cfg)
+    kr, kc = CF.keys(cfg)
+    core = CF.core(cfg)
+    vr = vc = None
+    if core is not None:
+        f = [O.rank1_factors(core[h].astype(np.float64)) for h in range(H)]
+        vr, vc = [x[0] for x in f], [x[1] for x in f]
+    for a, (q, K, v) in enumerate(((qr, kr, vr), (qc, kc, vc))):
+        want = O.selection_scores(O.axis_scores(q, K, cfg.rank), v)
+        # fp32 products and sums against fp64: bound by the size of the terms
+        scale = np.einsum("thd,hnd->thn", np.abs(q.astype(np.float64)), np.abs(K.astype(np.float64)))
+        err = np.abs(got[a] - want) / (scale + 1e-30)
+        log(f"[report] axis {a}: max err / sum|q k| = {err.max():.2e}")
+        assert err.max() <= 1e-5, (a, err.max())
+
+
 # ---------------------------------------------------------------- gather and projection alone
 
-@pytest.mark.parametrize("dv,vdtype,expand,bag", [
-    (512, CF.BF16, 1, 64), (1024, CF.BF16, 1, 77), (256, CF.F32, 1, 5), (512, CF.BF16, 4, 256),
-    (128, CF.BF16, 9, 40), (3072, CF.BF16, 1, 33), (8, CF.BF16, 4, 130)])
-def test_gather_standalone(dv, vdtype, expand, bag):
-    rng = np.random.default_rng(dv + bag)
-    Np, T = 5000, 37
+@pytest.mark.parametrize("dv,vdtype,expand,bag,T", [
+    (512, CF.BF16, 1, 64, 37), (1024, CF.BF16, 1, 77, 37), (256, CF.F32, 1, 5, 37),
+    (512, CF.BF16, 4, 256, 37), (128, CF.BF16, 9, 40, 37), (3072, CF.BF16, 1, 33, 37),
+    (8, CF.BF16, 4, 130, 37),
+    # thousands of tokens: a wave per token (ragged last workgroup, sub-rows, long rows)
+    (512, CF.BF16, 1, 64, 4099), (64, CF.BF16, 1, 33, 4100), (2048, CF.BF16, 1, 20, 4096),
+    (256, CF.F32, 1, 7, 5001)])
+def test_gather_standalone(dv, vdtype, expand, bag, T):
+    rng = np.random.default_rng(dv + bag + T)
+    Np = 5000
     vdt = torch.float32 if vdtype == CF.F32 else torch.bfloat16
     values = torch.empty((Np, dv), dtype=vdt, device="cuda")
     SD.fill_normal_(values, 21, S.TID_VALUES, 1 / np.sqrt(dv))
@@ -167,7 +211,7 @@ def test_gather_standalone(dv, vdtype, expand, bag):
     vals = values.float().cpu().numpy().astype(np.float64)
     ref = O.gather_sum(lambda r: vals[r], idx, w, perm, Np, expand)
     err = np.abs(out.cpu().numpy() - ref).max() / np.abs(ref).max()
-    log(f"[report] gather dv={dv} E={expand} bag={bag}: err={err:.2e}")
+    log(f"[report] gather T={T} dv={dv} E={expand} bag={bag}: err={err:.2e}")
     assert err <= 1e-5
 
 
