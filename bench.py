@@ -58,8 +58,9 @@ def log(msg):
 
 # ---------------------------------------------------------------- byte and flop accounting
 
-def kernel_work(cfg, T):
-    """Algorithmic bytes (and flops) per launch of each kernel at T tokens."""
+def kernel_work(cfg, T, fused=False):
+    """Algorithmic bytes (and flops) per launch of each kernel at T tokens; with ``fused`` the
+    selection kernel also reads the value rows and writes the pooled rows."""
     H, n, dk, k, m = cfg.heads, cfg.n_keys, cfg.dk, cfg.topk, cfg.topm
     keys = 2 * H * n * dk * 4
     q = 2 * T * H * dk * 4
@@ -68,7 +69,7 @@ def kernel_work(cfg, T):
     rows = T * cfg.bag * cfg.dv * cfg.vbytes
     return {
         "axis_scores_kernel": dict(bytes=keys + q + sel, flops=2 * 2 * T * H * n * dk),
-        "select_kernel": dict(bytes=sel + sel_out, flops=0),
+        "select_kernel": dict(bytes=sel + sel_out + (rows + T * cfg.dv * 4 if fused else 0), flops=0),
         "gather_kernel": dict(bytes=rows + T * cfg.bag * 8 + T * cfg.expand * cfg.dv * 4,
                               flops=2 * T * cfg.bag * cfg.dv, row_bytes=rows),
     }
@@ -116,6 +117,9 @@ class Runner:
         self.w = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.float32, device="cuda")
         self.sel = torch.empty((2, T, cfg.heads, cfg.n_keys), dtype=torch.float32, device="cuda")
         self.R = batches
+        # umem_forward pools inside the selection kernel for such layers (see umem_select)
+        self.fused = (cfg.expand == 1 and cfg.heads <= 2 and cfg.topm <= 64 and not cfg.dv_virt
+                      and cfg.dv * cfg.vbytes in (1024, 2048) and cfg.T <= 512)
 
     def _desc(self):
         c, d = self.cfg, self.U.umem_desc()
@@ -141,9 +145,12 @@ class Runner:
             U.check(st, "umem_axis_scores")
 
     def select(self, sel, idx, w):
+        """The selection as umem_forward launches it: pooling the rows itself where it can."""
         U, dl, c = self.U, self.dl, self.cfg
+        pool = self.fused
         st = U.umem_select(self.desc, c.T, sel, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col,
-                           dl.core, idx, w, None)
+                           dl.core, idx, w, None, dl.values if pool else None,
+                           self.out if pool else None)
         if st:
             U.check(st, "umem_select")
 
@@ -256,8 +263,8 @@ class Runner:
                     algorithmic_frac_of_peak=round(algo / secs / 1e9 / HBM_PEAK_GBS, 4))
 
 
-def roofline_for(cfg, T, name, avg_us, workload):
-    work = kernel_work(cfg, T)[name]
+def roofline_for(cfg, T, name, avg_us, workload, fused):
+    work = kernel_work(cfg, T, fused)[name]
     if name == "axis_scores_kernel" and work["flops"] / work["bytes"] > FP32_PEAK_TFLOPS * 1e3 / HBM_PEAK_GBS:
         achieved = work["flops"] / (avg_us * 1e-6) / 1e12
         return dict(kernel=name, bound="mfma", achieved=round(achieved, 3), peak=FP32_PEAK_TFLOPS,
@@ -356,7 +363,11 @@ def main():
     log(f"eager forward (one launch sequence per step from Python): {eager_us:.2f} us/step")
     stage_us = r.time_kernels(512)
     log(f"per-kernel (graph replay, events): {stage_us}")
-    dominant = max(stage_us, key=stage_us.get)
+    # the kernels umem_forward launches: the standalone gather only where the selection does not
+    # pool the rows itself
+    fwd_kernels = ["axis_scores_kernel", "select_kernel"] + ([] if r.fused else ["gather_kernel"])
+    dominant = max(fwd_kernels, key=stage_us.get)
+    fused = r.fused
     work = kernel_work(cfg, cfg.T)
     g_us = stage_us["gather_kernel"]
     gather = dict(row_bytes_per_launch=work["gather_kernel"]["row_bytes"], avg_us=round(g_us, 3),
@@ -378,8 +389,9 @@ def main():
                    "n_keys": cfg.n_keys, "slots": cfg.n_slots, "dv": cfg.dv, "values": "bf16",
                    "topk": cfg.topk, "topm": cfg.topm, "query_batches": args.batches,
                    "launch": "eager" if args.eager else "hip-graph"},
-        "roofline": roofline_for(cfg, cfg.T, dominant, stage_us[dominant], cfg.name),
+        "roofline": roofline_for(cfg, cfg.T, dominant, stage_us[dominant], cfg.name, fused),
         "kernel_us": {k: round(v, 3) for k, v in stage_us.items()},
+        "forward_kernels": fwd_kernels,
         "eager_us_per_step": round(eager_us, 3),
         "gather": gather,
         "gather_queue": queue,

@@ -103,16 +103,23 @@ UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const fl
 
 /* a3 + a4 + a5 from selection scores: per-axis top-k, grid scores of the k*k candidates
  * (additive eq. (3); Tucker eq. (10) with the per-slice scores recomputed exactly for the
- * candidates, non-candidates excluded), global top-m and weights.
+ * candidates, non-candidates excluded), global top-m and weights; optionally a7 as well.
  *   sel       fp32 [2, T, H, n] as written by umem_axis_scores, 16-byte aligned
  *   q_*, k_*, core  as above; read only for UMEM_GRID_TUCKER (may be NULL for ADD)
  *   idx       int32 [T, H, m] out: logical slot i*n + j, sorted by (score desc, index asc)
  *   w         fp32 [T, H, m] out: the weight of each slot (raw grid score, or SoftMax)
- *   axis_idx  int32 [2, T, H, k] out, optional (NULL): per-axis top-k, sorted */
+ *   axis_idx  int32 [2, T, H, k] out, optional (NULL): per-axis top-k, sorted
+ *   values, pooled  optional (both NULL or both set): the value table [n_values, dv] and fp32
+ *             [T, dv] (16-byte aligned); the selected rows are pooled as umem_gather_sum pools
+ *             them (eq. (1)) and ADDED to pooled, which the caller clears beforehand.  Only for
+ *             layers without expansion, with heads <= 2, topm <= 64 and value rows of 1 or
+ *             2 KiB (UMEM_ERR_UNSUPPORTED otherwise); with two heads the result does not depend
+ *             on their order (two adds onto zero commute exactly).  umem_forward uses this form
+ *             where it applies and T <= 512, instead of a separate gather launch. */
 UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* sel, const float* q_row,
                         const float* q_col, const float* k_row, const float* k_col,
                         const float* core, int32_t* idx, float* w, int32_t* axis_idx,
-                        hipStream_t stream);
+                        const void* values, float* pooled, hipStream_t stream);
 
 /* a1 .. a5: umem_axis_scores followed by umem_select, the scores kept in `ws`
  * (ws_bytes >= umem_workspace_size(desc, T)). */

@@ -59,7 +59,7 @@ def _load() -> ctypes.CDLL:
     sig = {
         "umem_workspace_size": [D, I32, ctypes.POINTER(SZ)],
         "umem_axis_scores": [D, I32, P, P, P, P, P, P, P, SZ, P],
-        "umem_select": [D, I32, P, P, P, P, P, P, P, P, P, P],
+        "umem_select": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P],
         "umem_score_topk": [D, I32, P, P, P, P, P, P, P, P, P, SZ, P],
         "umem_gather_sum": [I64, I32, I32, P, I32, I32, P, P, P, I32, P, P],
         "umem_project": [I32, I32, I32, I32, I32, P, P, P, P, P, SZ, P],
@@ -125,9 +125,10 @@ def umem_axis_scores(desc, T, q_row, q_col, k_row, k_col, core, sel, ws=None, ws
 
 
 def umem_select(desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx=None,
-                stream=None) -> int:
+                values=None, pooled=None, stream=None) -> int:
     return _lib.umem_select(_d(desc), T, _p(sel), _p(q_row), _p(q_col), _p(k_row), _p(k_col),
-                            _p(core), _p(idx), _p(w), _p(axis_idx), _s(stream))
+                            _p(core), _p(idx), _p(w), _p(axis_idx), _p(values), _p(pooled),
+                            _s(stream))
 
 
 def umem_score_topk(desc, T, q_row, q_col, k_row, k_col, core, idx, w, axis_idx, ws, ws_bytes,

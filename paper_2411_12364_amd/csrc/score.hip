@@ -30,11 +30,22 @@ constexpr int DC = 32;       // dims per LDS chunk
 constexpr int LDS_STRIDE = DC + 4;   // floats per LDS row: float4-aligned, conflict-free b128 reads
 constexpr int THREADS = 256;
 
+// Clears zero[0, n4) (float4s) with every thread of the grid: the forward pools both heads into
+// its output with atomic adds in the kernel that follows this one.
+__device__ __forceinline__ void clear_with_grid(float4* __restrict__ zero, int n4) {
+  if (zero == nullptr) return;
+  const size_t nt = static_cast<size_t>(gridDim.x) * gridDim.y * gridDim.z * blockDim.x;
+  const size_t gid = ((static_cast<size_t>(blockIdx.z) * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) *
+                         blockDim.x + threadIdx.x;
+  for (size_t i = gid; i < static_cast<size_t>(n4); i += nt) zero[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
 __global__ __launch_bounds__(THREADS) void axis_scores_valu(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
     const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
-    int rank) {
+    int rank, float4* __restrict__ zero, int zero_n4) {
+  clear_with_grid(zero, zero_n4);
   const int axis = blockIdx.z & 1;
   const int h = blockIdx.z >> 1;
   const float* __restrict__ q = axis ? q_col : q_row;
@@ -150,7 +161,8 @@ __global__ __launch_bounds__(THREADS) void axis_scores_mfma(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
     const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
-    int rank) {
+    int rank, float4* __restrict__ zero, int zero_n4) {
+  clear_with_grid(zero, zero_n4);
   constexpr int TM = 16 * MT;
   extern __shared__ __align__(16) float qs[];    // [TM][dk + 4]
   __shared__ float fvec[kMaxRank];
@@ -233,7 +245,8 @@ __global__ __launch_bounds__(THREADS) void axis_scores_split(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
     const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
-    int rank) {
+    int rank, float4* __restrict__ zero, int zero_n4) {
+  clear_with_grid(zero, zero_n4);
   constexpr int TM = 16 * MT;
   __shared__ f32x4 part[3][MT][kWave];       // partial D fragments of waves 1..3
   const int axis = blockIdx.z & 1;
@@ -315,7 +328,9 @@ hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, h
 
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
                               const float* k_row, const float* k_col, const float* factors,
-                              float* sel, hipStream_t s) {
+                              float* sel, float* zero_out, size_t zero_floats, hipStream_t s) {
+  float4* zero = reinterpret_cast<float4*>(zero_out);
+  const int zero_n4 = zero_out ? static_cast<int>(zero_floats / 4) : 0;
   clear_stale_error();
   if (T == 0) return hipSuccess;
   const float* c = (d.grid == UMEM_GRID_TUCKER) ? factors : nullptr;
@@ -326,7 +341,7 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
     dim3 grid((d.n_keys + 15) / 16, (T + 16 * mt - 1) / (16 * mt), d.heads * 2);
 #define UMEM_SPLIT(MT, CPW)                                                                      \
   hipLaunchKernelGGL((axis_scores_split<MT, CPW>), grid, dim3(THREADS), 0, s, q_row, q_col,      \
-                     k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank)
+                     k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank, zero, zero_n4)
     if (mt == 1) {
       if (d.dk == 64) UMEM_SPLIT(1, 1);
       else if (d.dk == 128) UMEM_SPLIT(1, 2);
@@ -346,7 +361,7 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
     dim3 grid((d.n_keys + 63) / 64, (T + 16 * mt - 1) / (16 * mt), d.heads * 2);
 #define UMEM_SCORE(MT, NCH)                                                                      \
   hipLaunchKernelGGL((axis_scores_mfma<MT, NCH>), grid, dim3(THREADS), lds, s, q_row, q_col,     \
-                     k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank)
+                     k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank, zero, zero_n4)
 #define UMEM_SCORE_DK(MT)                  \
   if (d.dk == 64) UMEM_SCORE(MT, 4);       \
   else if (d.dk == 128) UMEM_SCORE(MT, 8); \
@@ -360,7 +375,7 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
   }
   dim3 grid((d.n_keys + TN - 1) / TN, (T + TT - 1) / TT, d.heads * 2);
   hipLaunchKernelGGL(axis_scores_valu, grid, dim3(THREADS), 0, s, q_row, q_col, k_row, k_col, c,
-                     sel, T, d.heads, d.n_keys, d.dk, d.rank);
+                     sel, T, d.heads, d.n_keys, d.dk, d.rank, zero, zero_n4);
   return hipGetLastError();
 }
 

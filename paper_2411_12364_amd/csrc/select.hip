@@ -25,6 +25,9 @@
 // and c = ceil(m / r) <= k columns the r x c corner of the grid holds at least m pairs, all
 // scoring >= A[r-1] + B[c-1]: theta, the largest such bound over r, is <= the m-th best score,
 // and only candidates >= theta are ranked (typically a third of them).
+// For the forward without expansion (at most two heads, rows of 1 or 2 KiB) the workgroup also
+// pools its m rows (eq. (1)) and adds them into the token's output: the decode path then needs
+// no separate gather launch.
 // Tucker grid (eq. (10)): all k*k candidates, the exact per-slice scores recomputed for the
 // selected keys, candidate scores in fp64; the threshold of step 1 runs on their fp32 roundings
 // (rounding is monotone, so the survivors still contain the top-m) and the ranks on fp64.
@@ -374,6 +377,77 @@ __device__ __forceinline__ void rank_candidates(const Cand* cand, int S, int m, 
   __syncthreads();
 }
 
+// ---------------------------------------------------------------- a7 fused (decode)
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kPoolRowsPerWave = kMaxPoolTopM / NWAVES;
+
+// This (token, head)'s m rows pooled into out_t[0, dv) with fp32 atomic adds.  Wave v reads rows
+// v, v + 8, ... with 16-byte nontemporal loads (64 lanes x cpl chunks of a 1 or 2 KiB row, all
+// of the wave's rows in flight), the 8 partial rows meet in LDS and are added in wave order, and
+// each element takes one atomic add per head.
+template <bool BF16>
+__device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool softmax,
+                          const SelectShared& sh, float* red, float* __restrict__ out_t) {
+  constexpr int EPC = BF16 ? 8 : 4;                  // elements per 16-byte chunk
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int cpl = dv * (BF16 ? 2 : 4) / 1024;        // 16-byte chunks per lane: 1 or 2
+  const char* base = static_cast<const char*>(values);
+  const size_t row_bytes = static_cast<size_t>(dv) * (BF16 ? 2 : 4);
+  u32x4 raw[kPoolRowsPerWave][2];
+  float wt[kPoolRowsPerWave];
+#pragma unroll
+  for (int i = 0; i < kPoolRowsPerWave; ++i) {
+    const int r = wave + NWAVES * i;
+    wt[i] = 0.0f;
+    raw[i][0] = raw[i][1] = u32x4{0u, 0u, 0u, 0u};
+    if (r < m) {
+      wt[i] = softmax ? sh.e[r] / sh.esum : static_cast<float>(sh.out_g[r]);
+      const u32x4* src = reinterpret_cast<const u32x4*>(base + static_cast<size_t>(sh.out_flat[r]) * row_bytes);
+      raw[i][0] = __builtin_nontemporal_load(src + lane);
+      if (cpl > 1) raw[i][1] = __builtin_nontemporal_load(src + kWave + lane);
+    }
+  }
+  float acc[2][EPC];
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[c][e] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kPoolRowsPerWave; ++i)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const uint32_t q[4] = {raw[i][c].x, raw[i][c].y, raw[i][c].z, raw[i][c].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (BF16) {
+          acc[c][2 * e] = fmaf(wt[i], __uint_as_float(q[e] << 16), acc[c][2 * e]);
+          acc[c][2 * e + 1] = fmaf(wt[i], __uint_as_float(q[e] & 0xFFFF0000u), acc[c][2 * e + 1]);
+        } else {
+          acc[c][e] = fmaf(wt[i], __uint_as_float(q[e]), acc[c][e]);
+        }
+      }
+    }
+  // lane holds elements (64 c + lane) * EPC .. + EPC - 1 of chunk c
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+    if (c < cpl) {
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4)
+        *reinterpret_cast<float4*>(red + wave * dv + (kWave * c + lane) * EPC + e) =
+            make_float4(acc[c][e], acc[c][e + 1], acc[c][e + 2], acc[c][e + 3]);
+    }
+  __syncthreads();
+  for (int col = tid; col < dv; col += THREADS) {
+    float v = red[col];
+#pragma unroll
+    for (int u = 1; u < NWAVES; ++u) v += red[u * dv + col];
+    atomicAdd(out_t + col, v);
+  }
+}
+
 // ---------------------------------------------------------------- the kernel
 
 template <int NV, int VEC>
@@ -382,6 +456,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     const float* __restrict__ q_col, const float* __restrict__ k_row,
     const float* __restrict__ k_col, const float* __restrict__ core_all,
     int32_t* __restrict__ idx_out, float* __restrict__ w_out, int32_t* __restrict__ axis_out,
+    const void* __restrict__ values, int vbf16, int dv, float* __restrict__ pooled,
     int T, int H, int n, int dk, int rank, int k, int m, int tucker, int softmax, int n_cand) {
   extern __shared__ __align__(16) unsigned char dyn[];
   __shared__ SelectShared sh;
@@ -584,6 +659,13 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     idx_out[o] = sh.out_flat[j];
     w_out[o] = softmax ? sh.e[j] / sh.esum : static_cast<float>(sh.out_g[j]);
   }
+  // ---- a7 fused: pool this head's rows into the token's output (the axes' LDS is free now)
+  if (pooled != nullptr) {
+    float* red = reinterpret_cast<float*>(dyn);
+    float* out_t = pooled + static_cast<size_t>(t) * dv;
+    if (vbf16) pool_rows<true>(values, dv, m, softmax, sh, red, out_t);
+    else pool_rows<false>(values, dv, m, softmax, sh, red, out_t);
+  }
 }
 
 }  // namespace
@@ -594,26 +676,35 @@ int additive_candidates(int k, int m) {
   return c;
 }
 
-size_t select_lds_bytes(int n_cand, int tucker) {
+size_t select_lds_bytes(int n_cand, int tucker, int pool_dv) {
   const size_t axes = 2 * static_cast<size_t>(SMAX_AX) * 8;
   const size_t grid = static_cast<size_t>(tucker ? SMAX_S : 2 * n_cand) * sizeof(Cand);
-  return axes > grid ? axes : grid;
+  const size_t pool = static_cast<size_t>(NWAVES) * pool_dv * 4;
+  return axes > grid ? (axes > pool ? axes : pool) : (grid > pool ? grid : pool);
+}
+
+bool select_pools(const umem_desc& d) {
+  const int row_bytes = d.dv * (d.vdtype == UMEM_F32 ? 4 : 2);
+  return d.expand == 1 && d.heads <= 2 && d.topm <= kMaxPoolTopM &&
+         (row_bytes == 1024 || row_bytes == 2048);
 }
 
 hipError_t launch_select(const umem_desc& d, int T, const float* sel, const float* q_row,
                          const float* q_col, const float* k_row, const float* k_col,
                          const float* core, int32_t* idx, float* w, int32_t* axis_idx,
-                         hipStream_t s) {
+                         const void* values, float* pooled, hipStream_t s) {
   clear_stale_error();
+  if (pooled != nullptr && !select_pools(d)) return hipErrorInvalidValue;
   if (T == 0) return hipSuccess;
   const int tucker = d.grid == UMEM_GRID_TUCKER;
   const int n_cand = tucker ? d.topk * d.topk : additive_candidates(d.topk, d.topm);
   if (tucker && n_cand > KK_MAX) return hipErrorInvalidValue;
-  const size_t lds = select_lds_bytes(n_cand, tucker);
+  const size_t lds = select_lds_bytes(n_cand, tucker, pooled ? d.dv : 0);
   const dim3 grid(static_cast<unsigned>(T) * d.heads), block(THREADS);
 #define UMEM_SELECT(NV, VEC)                                                                      \
   hipLaunchKernelGGL((select_kernel<NV, VEC>), grid, block, lds, s, sel, q_row, q_col, k_row,    \
-                     k_col, core, idx, w, axis_idx, T, d.heads, d.n_keys, d.dk, d.rank, d.topk,  \
+                     k_col, core, idx, w, axis_idx, values, d.vdtype == UMEM_BF16, d.dv, pooled,  \
+                     T, d.heads, d.n_keys, d.dk, d.rank, d.topk,                                 \
                      d.topm, tucker, d.weight == UMEM_W_SOFTMAX, n_cand)
   const int n = d.n_keys;
   if (n % 4 == 0) {

@@ -180,14 +180,15 @@ UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const fl
   float* factors = tucker ? static_cast<float*>(ws) : nullptr;
   hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
   if (e == hipSuccess)
-    e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, factors, sel, stream);
+    e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, factors, sel, nullptr, 0, stream);
   return hip_status(e);
 }
 
 UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* sel,
                                  const float* q_row, const float* q_col, const float* k_row,
                                  const float* k_col, const float* core, int32_t* idx, float* w,
-                                 int32_t* axis_idx, hipStream_t stream) {
+                                 int32_t* axis_idx, const void* values, float* pooled,
+                                 hipStream_t stream) {
   umem_status st = check_desc(desc);
   if (st == UMEM_OK) st = check_tokens(T);
   if (st != UMEM_OK || T == 0) return st;
@@ -196,9 +197,14 @@ UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* 
   if (st == UMEM_OK && (!sel || !idx || !w || !aligned(sel, 16) || !aligned(idx, 4) || !aligned(w, 4) ||
                         !aligned(axis_idx, 4)))
     st = UMEM_ERR_INVALID_ARG;
+  if (st == UMEM_OK && (values == nullptr) != (pooled == nullptr)) st = UMEM_ERR_INVALID_ARG;
+  if (st == UMEM_OK && pooled != nullptr) {
+    if (!aligned(values, 16) || !aligned(pooled, 16)) st = UMEM_ERR_INVALID_ARG;
+    else if (!select_pools(*desc)) st = UMEM_ERR_UNSUPPORTED;
+  }
   if (st != UMEM_OK) return st;
-  return hip_status(launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx,
-                                  stream));
+  return hip_status(launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w,
+                                  axis_idx, values, pooled, stream));
 }
 
 UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const float* q_row,
@@ -220,9 +226,10 @@ UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const flo
   hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
   if (e == hipSuccess)
     e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, tucker ? factors : nullptr, sel,
-                           stream);
+                           nullptr, 0, stream);
   if (e == hipSuccess)
-    e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx, stream);
+    e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx, nullptr,
+                      nullptr, stream);
   return hip_status(e);
 }
 
@@ -280,12 +287,17 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
   float* factors = reinterpret_cast<float*>(base + L.factors);
   const bool tucker = desc->grid == UMEM_GRID_TUCKER;
   hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
+  // For decode-sized batches without expansion or projection the selection pools the rows
+  // itself (scoring clears out first); otherwise the gather kernel, with more rows in flight per
+  // CU, pools them after it.
+  const bool fused = !project && select_pools(*desc) && T <= kMaxPoolTokens;
   if (e == hipSuccess)
     e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, tucker ? factors : nullptr, sel,
-                           stream);
+                           fused ? out : nullptr, static_cast<size_t>(T) * desc->dv, stream);
   if (e == hipSuccess)
-    e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, nullptr, stream);
-  if (e == hipSuccess)
+    e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, nullptr,
+                      fused ? values : nullptr, fused ? out : nullptr, stream);
+  if (e == hipSuccess && !fused)
     e = launch_gather(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, perm,
                       desc->expand, pooled, stream);
   if (e == hipSuccess && project)

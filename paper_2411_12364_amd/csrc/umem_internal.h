@@ -13,6 +13,8 @@ constexpr int kMaxSelect = 8192;     // max(n, k*k): one selection's keys in 32 
 constexpr int kMaxTopK = 90;         // k*k <= kMaxSelect
 constexpr int kMaxTopKTucker = 64;   // Tucker: the k*k candidate keys in 16 KiB of LDS
 constexpr int kMaxTopM = 256;
+constexpr int kMaxPoolTopM = 64;      // the selection kernel pools rows itself up to this topm
+constexpr int kMaxPoolTokens = 512;   // ... and umem_forward lets it up to this many tokens
 constexpr int kMaxRank = 4;
 constexpr int kMaxBag = 2048;
 constexpr int kMaxTokens = 1 << 20;
@@ -22,7 +24,7 @@ constexpr int kMaxDk = 1024;
 constexpr size_t kFactorBytes = static_cast<size_t>(kMaxHeads) * 2 * 4 * sizeof(float);
 
 bool gather_row_supported(int dv, int vdtype);
-size_t select_lds_bytes(int n_cand, int tucker);
+size_t select_lds_bytes(int n_cand, int tucker, int pool_dv);
 int additive_candidates(int k, int m);
 constexpr int kMaxRowBytes = 8192;
 
@@ -36,15 +38,23 @@ inline void clear_stale_error() { (void)hipGetLastError(); }
 
 hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, hipStream_t s);
 
-// Selection scores; factors is the output of launch_rank1 (Tucker) or NULL (additive).
+// Selection scores; factors is the output of launch_rank1 (Tucker) or NULL (additive).  With
+// zero_out set the same grid also clears zero_out[0, zero_floats) (a multiple of 4 floats).
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
                               const float* k_row, const float* k_col, const float* factors,
-                              float* sel, hipStream_t s);
+                              float* sel, float* zero_out, size_t zero_floats, hipStream_t s);
 
+// Per-axis top-k, grid, top-m and weights.  With pooled set (only where select_pools(d)), each
+// (token, head) workgroup also pools its m value rows into pooled[t, :] with atomic adds, which
+// must start from zero (launch_axis_scores clears it).
 hipError_t launch_select(const umem_desc& d, int T, const float* sel, const float* q_row,
                          const float* q_col, const float* k_row, const float* k_col,
                          const float* core, int32_t* idx, float* w, int32_t* axis_idx,
-                         hipStream_t s);
+                         const void* values, float* pooled, hipStream_t s);
+
+// Whether the selection kernel can pool the rows itself: no expansion, at most two heads (two
+// atomic adds onto zero give the same bits in either order), topm <= 64 and rows of 1 or 2 KiB.
+bool select_pools(const umem_desc& d);
 
 hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* values, int T,
                          int bag, const int32_t* idx, const float* w, const int32_t* perm,

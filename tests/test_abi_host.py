@@ -98,7 +98,12 @@ def test_entry_points_reject_before_launch():
     tucker = desc(grid=1, rank=2)
     assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, fake, fake, None, 0, 0) == U.UMEM_ERR_WORKSPACE
-    assert U.umem_select(d, 8, None, None, None, None, None, None, fake, fake, None, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_select(d, 8, None, None, None, None, None, None, fake, fake, None, None, None, 0) == U.UMEM_ERR_INVALID_ARG
+    # select with pooling: values and pooled together, aligned, and only where the layer allows
+    assert U.umem_select(d, 8, fake, None, None, None, None, None, fake, fake, None, None, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_select(d, 8, fake, None, None, None, None, None, fake, fake, None, fake, fake + 4, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_select(desc(heads=3), 8, fake, None, None, None, None, None, fake, fake, None, fake, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_select(desc(topm=65, topk=16), 8, fake, None, None, None, None, None, fake, fake, None, fake, fake, 0) == U.UMEM_ERR_UNSUPPORTED
     # gather: bad sizes, misaligned values, bag beyond the limit, unsupported row
     assert U.umem_gather_sum(100, 512, 1, fake, 4, 0, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_gather_sum(100, 512, 1, fake + 8, 4, 64, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
