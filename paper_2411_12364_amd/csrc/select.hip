@@ -42,6 +42,7 @@ constexpr int GROUP = 256;          // threads per axis
 constexpr int SMAX_AX = 512;        // survivors per axis
 constexpr int SMAX_S = 512;         // grid survivors (Tucker)
 constexpr int KK_MAX = 4096;        // Tucker: k*k candidates
+constexpr int ADD_MAX = 2048;       // additive candidates (a+1)(b+1) <= m, a, b < k
 constexpr int CPT = KK_MAX / THREADS;   // Tucker candidates per thread
 
 struct SelectShared {
@@ -52,6 +53,9 @@ struct SelectShared {
   int32_t ax_idx[2][kMaxTopK];        // axis top-k, sorted by (score desc, index asc)
   float ax_sc[2][kMaxTopK];
   int grid_cnt;                       // additive grid: candidates kept for ranking
+  int grid_total;                     // additive grid: (a+1)(b+1) <= m candidates
+  uint16_t grid_ab[ADD_MAX];          // ... their (a << 8) | b, row by row
+  uint8_t th_col[kMaxTopK + 1];       // ceil(m / r) for the corner bound of r rows (0: beyond k)
   float s_ex[2][kMaxRank][kMaxTopK];  // Tucker: exact per-slice scores of the selected keys
   double p_col[kMaxRank][kMaxTopK];   // Tucker: (C S_col)[rho, b] in fp64
   float core[kMaxRank * kMaxRank];
@@ -114,6 +118,18 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
   const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), kWave - 1);
   const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(x >> 32), kWave - 1);
   return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Sum over aligned groups of 2^lp consecutive lanes (every lane of a group gets the sum): the
+// quad swaps, the half-row and row mirrors of DPP, then shuffles across rows.
+__device__ __forceinline__ int group_sum(int r, int lp) {
+  if (lp >= 1) r += __builtin_amdgcn_update_dpp(0, r, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+  if (lp >= 2) r += __builtin_amdgcn_update_dpp(0, r, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+  if (lp >= 3) r += __builtin_amdgcn_update_dpp(0, r, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  if (lp >= 4) r += __builtin_amdgcn_update_dpp(0, r, 0x140, 0xF, 0xF, false);  // row_mirror
+  if (lp >= 5) r += __shfl_xor(r, 16, kWave);
+  if (lp >= 6) r += __shfl_xor(r, 32, kWave);
+  return r;
 }
 
 // Exclusive offset of each thread's count within waves [w0, w0 + nw), and their total.
@@ -213,7 +229,7 @@ __device__ __forceinline__ void rank_axis(const uint64_t* comp, int S, int axis,
       }
       for (; u < S; u += P) r += comp[u] > me;
     }
-    for (int o = 1; o < P; o <<= 1) r += __shfl_xor(r, o, kWave);
+    r = group_sum(r, lp);
     if (part == 0 && e < S && r < k) {
       sh.ax_idx[axis][r] = static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(me & 0xFFFFFFFFull));
       sh.ax_sc[axis][r] = key32_value(static_cast<uint32_t>(me >> 32));
@@ -222,9 +238,29 @@ __device__ __forceinline__ void rank_axis(const uint64_t* comp, int S, int axis,
 }
 
 // Both axes' top-k into sh.ax_idx / sh.ax_sc.
+// The additive grid's candidates (a+1)(b+1) <= m as a table, row by row, and ceil(m / r) for
+// the corner bound; one wave, while the score loads are in flight.
+__device__ __forceinline__ void additive_tables(int k, int m, SelectShared& sh) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int R = min(k, m);
+  int carry = 0;
+  for (int a0 = 0; a0 < R; a0 += kWave) {
+    const int a = a0 + lane;
+    const int len = a < R ? min(k, m / (a + 1)) : 0;
+    const int first = carry + wave_scan_dpp(len) - len;
+    for (int b = 0; b < len; ++b) sh.grid_ab[first + b] = static_cast<uint16_t>((a << 8) | b);
+    if (a < R) {
+      const int c = (m + a) / (a + 1);                   // ceil(m / r), r = a + 1
+      sh.th_col[a + 1] = static_cast<uint8_t>(c <= k ? c : 0);
+    }
+    carry += __shfl(first + len, kWave - 1, kWave);
+  }
+  if (lane == 0) sh.grid_total = carry;
+}
+
 template <int NV, int VEC>
 __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, int h, int n, int k,
-                            uint64_t* comp_all, SelectShared& sh) {
+                            int m, bool tables, uint64_t* comp_all, SelectShared& sh) {
   constexpr int NE = NV * VEC;
   const int tid = threadIdx.x;
   const int axis = tid / GROUP;
@@ -245,6 +281,7 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
       key[j] = order_key(src[min(GROUP * j + g, n - 1)]);
     }
   }
+  if (tables && tid < kWave) additive_tables(k, m, sh);
   uint32_t mx = 0u;
 #pragma unroll
   for (int j = 0; j < NV; ++j)
@@ -368,7 +405,7 @@ __device__ __forceinline__ void rank_candidates(const Cand* cand, int S, int m, 
       }
       for (; u < S; u += P) r += before(cand[u], ks, is);
     }
-    for (int o = 1; o < P; o <<= 1) r += __shfl_xor(r, o, kWave);
+    r = group_sum(r, lp);
     if (part == 0 && e < S && r < m) {
       sh.out_flat[r] = is;
       sh.out_g[r] = key64_value(ks);
@@ -470,7 +507,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
   if (tucker && tid < rank * rank) sh.core[tid] = core_all[static_cast<size_t>(h) * rank * rank + tid];
   if (tid < 2) sh.ax_cnt[tid] = 0;
   if (tid == 0) sh.grid_cnt = 0;
-  select_axes<NV, VEC>(sel, T, H, t, h, n, k, reinterpret_cast<uint64_t*>(dyn), sh);
+  select_axes<NV, VEC>(sel, T, H, t, h, n, k, m, !tucker, reinterpret_cast<uint64_t*>(dyn), sh);
   if (axis_out != nullptr)
     for (int a = tid; a < 2 * k; a += THREADS)
       axis_out[((static_cast<size_t>(a / k) * T + t) * H + h) * k + a % k] = sh.ax_idx[a / k][a % k];
@@ -484,20 +521,21 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     uint64_t th = 0ull;
     for (int r0 = 1; r0 <= R; r0 += kWave) {
       const int r = r0 + lane;
-      const int c = r <= R ? (m + r - 1) / r : k + 1;
-      if (c <= k)
+      const int c = r <= R ? sh.th_col[r] : 0;
+      if (c > 0)
         th = max(th, order_key64(static_cast<double>(sh.ax_sc[0][r - 1]) + static_cast<double>(sh.ax_sc[1][c - 1])));
     }
     th = wave_max_u64(th);
-    const float inv_k = 1.0f / static_cast<float>(k);
-    for (int c0 = wave * kWave; c0 < R * k; c0 += THREADS) {
+    const int C = sh.grid_total;
+    for (int c0 = wave * kWave; c0 < C; c0 += THREADS) {
       const int c = c0 + lane;
-      // a = c / k: (c + 1/2) / k is at least 1/(2k) away from an integer, far beyond the fp32 error
-      const int a = static_cast<int>((static_cast<float>(c) + 0.5f) * inv_k);
-      const int b = c - a * k;
       uint64_t key = 0ull;
       bool keep = false;
-      if (c < R * k && (a + 1) * (b + 1) <= m) {
+      int a = 0, b = 0;
+      if (c < C) {
+        const int ab = sh.grid_ab[c];
+        a = ab >> 8;
+        b = ab & 0xFF;
         key = order_key64(static_cast<double>(sh.ax_sc[0][a]) + static_cast<double>(sh.ax_sc[1][b]));
         keep = key >= th;
       }
