@@ -5,20 +5,21 @@
 // score is sum_rho f[rho] S_rho[t, i] with f = u (rows) or t (columns), the leading singular pair
 // of the head's Tucker core (eqs. (6), (8), (9)); for the additive grid f = [1].
 //
-// Two kernels compute the same scores:
-//  * axis_scores_mfma (slices of 16-multiple width, dk <= 256): scores as a GEMM on
-//    v_mfma_f32_16x16x4_f32.  A workgroup covers 64 keys x 16*MT tokens of one (head, axis): each
-//    of its 4 waves owns 16 keys and loads their key rows straight into registers (every load
-//    issued up front: one memory round trip), while the query tile is staged once in LDS and
-//    shared by the waves.  Each key is read from HBM once per token tile; at decode (T <= 64)
-//    once in total.
-//  * axis_scores_split (the same shapes, decode-sized T <= 64): a workgroup covers only 16 keys
-//    x 16*MT tokens, and its 4 waves split the key/query dim into quarters.  Each lane loads its
-//    key and query fragments straight into registers, so nothing waits on a barrier before the
-//    MFMAs; the four partial tiles meet once in LDS.  With 4x the workgroups of the kernel above
-//    every CU has several in flight, which hides the memory latency that bounds small T.
+// Four kernels compute the same scores (dk in {64, 128, 256} take one of the first three):
+//  * axis_scores_split (T <= 16): a workgroup covers 16 keys x 16 tokens of one (head, axis) on
+//    v_mfma_f32_16x16x4_f32, and its 4 waves split the key/query dim into quarters.  Each lane
+//    loads its key and query fragments straight into registers, so nothing waits on a barrier
+//    before the MFMAs; the four partial tiles meet once in LDS.  Many small workgroups keep
+//    several in flight per CU, which hides the memory latency that bounds small T.
+//  * axis_scores_wide (16 < T <= 64): the same split of the dim, on v_mfma_f32_32x32x2f32 over
+//    32 keys x 32 tokens: half the query fetches per key, and stores of 128-byte runs.
+//  * axis_scores_mfma (larger T): a workgroup covers 64 keys x 16*MT tokens; each of its 4 waves
+//    owns 16 keys and loads their key rows straight into registers, while the query tile is
+//    staged once in LDS and shared by the waves.  Each key is read once per token tile.
 //  * axis_scores_valu (any shape): a TT x TN tile on the vector ALUs, key and query tiles
 //    streamed through LDS in chunks of DC dims.
+// With a rank-r core each slice's partial scores are multiplied by their factor (u or t) before
+// they are summed; for the additive grid the factor is 1.
 #include "umem_internal.h"
 
 namespace umem {
@@ -310,6 +311,68 @@ __global__ __launch_bounds__(THREADS) void axis_scores_split(
   }
 }
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Decode-sized T on v_mfma_f32_32x32x2f32: a workgroup covers 32 keys x 32 tokens of one (head,
+// axis) and its 4 waves split the dim into quarters of DW = dk / 4.  Lane l (token / key l % 32,
+// half l / 32) holds dims d0 + (l / 32) * DW/2 .. + DW/2 - 1 of its token and of its key, so
+// MFMA i pairs dims d0 + i and d0 + DW/2 + i.  The four partial tiles meet in LDS; wave w adds
+// them (in wave order) for tokens 8w .. 8w + 7 and stores 128-byte runs of keys.
+template <int NV4>
+__global__ __launch_bounds__(THREADS) void axis_scores_wide(
+    const float* __restrict__ q_row, const float* __restrict__ q_col,
+    const float* __restrict__ k_row, const float* __restrict__ k_col,
+    const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
+    int rank, float4* __restrict__ zero, int zero_n4) {
+  clear_with_grid(zero, zero_n4);
+  constexpr int HALF = 4 * NV4;                 // DW / 2 dims per lane
+  __shared__ float part[4][16][kWave];          // the four waves' D fragments
+  const int axis = blockIdx.z & 1;
+  const int h = blockIdx.z >> 1;
+  const float* __restrict__ q = axis ? q_col : q_row;
+  const float* __restrict__ K = axis ? k_col : k_row;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int c = lane & 31, hh = lane >> 5;
+  const int key = blockIdx.x * 32 + c;
+  const int tok = blockIdx.y * 32 + c;
+  const int d0 = wave * 2 * HALF + hh * HALF;
+  f32x4 kf[NV4], qf[NV4];
+  const float* krow = K + (static_cast<size_t>(h) * n + (key < n ? key : n - 1)) * dk + d0;
+  const float* qrow = q + (static_cast<size_t>(tok < T ? tok : T - 1) * H + h) * dk + d0;
+#pragma unroll
+  for (int i = 0; i < NV4; ++i) kf[i] = *reinterpret_cast<const f32x4*>(krow + 4 * i);
+#pragma unroll
+  for (int i = 0; i < NV4; ++i) qf[i] = *reinterpret_cast<const f32x4*>(qrow + 4 * i);
+  f32x16 acc;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) acc[j] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NV4; ++i) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qf[i].x, kf[i].x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qf[i].y, kf[i].y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qf[i].z, kf[i].z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qf[i].w, kf[i].w, acc, 0, 0, 0);
+  }
+  // a wave's quarter of the dims lies in one slice (the launcher checks 4 % rank == 0): fold it
+  if (factors != nullptr) {
+    const float f = factors[(h * 2 + axis) * kMaxRank + (wave * 2 * HALF) / (dk / rank)];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[j] *= f;
+  }
+#pragma unroll
+  for (int j = 0; j < 16; ++j) part[wave][j][lane] = acc[j];
+  __syncthreads();
+  // D register j of lane l: token 8 (j / 4) + 4 (l / 32) + j % 4, key l % 32
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) {
+    const int j = 4 * wave + jj;
+    const float o = ((part[0][j][lane] + part[1][j][lane]) + part[2][j][lane]) + part[3][j][lane];
+    const int t = blockIdx.y * 32 + 8 * wave + 4 * hh + jj;
+    if (t < T && key < n) sel[((static_cast<size_t>(axis) * T + t) * H + h) * n + key] = o;
+  }
+}
+
 }  // namespace
 
 __global__ void rank1_kernel(const float* __restrict__ core, int H, int r, float* __restrict__ factors) {
@@ -335,23 +398,27 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
   if (T == 0) return hipSuccess;
   const float* c = (d.grid == UMEM_GRID_TUCKER) ? factors : nullptr;
   const int width = d.dk / d.rank;
-  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && width % 16 == 0 && T <= 64 &&
+  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && width % 16 == 0 && T <= 16 &&
       4 % d.rank == 0) {
-    const int mt = T <= 16 ? 1 : 2;
-    dim3 grid((d.n_keys + 15) / 16, (T + 16 * mt - 1) / (16 * mt), d.heads * 2);
-#define UMEM_SPLIT(MT, CPW)                                                                      \
-  hipLaunchKernelGGL((axis_scores_split<MT, CPW>), grid, dim3(THREADS), 0, s, q_row, q_col,      \
+    dim3 grid((d.n_keys + 15) / 16, 1, d.heads * 2);
+#define UMEM_SPLIT(CPW)                                                                          \
+  hipLaunchKernelGGL((axis_scores_split<1, CPW>), grid, dim3(THREADS), 0, s, q_row, q_col,       \
                      k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank, zero, zero_n4)
-    if (mt == 1) {
-      if (d.dk == 64) UMEM_SPLIT(1, 1);
-      else if (d.dk == 128) UMEM_SPLIT(1, 2);
-      else UMEM_SPLIT(1, 4);
-    } else {
-      if (d.dk == 64) UMEM_SPLIT(2, 1);
-      else if (d.dk == 128) UMEM_SPLIT(2, 2);
-      else UMEM_SPLIT(2, 4);
-    }
+    if (d.dk == 64) UMEM_SPLIT(1);
+    else if (d.dk == 128) UMEM_SPLIT(2);
+    else UMEM_SPLIT(4);
 #undef UMEM_SPLIT
+    return hipGetLastError();
+  }
+  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && T > 16 && T <= 64 && 4 % d.rank == 0) {
+    dim3 grid((d.n_keys + 31) / 32, (T + 31) / 32, d.heads * 2);
+#define UMEM_WIDE(NV4)                                                                            \
+  hipLaunchKernelGGL((axis_scores_wide<NV4>), grid, dim3(THREADS), 0, s, q_row, q_col, k_row,     \
+                     k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank, zero, zero_n4)
+    if (d.dk == 64) UMEM_WIDE(2);
+    else if (d.dk == 128) UMEM_WIDE(4);
+    else UMEM_WIDE(8);
+#undef UMEM_WIDE
     return hipGetLastError();
   }
   if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && width % 16 == 0) {
