@@ -13,7 +13,9 @@ It follows the paper ("Ultra-Sparse Memory Network", Huang et al.) step by step:
                     Sec. 3.2 removes the softmax) or eq. (3)'s SoftMax
 6. address map      Sec. 3.1 (physical address n*i + j); Sec. 3.2 IVE eq. (14) Shuffle and the
                     block concatenation of eq. (13)
-7. gather-sum       eq. (1) o = V^T s; eq. (15) V^T s_p per virtual block; heads add (Sec. 3.1)
+7. gather-sum       eq. (1) o = V^T s; eq. (15) V^T s_p per virtual block; heads add (Sec. 3.1);
+                    with multi-core scoring (Sec. 3.2 MCS), eq. (17): column slice i of the
+                    values pooled with core i's scores
 8. projection       eq. (15) sum_p W_p^T (.); output linear of Trick 6 (Sec. 3.2)
 
 Readings where the paper is silent or ambiguous (each is also a test):
@@ -33,6 +35,11 @@ Readings where the paper is silent or ambiguous (each is also a test):
 * IVE layout: blocks p = 0..E-1; virtual slot v = p * N_p + physical row (the concatenation
   order of eq. (13)); the shuffle sends the score of logical slot x to virtual slot perm[x].
 * Heads: each head has its own keys and core, all heads share V, and their pooled outputs add.
+* Multi-core scoring (Sec. 3.2, eqs. (16), (17)): the Tucker core of each head is given as h
+  component cores; selection runs on their sum (eq. (16)), and each selected slot carries h
+  scores, S_row^T C^(i) S_col, that weight column slice i (of Dv / h columns) of its value row.
+  With IVE the physical rows are split.  Only raw scores are defined for it (the paper pairs
+  MCS with Trick 1's removal of the softmax).
 * Precision: everything in fp64 from the stored fp32 / bf16 inputs (a product of two fp32 numbers
   is exact in fp64).
 """
@@ -49,7 +56,7 @@ DEGENERATE_GAP = 1e-9
 
 __all__ = [
     "GRID_ADD", "GRID_TUCKER", "W_RAW", "W_SOFTMAX", "axis_scores", "rank1_factors",
-    "selection_scores", "top_sorted", "grid_topm", "pooling_weights", "score_topk",
+    "selection_scores", "top_sorted", "grid_topm", "core_scores", "pooling_weights", "score_topk",
     "address_map", "gather_sum", "ive_project", "forward",
 ]
 
@@ -153,6 +160,24 @@ def grid_topm(S_row, S_col, I_row, I_col, n: int, m: int, grid: int = GRID_ADD, 
     return flat[order], g[order]
 
 
+def core_scores(S_row, S_col, flat, n: int, core_parts) -> np.ndarray:
+    """Per-core scores of the selected slots -- multi-core scoring, Sec. 3.2, eq. (16):
+    S^(i) = S_row^T C^(i) S_col at slot (i_row, j_col) = divmod(flat, n).
+
+    S_row, S_col: [r, n] of one (token, head); core_parts: [h, r, r].  Returns [len(flat), h].
+    """
+    flat = np.asarray(flat, dtype=np.int64)
+    ii, jj = flat // n, flat % n
+    parts = np.asarray(core_parts, dtype=np.float64)
+    h, r, _ = parts.shape
+    out = np.zeros((len(flat), h))
+    for c in range(h):
+        for rho in range(r):
+            for sig in range(r):
+                out[:, c] += S_row[rho, ii] * parts[c, rho, sig] * S_col[sig, jj]
+    return out
+
+
 def pooling_weights(g, weight: int = W_RAW) -> np.ndarray:
     """Weights of the m selected slots of one (token, head).
 
@@ -168,13 +193,21 @@ def pooling_weights(g, weight: int = W_RAW) -> np.ndarray:
 
 
 def score_topk(q_row, q_col, K_row, K_col, topk: int, topm: int, grid: int = GRID_ADD,
-               weight: int = W_RAW, core=None, rank: int = 1):
+               weight: int = W_RAW, core=None, rank: int = 1, core_parts=None):
     """Steps 1-5 for every token and head.  Returns a dict with
 
     idx [T, H, m] logical flat indices (sorted), w [T, H, m] weights, g [T, H, m] grid scores,
     axis_idx [2, T, H, k] per-axis top-k (row, col; sorted), sel_row / sel_col [T, H, n] the
     per-axis selection scores, S_row / S_col [T, H, r, n], factors [(u, t, sig)] per head.
+
+    Multi-core scoring: core_parts [H, h, r, r] are the component cores (core must then be None);
+    selection runs on their sum, and w_core [T, H, m, h] holds each core's score of every
+    selected slot (raw weights only).
     """
+    if core_parts is not None:
+        if core is not None or grid != GRID_TUCKER or weight != W_RAW:
+            raise ValueError("multi-core scoring takes component cores, the Tucker grid, raw weights")
+        core = np.asarray(core_parts, dtype=np.float64).sum(axis=1)     # eq. (16)
     T, H, dk = np.shape(q_row)
     n = np.shape(K_row)[1]
     if grid == GRID_ADD:
@@ -195,6 +228,7 @@ def score_topk(q_row, q_col, K_row, K_col, topk: int, topm: int, grid: int = GRI
     w = np.empty((T, H, topm))
     g = np.empty((T, H, topm))
     axis_idx = np.empty((2, T, H, topk), dtype=np.int64)
+    w_core = None if core_parts is None else np.empty((T, H, topm, np.shape(core_parts)[1]))
     for t in range(T):
         for h in range(H):
             I_row = top_sorted(sel_row[t, h], topk)
@@ -204,8 +238,10 @@ def score_topk(q_row, q_col, K_row, K_col, topk: int, topm: int, grid: int = GRI
             idx[t, h], g[t, h] = flat, gs
             w[t, h] = pooling_weights(gs, weight)
             axis_idx[0, t, h], axis_idx[1, t, h] = I_row, I_col
+            if core_parts is not None:
+                w_core[t, h] = core_scores(S_row[t, h], S_col[t, h], flat, n, core_parts[h])
     return dict(idx=idx, w=w, g=g, axis_idx=axis_idx, sel_row=sel_row, sel_col=sel_col,
-                S_row=S_row, S_col=S_col, factors=factors)
+                S_row=S_row, S_col=S_col, factors=factors, w_core=w_core)
 
 
 def address_map(idx, perm=None, n_values: int | None = None, expand: int = 1):
@@ -227,9 +263,11 @@ def gather_sum(value_rows, idx, w, perm=None, n_values: int | None = None, expan
     """Score-weighted pooling of the selected value rows -- eq. (1) o = V^T s, eq. (3), and
     eq. (15)'s per-block V^T s_p.
 
-    value_rows(rows) returns the stored rows [len(rows), Dv] (any float type); idx, w: [T, bag]
-    (a bag is all heads' m selections of a token).  Returns out [T, E, Dv] in fp64 with
-    out[t, p, :] = sum over entries b of block p of w[t, b] * V[row[t, b], :]; repeats add.
+    value_rows(rows) returns the stored rows [len(rows), Dv] (any float type); idx: [T, bag] (a
+    bag is all heads' m selections of a token); w: [T, bag], or [T, bag, h] with multi-core
+    scoring, where column slice i (Dv / h columns) of each row takes weight w[..., i] (eq. (17)).
+    Returns out [T, E, Dv] in fp64 with out[t, p, :] = sum over entries b of block p of
+    w[t, b] * V[row[t, b], :]; repeats add.
     """
     idx = np.asarray(idx, dtype=np.int64)
     w = np.asarray(w, dtype=np.float64)
@@ -240,7 +278,12 @@ def gather_sum(value_rows, idx, w, perm=None, n_values: int | None = None, expan
         vals = np.asarray(value_rows(row[t]), dtype=np.float64)
         if out is None:
             out = np.zeros((T, expand, vals.shape[1]))
-        np.add.at(out[t], p[t], w[t][:, None] * vals)
+        if w.ndim == 2:
+            wt = w[t][:, None]
+        else:
+            h = w.shape[2]
+            wt = np.repeat(w[t], vals.shape[1] // h, axis=1)   # weight of each column
+        np.add.at(out[t], p[t], wt * vals)
     return out
 
 
@@ -267,12 +310,12 @@ def ive_project(pooled, W_proj=None, W_out=None) -> np.ndarray:
 
 def forward(q_row, q_col, K_row, K_col, value_rows, topk: int, topm: int, grid: int = GRID_ADD,
             weight: int = W_RAW, core=None, rank: int = 1, perm=None, n_values=None,
-            expand: int = 1, W_proj=None, W_out=None):
+            expand: int = 1, W_proj=None, W_out=None, core_parts=None):
     """The whole layer (steps 1-8).  Returns (output, score_topk dict, pooled [T, E, Dv])."""
-    sel = score_topk(q_row, q_col, K_row, K_col, topk, topm, grid, weight, core, rank)
+    sel = score_topk(q_row, q_col, K_row, K_col, topk, topm, grid, weight, core, rank, core_parts)
     T, H, m = sel["idx"].shape
-    pooled = gather_sum(value_rows, sel["idx"].reshape(T, H * m), sel["w"].reshape(T, H * m),
-                        perm, n_values, expand)
+    w = sel["w"].reshape(T, H * m) if core_parts is None else sel["w_core"].reshape(T, H * m, -1)
+    pooled = gather_sum(value_rows, sel["idx"].reshape(T, H * m), w, perm, n_values, expand)
     if W_proj is None and W_out is None:
         out = pooled[:, 0, :] if expand == 1 else pooled
     else:

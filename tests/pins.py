@@ -324,6 +324,71 @@ def pin_ive_concat_same_column(O):
             assert len(cols) == 1 and len(x[row == r]) == E
 
 
+# ---------------------------------------------------------------- multi-core scoring
+
+def pin_golden_mcs(O):
+    g = _golden("mcs_two_cores_n2.json")
+    args = (_arr(g["q_row"]), _arr(g["q_col"]), _arr(g["K_row"]), _arr(g["K_col"]), g["topk"])
+    V = _arr(g["values"])
+    res = O.score_topk(*args, 2, O.GRID_TUCKER, O.W_RAW, rank=g["rank"], core_parts=_arr(g["core_parts"]))
+    assert list(res["idx"][0, 0]) == g["expect_idx_m2"]
+    assert np.allclose(res["g"][0, 0], g["expect_g_m2"], rtol=0, atol=1e-12)
+    assert np.allclose(res["w_core"][0, 0], g["expect_w_core_m2"], rtol=0, atol=1e-12)
+    out, _, _ = O.forward(*args[:4], lambda r: V[r], g["topk"], 2, O.GRID_TUCKER, O.W_RAW,
+                          rank=g["rank"], core_parts=_arr(g["core_parts"]))
+    assert np.allclose(out[0], g["expect_out_m2"], rtol=0, atol=1e-12)
+    res3 = O.score_topk(*args, 3, O.GRID_TUCKER, O.W_RAW, rank=g["rank"], core_parts=_arr(g["core_parts"]))
+    assert list(res3["idx"][0, 0]) == g["expect_idx_m3"]
+    assert np.allclose(res3["w_core"][0, 0], g["expect_w_core_m3"], rtol=0, atol=1e-12)
+
+
+def pin_mcs_scores_add_up(O, seeds=range(4)):
+    """eq. (16): the component scores of every selected slot add up to its grid score, and the
+    selection is the one the summed core makes; one component reproduces the plain grid."""
+    for seed in seeds:
+        rng = np.random.default_rng(11000 + seed)
+        n, r, T, H, k, m, h = 7, 2, 2, 2, 4, 6, 3
+        qr, qc, Kr, Kc = _rand_layer(rng, n, 2 * r, T, H)
+        parts = rng.standard_normal((H, h, r, r))
+        res = O.score_topk(qr, qc, Kr, Kc, k, m, O.GRID_TUCKER, O.W_RAW, rank=r, core_parts=parts)
+        whole = O.score_topk(qr, qc, Kr, Kc, k, m, O.GRID_TUCKER, O.W_RAW, core=parts.sum(axis=1), rank=r)
+        assert np.array_equal(res["idx"], whole["idx"])
+        assert np.allclose(res["w_core"].sum(axis=3), whole["g"], rtol=1e-12, atol=1e-12)
+        ex = BF.exhaustive_scores_tucker(qr, qc, Kr, Kc, parts[:, 1], r)   # core 1 alone, all slots
+        for t in range(T):
+            for hd in range(H):
+                assert np.allclose(res["w_core"][t, hd, :, 1], ex[t, hd][res["idx"][t, hd]],
+                                   rtol=1e-12, atol=1e-12)
+        one = O.score_topk(qr, qc, Kr, Kc, k, m, O.GRID_TUCKER, O.W_RAW, rank=r, core_parts=parts[:, :1])
+        assert np.array_equal(one["w_core"][..., 0], one["g"])
+
+
+def pin_mcs_dense_pool(O, seeds=range(3)):
+    """eq. (17) as written: dense score vectors s^(i) over all N slots, o = [s^(1)T V^(1), ...];
+    with IVE, the physical rows split, per virtual block (eq. (15))."""
+    for seed in seeds:
+        rng = np.random.default_rng(12000 + seed)
+        h, dv, T, bag, Np = 2, 6, 3, 9, 16
+        V = rng.standard_normal((Np, dv))
+        idx = rng.integers(0, Np, size=(T, bag))
+        idx[:, 1] = idx[:, 0]                      # a repeated slot adds
+        w = rng.standard_normal((T, bag, h))
+        got = O.gather_sum(lambda r: V[r], idx, w, None, Np, 1)[:, 0, :]
+        want = np.concatenate([BF.dense_pool(V[:, c * dv // h:(c + 1) * dv // h], idx, w[:, :, c], Np)
+                               for c in range(h)], axis=1)
+        assert np.allclose(got, want, rtol=1e-12, atol=1e-12)
+        E = 4
+        perm = rng.permutation(E * Np)
+        idx = rng.integers(0, E * Np, size=(T, bag))
+        pooled = O.gather_sum(lambda r: V[r], idx, w, perm, Np, E)
+        v = perm[idx]
+        for p in range(E):
+            wp = np.where((v // Np) == p, 1.0, 0.0)[:, :, None] * w
+            want = np.concatenate([BF.dense_pool(V[:, c * dv // h:(c + 1) * dv // h], v % Np, wp[:, :, c], Np)
+                                   for c in range(h)], axis=1)
+            assert np.allclose(pooled[:, p, :], want, rtol=1e-12, atol=1e-12)
+
+
 ALL_PINS = [
     pin_golden_additive, pin_golden_tucker, pin_golden_signed_zero, pin_golden_ive, pin_golden_svd,
     pin_scores_full_keys, pin_exhaustive_topm_additive,
@@ -331,4 +396,5 @@ ALL_PINS = [
     pin_topology_bias, pin_softmax_full_vector, pin_gather_dense, pin_svd_closed_form,
     pin_svd_power_iteration, pin_tucker_rank1_core_exact, pin_tucker_exact_scores,
     pin_tucker_rank_one_slices, pin_ive_materialised, pin_ive_concat_same_column,
+    pin_golden_mcs, pin_mcs_scores_add_up, pin_mcs_dense_pool,
 ]

@@ -7,7 +7,7 @@ from tests.pins import ALL_PINS
 
 _orig = {name: getattr(O, name) for name in
          ("axis_scores", "rank1_factors", "selection_scores", "top_sorted", "grid_topm",
-          "pooling_weights", "address_map", "gather_sum", "ive_project")}
+          "pooling_weights", "address_map", "gather_sum", "ive_project", "core_scores")}
 
 
 def m_flat_transposed(S_row, S_col, I_row, I_col, n, m, grid=0, C=None):
@@ -96,7 +96,37 @@ def m_softmax_no_normalise(g, weight=0):
     return g.copy() if weight == 0 else np.exp(g - g.max())
 
 
+def m_core_scores_reversed(S_row, S_col, flat, n, core_parts):
+    return _orig["core_scores"](S_row, S_col, flat, n, core_parts)[:, ::-1]
+
+
+def m_mcs_one_weight_for_all(value_rows, idx, w, perm=None, n_values=None, expand=1):
+    w = np.asarray(w, dtype=np.float64)
+    if w.ndim == 3:
+        w = w.sum(axis=2)                       # the aggregated score on every slice
+    return _orig["gather_sum"](value_rows, idx, w, perm, n_values, expand)
+
+
+def m_mcs_slices_interleaved(value_rows, idx, w, perm=None, n_values=None, expand=1):
+    w = np.asarray(w, dtype=np.float64)
+    if w.ndim == 2:
+        return _orig["gather_sum"](value_rows, idx, w, perm, n_values, expand)
+    h = w.shape[2]
+    out = None
+    idx = np.asarray(idx)
+    p, row = O.address_map(idx, perm, n_values, expand)
+    for t in range(idx.shape[0]):
+        vals = np.asarray(value_rows(row[t]), dtype=np.float64)
+        if out is None:
+            out = np.zeros((idx.shape[0], expand, vals.shape[1]))
+        wt = np.tile(w[t], (1, vals.shape[1] // h))          # column c takes core c % h
+        np.add.at(out[t], p[t], wt * vals)
+    return out
+
+
 MUTANTS = [
+    ("core_scores", m_core_scores_reversed), ("gather_sum", m_mcs_one_weight_for_all),
+    ("gather_sum", m_mcs_slices_interleaved),
     ("grid_topm", m_flat_transposed), ("grid_topm", m_drop_col_term),
     ("grid_topm", m_core_transposed), ("top_sorted", m_bottom_k),
     ("top_sorted", m_ties_high_index), ("rank1_factors", m_sign_negative),
