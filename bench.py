@@ -126,7 +126,7 @@ class Runner:
         d.heads, d.dk, d.n_keys, d.rank = c.heads, c.dk, c.n_keys, c.rank
         d.topk, d.topm, d.grid, d.weight = c.topk, c.topm, c.grid, c.weight
         d.n_values, d.dv, d.vdtype, d.expand = c.n_values, c.dv, c.vdtype, c.expand
-        d.dv_virt, d.d_out, d.reserved = c.dv_virt, c.d_out, 0
+        d.dv_virt, d.d_out, d.cores = c.dv_virt, c.d_out, c.cores
         return d
 
     def forward(self, b):
@@ -157,7 +157,7 @@ class Runner:
     def gather(self, idx, w):
         U, dl, c = self.U, self.dl, self.cfg
         st = U.umem_gather_sum(c.n_values, c.dv, c.vdtype, dl.values, c.T, c.bag, idx, w, dl.perm,
-                               c.expand, self.out)
+                               c.expand, c.cores, self.out)
         if st:
             U.check(st, "umem_gather_sum")
 
@@ -246,7 +246,7 @@ class Runner:
 
         def launch(i):
             st = U.umem_gather_sum(c.n_values, c.dv, c.vdtype, dl.values, Tq, c.bag, stacks[i][0],
-                                   stacks[i][1], dl.perm, c.expand, outq)
+                                   stacks[i][1], dl.perm, c.expand, c.cores, outq)
             if st:
                 U.check(st, "umem_gather_sum")
         secs = self._graph_time([lambda i=i: launch(i % 2) for i in range(16)])

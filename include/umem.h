@@ -58,11 +58,13 @@ enum { UMEM_W_RAW = 0, UMEM_W_SOFTMAX = 1 };      /* Trick 1 (raw scores) / eq. 
 /* Shape of one memory layer.
  * Requirements (UMEM_ERR_INVALID_ARG otherwise): every count >= 1; dk % rank == 0;
  *   rank == 1 for UMEM_GRID_ADD; topk <= n_keys; topm <= topk^2; expand a perfect square with
- *   n_values * expand == n_keys^2; dv_virt > 0 when expand > 1; reserved == 0.
+ *   n_values * expand == n_keys^2; dv_virt > 0 when expand > 1; cores (h) of 0 or 1, or h >= 2
+ *   with the Tucker grid, raw weights and dv % h == 0.
  * Limits of this library (UMEM_ERR_UNSUPPORTED beyond them): max(n_keys, topk^2) <= 8192;
  *   topk <= 90 (64 for the Tucker grid); topm <= 256; rank <= 4; (dk / rank) % 4 == 0; dk <= 1024; heads <= 64;
  *   heads * topm <= 2048; expand <= 64; a value row (dv * element size) of 16 * 2^j <= 1024
- *   bytes or a multiple of 1024 up to 8192 bytes; T <= 2^20. */
+ *   bytes or a multiple of 1024 up to 8192 bytes; T <= 2^20; cores <= 8, each core's column
+ *   slice (dv / h elements) a multiple of 16 bytes. */
 typedef struct umem_desc {
   int32_t heads;    /* H: key sets (each with its own keys and core) sharing one value table */
   int32_t dk;       /* query/key dimension per axis per head */
@@ -78,7 +80,11 @@ typedef struct umem_desc {
   int32_t expand;   /* E: implicit value expansion (1 = none) */
   int32_t dv_virt;  /* D'v: IVE projector width (0 = no projection; required when expand > 1) */
   int32_t d_out;    /* output linear width (0 = none) */
-  int32_t reserved; /* must be 0 */
+  int32_t cores;    /* h: multi-core scoring (Sec. 3.2 MCS, eqs. (16), (17)); 0 or 1 = one core.
+                     * With h >= 2 each head's Tucker core is given as h component cores
+                     * [H, h, r, r]; selection runs on their sum, every selected slot carries
+                     * the h component scores as weights [.., m, h], and column slice i of each
+                     * value row (dv / h columns; physical rows with IVE) takes weight i. */
 } umem_desc;
 
 /* Bytes of scratch `ws` that umem_score_topk / umem_forward need for T tokens (a multiple of
@@ -92,7 +98,8 @@ UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_
  * positive and t = C^T u / sigma_1.  The singular pair is computed on the device, in fp64.
  *   q_row, q_col  fp32 [T, H, dk]  the two queries; may be the same pointer (Trick 5)
  *   k_row, k_col  fp32 [H, n, dk]  keys; with rank r each dk row holds r contiguous slices
- *   core          fp32 [H, r, r]   Tucker cores (NULL for UMEM_GRID_ADD)
+ *   core          fp32 [H, r, r]   Tucker cores (NULL for UMEM_GRID_ADD); [H, h, r, r] component
+ *                                  cores with multi-core scoring (their sum is the core)
  *   sel           fp32 [2, T, H, n] out: [0] row scores, [1] column scores
  *   ws            scratch for the singular vectors, Tucker grid only (2 KiB, 256-byte aligned;
  *                 a workspace sized by umem_workspace_size suffices); may be NULL otherwise */
@@ -107,7 +114,8 @@ UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const fl
  *   sel       fp32 [2, T, H, n] as written by umem_axis_scores, 16-byte aligned
  *   q_*, k_*, core  as above; read only for UMEM_GRID_TUCKER (may be NULL for ADD)
  *   idx       int32 [T, H, m] out: logical slot i*n + j, sorted by (score desc, index asc)
- *   w         fp32 [T, H, m] out: the weight of each slot (raw grid score, or SoftMax)
+ *   w         fp32 [T, H, m] out: the weight of each slot (raw grid score, or SoftMax); with
+ *             multi-core scoring [T, H, m, h]: the h component scores of each slot (eq. (16))
  *   axis_idx  int32 [2, T, H, k] out, optional (NULL): per-axis top-k, sorted
  *   values, pooled  optional (both NULL or both set): the value table [n_values, dv] and fp32
  *             [T, dv] (16-byte aligned); the selected rows are pooled as umem_gather_sum pools
@@ -132,15 +140,18 @@ UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const flo
  *   values  [n_values, dv] of vdtype, 16-byte aligned
  *   idx     int32 [T, bag]: logical slots; without perm and with expand == 1 they are physical
  *           rows (Sec. 3.1: slot (i, j) lives at row n*i + j)
- *   w       fp32 [T, bag]
+ *   w       fp32 [T, bag], or [T, bag, cores]: with cores = h >= 2 column slice i of each row
+ *           (dv / h columns) takes weight i (multi-core scoring, eq. (17))
  *   perm    int32 [expand * n_values] or NULL: the IVE shuffle (eq. (14)); slot x goes to virtual
  *           slot v = perm[x], block p = v / n_values, physical row v % n_values
+ *   cores   1 (or 0), or the h of multi-core scoring: dv % h == 0, each slice a multiple of
+ *           16 bytes, h <= 8
  *   out     fp32 [T, expand, dv], 16-byte aligned: out[t, p, :] = sum over the bag entries of
  *           block p of w * values[row, :] (fp32 accumulation; repeated rows add)
  * Every index must be in range ([0, n_values) without perm, [0, expand*n_values) with it). */
 UMEM_API umem_status umem_gather_sum(int64_t n_values, int32_t dv, int32_t vdtype, const void* values,
                             int32_t T, int32_t bag, const int32_t* idx, const float* w,
-                            const int32_t* perm, int32_t expand, float* out,
+                            const int32_t* perm, int32_t expand, int32_t cores, float* out,
                             hipStream_t stream);
 
 /* a8: y = sum_p pooled[:, p, :] W_p (eq. (15)), then y W_out (Trick 6).  bf16 operands (the
@@ -157,6 +168,7 @@ UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t
  *   w_proj, w_out    as for umem_project (w_proj required iff dv_virt > 0; w_out iff d_out > 0)
  *   out              fp32: [T, dv] without projection, else [T, d_out] (or [T, dv_virt])
  *   idx_out, w_out_scores  optional (NULL) copies of the selection, [T, H, m] each
+ *                    (w_out_scores [T, H, m, h] with multi-core scoring)
  * ws_bytes >= umem_workspace_size(desc, T). */
 UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float* q_row, const float* q_col,
                          const float* k_row, const float* k_col, const float* core,

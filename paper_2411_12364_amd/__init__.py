@@ -40,7 +40,7 @@ class umem_desc(ctypes.Structure):
         ("rank", ctypes.c_int32), ("topk", ctypes.c_int32), ("topm", ctypes.c_int32),
         ("grid", ctypes.c_int32), ("weight", ctypes.c_int32), ("n_values", ctypes.c_int64),
         ("dv", ctypes.c_int32), ("vdtype", ctypes.c_int32), ("expand", ctypes.c_int32),
-        ("dv_virt", ctypes.c_int32), ("d_out", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("dv_virt", ctypes.c_int32), ("d_out", ctypes.c_int32), ("cores", ctypes.c_int32),
     ]
 
 
@@ -61,7 +61,7 @@ def _load() -> ctypes.CDLL:
         "umem_axis_scores": [D, I32, P, P, P, P, P, P, P, SZ, P],
         "umem_select": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P],
         "umem_score_topk": [D, I32, P, P, P, P, P, P, P, P, P, SZ, P],
-        "umem_gather_sum": [I64, I32, I32, P, I32, I32, P, P, P, I32, P, P],
+        "umem_gather_sum": [I64, I32, I32, P, I32, I32, P, P, P, I32, I32, P, P],
         "umem_project": [I32, I32, I32, I32, I32, P, P, P, P, P, SZ, P],
         "umem_forward": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
     }
@@ -137,10 +137,10 @@ def umem_score_topk(desc, T, q_row, q_col, k_row, k_col, core, idx, w, axis_idx,
                                 _p(idx), _p(w), _p(axis_idx), _p(ws), ws_bytes, _s(stream))
 
 
-def umem_gather_sum(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, out,
+def umem_gather_sum(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores, out,
                     stream=None) -> int:
     return _lib.umem_gather_sum(n_values, dv, vdtype, _p(values), T, bag, _p(idx), _p(w), _p(perm),
-                                expand, _p(out), _s(stream))
+                                expand, cores, _p(out), _s(stream))
 
 
 def umem_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws, ws_bytes,

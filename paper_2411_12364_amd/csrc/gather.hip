@@ -57,11 +57,13 @@ struct ElemTraits<uint16_t> {   // bf16 bit patterns
 
 // Rows of one bag (or of one virtual block of it) are split into NWAVES contiguous ranges, one
 // per wave; sub-group `sub` of a wave (L lanes) reads entries beg + SUB * i + sub of its range.
-// `slot(j)` gives entry j's position in idx / w (after the block partition, if any).
+// `slot(j)` gives entry j's position in idx / w (after the block partition, if any).  With
+// multi-core scoring (cores > 1) entry s has cores weights, w_of[s * cores + i], and a lane's
+// 16-byte chunk takes the weight of the column slice it lies in.
 template <typename Elem, int L, int CPL, typename Slot>
 __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int dv, int cnt,
                                           const Slot& slot, const int32_t* __restrict__ rows_of,
-                                          const float* __restrict__ w_of, float* red,
+                                          const float* __restrict__ w_of, int cores, float* red,
                                           float* __restrict__ dst) {
   using TR = ElemTraits<Elem>;
   constexpr int EPC = TR::kPerChunk;
@@ -75,6 +77,9 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
   const int per_wave = (cnt + NWAVES - 1) / NWAVES;
   const int wbeg = wave * per_wave;
   const int wend = min(cnt, wbeg + per_wave);
+  int slice[CPL];                                  // this lane's chunks' core (0 with one core)
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) slice[c] = cores > 1 ? ((cl + L * c) * EPC) / (dv / cores) : 0;
 
   float acc[CPL][EPC];
 #pragma unroll
@@ -83,21 +88,24 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
     for (int e = 0; e < EPC; ++e) acc[c][e] = 0.0f;
   for (int j0 = wbeg; j0 < wend; j0 += SUB * U) {
     u32x4 raw[U][CPL];
-    float wt[U];
+    float wt[U][CPL];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = j0 + SUB * u + sub;
       if (j < wend) {
         const int s = slot(j);
-        wt[u] = w_of[s];
         const Elem* src = values + static_cast<int64_t>(rows_of[s]) * dv;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c)
+        for (int c = 0; c < CPL; ++c) {
+          wt[u][c] = w_of[static_cast<size_t>(s) * cores + slice[c]];
           raw[u][c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + (cl + L * c) * EPC));
+        }
       } else {
-        wt[u] = 0.0f;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) raw[u][c] = u32x4{0u, 0u, 0u, 0u};
+        for (int c = 0; c < CPL; ++c) {
+          wt[u][c] = 0.0f;
+          raw[u][c] = u32x4{0u, 0u, 0u, 0u};
+        }
       }
     }
 #pragma unroll
@@ -107,7 +115,7 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
         float x[EPC];
         TR::widen(raw[u][c], x);
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) acc[c][e] = fmaf(wt[u], x[e], acc[c][e]);
+        for (int e = 0; e < EPC; ++e) acc[c][e] = fmaf(wt[u][c], x[e], acc[c][e]);
       }
   }
   // combine the SUB sub-rows of this wave (lanes cl, cl + L, ...) with shuffles
@@ -166,13 +174,13 @@ template <typename Elem, int L, int CPL>
 __global__ __launch_bounds__(THREADS) void gather_kernel(
     const Elem* __restrict__ values, int64_t n_values, int dv, int bag,
     const int32_t* __restrict__ idx, const float* __restrict__ w, const int32_t* __restrict__ perm,
-    int expand, float* __restrict__ out) {
+    int expand, int cores, float* __restrict__ out) {
   extern __shared__ __align__(16) float red[];               // [red_rows][dv], then the bag
   const int t = blockIdx.x;
   const int32_t* __restrict__ idx_t = idx + static_cast<size_t>(t) * bag;
-  const float* __restrict__ w_t = w + static_cast<size_t>(t) * bag;
+  const float* __restrict__ w_t = w + static_cast<size_t>(t) * bag * cores;
   if (expand == 1) {
-    pool_rows<Elem, L, CPL>(values, dv, bag, [](int j) { return j; }, idx_t, w_t, red,
+    pool_rows<Elem, L, CPL>(values, dv, bag, [](int j) { return j; }, idx_t, w_t, cores, red,
                             out + static_cast<size_t>(t) * dv);
     return;
   }
@@ -209,7 +217,7 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
   for (int p = 0; p < expand; ++p) {
     const int beg = bstart[p];
     pool_rows<Elem, L, CPL>(values, dv, bcount[p], [=](int j) { return order[beg + j]; }, rows,
-                            w_t, red, out + (static_cast<size_t>(t) * expand + p) * dv);
+                            w_t, cores, red, out + (static_cast<size_t>(t) * expand + p) * dv);
     __syncthreads();
   }
 }
@@ -312,13 +320,13 @@ __global__ __launch_bounds__(THREADS) void gather_wave_kernel(
 template <typename Elem>
 hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int bag,
                         const int32_t* idx, const float* w, const int32_t* perm, int expand,
-                        float* out, hipStream_t s) {
+                        int cores, float* out, hipStream_t s) {
   const int chunks = dv * static_cast<int>(sizeof(Elem)) / 16;
   const size_t lds = static_cast<size_t>(dv <= 2048 ? NWAVES : 2) * dv * 4 +
                     (expand > 1 ? static_cast<size_t>(bag) * 12 : 0);
   const dim3 block(THREADS);
-  // thousands of tokens without expansion: a wave per token
-  const bool per_wave = expand == 1 && T >= kWaveTokensMin;
+  // thousands of tokens without expansion (or multi-core weights): a wave per token
+  const bool per_wave = expand == 1 && cores == 1 && T >= kWaveTokensMin;
   const dim3 grid(per_wave ? (T + NWAVES - 1) / NWAVES : T);
 #define UMEM_GATHER(LL, CC)                                                                      \
   if (per_wave)                                                                                  \
@@ -326,7 +334,7 @@ hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int
                        idx, w, out);                                                             \
   else                                                                                           \
     hipLaunchKernelGGL((gather_kernel<Elem, LL, CC>), grid, block, lds, s, values, n_values, dv,   \
-                       bag, idx, w, perm, expand, out)
+                       bag, idx, w, perm, expand, cores, out)
   switch (chunks) {
     case 1: UMEM_GATHER(1, 1); break;
     case 2: UMEM_GATHER(2, 1); break;
@@ -358,16 +366,21 @@ bool gather_row_supported(int dv, int vdtype) {
   return chunks % 64 == 0;
 }
 
+bool cores_supported(int dv, int vdtype, int cores) {
+  if (cores < 1 || cores > kMaxCores || dv % cores != 0) return false;
+  return (dv / cores) * (vdtype == UMEM_F32 ? 4 : 2) % 16 == 0;   // whole 16-byte chunks
+}
+
 hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* values, int T,
                          int bag, const int32_t* idx, const float* w, const int32_t* perm,
-                         int expand, float* out, hipStream_t s) {
+                         int expand, int cores, float* out, hipStream_t s) {
   clear_stale_error();
   if (T == 0) return hipSuccess;
   if (vdtype == UMEM_F32)
     return launch_typed(static_cast<const float*>(values), n_values, dv, T, bag, idx, w, perm,
-                        expand, out, s);
+                        expand, cores, out, s);
   return launch_typed(static_cast<const uint16_t*>(values), n_values, dv, T, bag, idx, w, perm,
-                      expand, out, s);
+                      expand, cores, out, s);
 }
 
 }  // namespace umem

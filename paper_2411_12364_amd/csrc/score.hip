@@ -375,17 +375,21 @@ __global__ __launch_bounds__(THREADS) void axis_scores_wide(
 
 }  // namespace
 
-__global__ void rank1_kernel(const float* __restrict__ core, int H, int r, float* __restrict__ factors) {
+// One thread per head; with multi-core scoring the head's component cores are summed first
+// (eq. (16)): the singular pair of the whole core drives the retrieval.
+__global__ void rank1_kernel(const float* __restrict__ core, int H, int r, int parts,
+                             float* __restrict__ factors) {
   const int h = threadIdx.x;
   if (h < H) {
     float* f = factors + h * 2 * kMaxRank;
-    rank1_factors(core + static_cast<size_t>(h) * r * r, r, f, f + kMaxRank);
+    rank1_factors(core + static_cast<size_t>(h) * parts * r * r, r, parts, f, f + kMaxRank);
   }
 }
 
 hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, hipStream_t s) {
   clear_stale_error();
-  hipLaunchKernelGGL(rank1_kernel, dim3(1), dim3(kWave), 0, s, core, d.heads, d.rank, factors);
+  hipLaunchKernelGGL(rank1_kernel, dim3(1), dim3(kWave), 0, s, core, d.heads, d.rank, n_cores(d),
+                     factors);
   return hipGetLastError();
 }
 

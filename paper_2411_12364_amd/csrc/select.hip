@@ -28,6 +28,8 @@
 // For the forward without expansion (at most two heads, rows of 1 or 2 KiB) the workgroup also
 // pools its m rows (eq. (1)) and adds them into the token's output: the decode path then needs
 // no separate gather launch.
+// With multi-core scoring (eqs. (16), (17)) the selection runs on the summed core and, for the
+// m selected slots, each component core's exact score is computed (fp64) as its weight.
 // Tucker grid (eq. (10)): all k*k candidates, the exact per-slice scores recomputed for the
 // selected keys, candidate scores in fp64; the threshold of step 1 runs on their fp32 roundings
 // (rounding is monotone, so the survivors still contain the top-m) and the ranks on fp64.
@@ -58,7 +60,10 @@ struct SelectShared {
   uint8_t th_col[kMaxTopK + 1];       // ceil(m / r) for the corner bound of r rows (0: beyond k)
   float s_ex[2][kMaxRank][kMaxTopK];  // Tucker: exact per-slice scores of the selected keys
   double p_col[kMaxRank][kMaxTopK];   // Tucker: (C S_col)[rho, b] in fp64
-  float core[kMaxRank * kMaxRank];
+  double core[kMaxRank * kMaxRank];              // Tucker: the core (sum of its components)
+  float core_parts[kMaxCores][kMaxRank * kMaxRank];   // multi-core scoring: the components
+  int32_t out_ab[kMaxTopM];                      // Tucker: (a << 8) | b of each selected slot
+  float w_core[kMaxTopM * kMaxCores];            // multi-core scoring: weights [m][cores]
   int32_t out_flat[kMaxTopM];         // final top-m, by rank
   double out_g[kMaxTopM];
   float e[kMaxTopM];
@@ -394,10 +399,11 @@ __device__ __forceinline__ void rank_candidates(const Cand* cand, int S, int m, 
     const int slot = base + static_cast<int>(threadIdx.x);
     const int e = slot >> lp, part = slot & (P - 1);
     uint64_t ks = 0ull;
-    int is = 0, r = 0;
+    int is = 0, ab = 0, r = 0;
     if (e < S) {
       ks = cand[e].key;
       is = cand[e].id;
+      ab = cand[e].pad;
       int u = part;
       for (; u + 3 * P < S; u += 4 * P) {
         const Cand b0 = cand[u], b1 = cand[u + P], b2 = cand[u + 2 * P], b3 = cand[u + 3 * P];
@@ -409,6 +415,7 @@ __device__ __forceinline__ void rank_candidates(const Cand* cand, int S, int m, 
     if (part == 0 && e < S && r < m) {
       sh.out_flat[r] = is;
       sh.out_g[r] = key64_value(ks);
+      sh.out_ab[r] = ab;
     }
   }
   __syncthreads();
@@ -424,7 +431,7 @@ constexpr int kPoolRowsPerWave = kMaxPoolTopM / NWAVES;
 // of the wave's rows in flight), the 8 partial rows meet in LDS and are added in wave order, and
 // each element takes one atomic add per head.
 template <bool BF16>
-__device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool softmax,
+__device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool softmax, int cores,
                           const SelectShared& sh, float* red, float* __restrict__ out_t) {
   constexpr int EPC = BF16 ? 8 : 4;                  // elements per 16-byte chunk
   const int tid = threadIdx.x;
@@ -433,15 +440,26 @@ __device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool s
   const int cpl = dv * (BF16 ? 2 : 4) / 1024;        // 16-byte chunks per lane: 1 or 2
   const char* base = static_cast<const char*>(values);
   const size_t row_bytes = static_cast<size_t>(dv) * (BF16 ? 2 : 4);
+  // with multi-core scoring a lane's chunk c takes the weight of the column slice it lies in
+  // (a second chunk past a 1 KiB row is never loaded; its slice is clamped to a real one)
+  int slice[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+    slice[c] = cores > 1 ? min(((kWave * c + lane) * EPC) / (dv / cores), cores - 1) : 0;
   u32x4 raw[kPoolRowsPerWave][2];
-  float wt[kPoolRowsPerWave];
+  float wt[kPoolRowsPerWave][2];
 #pragma unroll
   for (int i = 0; i < kPoolRowsPerWave; ++i) {
     const int r = wave + NWAVES * i;
-    wt[i] = 0.0f;
+    wt[i][0] = wt[i][1] = 0.0f;
     raw[i][0] = raw[i][1] = u32x4{0u, 0u, 0u, 0u};
     if (r < m) {
-      wt[i] = softmax ? sh.e[r] / sh.esum : static_cast<float>(sh.out_g[r]);
+      if (cores > 1) {
+        wt[i][0] = sh.w_core[r * cores + slice[0]];
+        wt[i][1] = sh.w_core[r * cores + slice[1]];
+      } else {
+        wt[i][0] = wt[i][1] = softmax ? sh.e[r] / sh.esum : static_cast<float>(sh.out_g[r]);
+      }
       const u32x4* src = reinterpret_cast<const u32x4*>(base + static_cast<size_t>(sh.out_flat[r]) * row_bytes);
       raw[i][0] = __builtin_nontemporal_load(src + lane);
       if (cpl > 1) raw[i][1] = __builtin_nontemporal_load(src + kWave + lane);
@@ -460,10 +478,10 @@ __device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool s
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (BF16) {
-          acc[c][2 * e] = fmaf(wt[i], __uint_as_float(q[e] << 16), acc[c][2 * e]);
-          acc[c][2 * e + 1] = fmaf(wt[i], __uint_as_float(q[e] & 0xFFFF0000u), acc[c][2 * e + 1]);
+          acc[c][2 * e] = fmaf(wt[i][c], __uint_as_float(q[e] << 16), acc[c][2 * e]);
+          acc[c][2 * e + 1] = fmaf(wt[i][c], __uint_as_float(q[e] & 0xFFFF0000u), acc[c][2 * e + 1]);
         } else {
-          acc[c][e] = fmaf(wt[i], __uint_as_float(q[e]), acc[c][e]);
+          acc[c][e] = fmaf(wt[i][c], __uint_as_float(q[e]), acc[c][e]);
         }
       }
     }
@@ -494,7 +512,8 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     const float* __restrict__ k_col, const float* __restrict__ core_all,
     int32_t* __restrict__ idx_out, float* __restrict__ w_out, int32_t* __restrict__ axis_out,
     const void* __restrict__ values, int vbf16, int dv, float* __restrict__ pooled,
-    int T, int H, int n, int dk, int rank, int k, int m, int tucker, int softmax, int n_cand) {
+    int T, int H, int n, int dk, int rank, int k, int m, int tucker, int softmax, int n_cand,
+    int cores) {
   extern __shared__ __align__(16) unsigned char dyn[];
   __shared__ SelectShared sh;
   const int tid = threadIdx.x;
@@ -504,7 +523,16 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
   const int h = blockIdx.x % H;
 
   // ---- a3: the two axes, four waves each
-  if (tucker && tid < rank * rank) sh.core[tid] = core_all[static_cast<size_t>(h) * rank * rank + tid];
+  if (tucker && tid < rank * rank) {
+    const float* ch = core_all + static_cast<size_t>(h) * cores * rank * rank;
+    double c = 0.0;
+    for (int i = 0; i < cores; ++i) {
+      const float x = ch[i * rank * rank + tid];
+      c += static_cast<double>(x);                 // eq. (16): the core is the sum
+      if (cores > 1) sh.core_parts[i][tid] = x;
+    }
+    sh.core[tid] = c;
+  }
   if (tid < 2) sh.ax_cnt[tid] = 0;
   if (tid == 0) sh.grid_cnt = 0;
   select_axes<NV, VEC>(sel, T, H, t, h, n, k, m, !tucker, reinterpret_cast<uint64_t*>(dyn), sh);
@@ -578,7 +606,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       const int rho = job / k, b = job % k;
       double p = 0.0;
       for (int sg = 0; sg < rank; ++sg)
-        p += static_cast<double>(sh.core[rho * rank + sg]) * static_cast<double>(sh.s_ex[1][sg][b]);
+        p += sh.core[rho * rank + sg] * static_cast<double>(sh.s_ex[1][sg][b]);
       sh.p_col[rho][b] = p;
     }
     __syncthreads();
@@ -621,6 +649,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
         if ((c < kk) & (k32[j] >= L)) {
           cand[pos].key = k64[j];
           cand[pos].id = sh.ax_idx[0][c / k] * n + sh.ax_idx[1][c % k];
+          cand[pos].pad = ((c / k) << 8) | (c % k);
           ++pos;
         }
       }
@@ -669,8 +698,10 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       for (int j = 0; j < CPT; ++j) {
         const bool ok = tid + THREADS * j < kk;
         if (ok & ((k64[j] > theta) | ((k64[j] == theta) & (static_cast<uint32_t>(fl[j]) <= ylim)))) {
+          const int c = tid + THREADS * j;
           cand[pos].key = k64[j];
           cand[pos].id = fl[j];
+          cand[pos].pad = ((c / k) << 8) | (c % k);
           ++pos;
         }
       }
@@ -695,14 +726,31 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
   for (int j = tid; j < m; j += THREADS) {
     const size_t o = (static_cast<size_t>(t) * H + h) * m + j;
     idx_out[o] = sh.out_flat[j];
-    w_out[o] = softmax ? sh.e[j] / sh.esum : static_cast<float>(sh.out_g[j]);
+    if (cores == 1) w_out[o] = softmax ? sh.e[j] / sh.esum : static_cast<float>(sh.out_g[j]);
+  }
+  if (cores > 1) {
+    // multi-core scoring (eq. (16)): each core's exact score of every selected slot, in fp64
+    for (int x = tid; x < m * cores; x += THREADS) {
+      const int j = x / cores, i = x - (x / cores) * cores;
+      const int a = sh.out_ab[j] >> 8, b = sh.out_ab[j] & 0xFF;
+      double g = 0.0;
+      for (int rho = 0; rho < rank; ++rho) {
+        double p = 0.0;
+        for (int sg = 0; sg < rank; ++sg)
+          p += static_cast<double>(sh.core_parts[i][rho * rank + sg]) * static_cast<double>(sh.s_ex[1][sg][b]);
+        g += static_cast<double>(sh.s_ex[0][rho][a]) * p;
+      }
+      sh.w_core[x] = static_cast<float>(g);
+      w_out[((static_cast<size_t>(t) * H + h) * m + j) * cores + i] = static_cast<float>(g);
+    }
+    __syncthreads();
   }
   // ---- a7 fused: pool this head's rows into the token's output (the axes' LDS is free now)
   if (pooled != nullptr) {
     float* red = reinterpret_cast<float*>(dyn);
     float* out_t = pooled + static_cast<size_t>(t) * dv;
-    if (vbf16) pool_rows<true>(values, dv, m, softmax, sh, red, out_t);
-    else pool_rows<false>(values, dv, m, softmax, sh, red, out_t);
+    if (vbf16) pool_rows<true>(values, dv, m, softmax, cores, sh, red, out_t);
+    else pool_rows<false>(values, dv, m, softmax, cores, sh, red, out_t);
   }
 }
 
@@ -743,7 +791,7 @@ hipError_t launch_select(const umem_desc& d, int T, const float* sel, const floa
   hipLaunchKernelGGL((select_kernel<NV, VEC>), grid, block, lds, s, sel, q_row, q_col, k_row,    \
                      k_col, core, idx, w, axis_idx, values, d.vdtype == UMEM_BF16, d.dv, pooled,  \
                      T, d.heads, d.n_keys, d.dk, d.rank, d.topk,                                 \
-                     d.topm, tucker, d.weight == UMEM_W_SOFTMAX, n_cand)
+                     d.topm, tucker, d.weight == UMEM_W_SOFTMAX, n_cand, n_cores(d))
   const int n = d.n_keys;
   if (n % 4 == 0) {
     const int nv = (n + 1023) / 1024;

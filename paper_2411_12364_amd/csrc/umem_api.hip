@@ -28,7 +28,12 @@ umem_status check_desc(const umem_desc* d) {
   if (d->grid != UMEM_GRID_ADD && d->grid != UMEM_GRID_TUCKER) return UMEM_ERR_INVALID_ARG;
   if (d->weight != UMEM_W_RAW && d->weight != UMEM_W_SOFTMAX) return UMEM_ERR_INVALID_ARG;
   if (d->vdtype != UMEM_F32 && d->vdtype != UMEM_BF16) return UMEM_ERR_INVALID_ARG;
-  if (d->reserved != 0) return UMEM_ERR_INVALID_ARG;
+  if (d->cores < 0) return UMEM_ERR_INVALID_ARG;
+  if (d->cores > 1) {
+    if (d->grid != UMEM_GRID_TUCKER || d->weight != UMEM_W_RAW || d->dv % d->cores != 0)
+      return UMEM_ERR_INVALID_ARG;
+    if (!cores_supported(d->dv, d->vdtype, d->cores)) return UMEM_ERR_UNSUPPORTED;
+  }
   if (d->dk % d->rank != 0) return UMEM_ERR_INVALID_ARG;
   if (d->grid == UMEM_GRID_ADD && d->rank != 1) return UMEM_ERR_INVALID_ARG;
   if (d->topk > d->n_keys) return UMEM_ERR_INVALID_ARG;
@@ -82,7 +87,7 @@ Layout layout(const umem_desc* d, int32_t T) {
   L.idx = off;
   off += round_up(th * d->topm * sizeof(int32_t));
   L.w = off;
-  off += round_up(th * d->topm * sizeof(float));
+  off += round_up(th * d->topm * n_cores(*d) * sizeof(float));
   L.pooled = off;
   if (d->dv_virt > 0 || d->d_out > 0)
     off += round_up(static_cast<size_t>(T) * d->expand * d->dv * sizeof(float));
@@ -103,8 +108,9 @@ umem_status hip_status(hipError_t e) { return e == hipSuccess ? UMEM_OK : UMEM_E
 
 umem_status check_gather(int64_t n_values, int32_t dv, int32_t vdtype, const void* values,
                          int32_t T, int32_t bag, const int32_t* idx, const float* w,
-                         int32_t expand, const float* out) {
-  if (n_values < 1 || dv < 1 || bag < 1 || expand < 1) return UMEM_ERR_INVALID_ARG;
+                         int32_t expand, int32_t cores, const float* out) {
+  if (n_values < 1 || dv < 1 || bag < 1 || expand < 1 || cores < 0) return UMEM_ERR_INVALID_ARG;
+  if (cores > 1 && dv % cores != 0) return UMEM_ERR_INVALID_ARG;
   if (vdtype != UMEM_F32 && vdtype != UMEM_BF16) return UMEM_ERR_INVALID_ARG;
   umem_status st = check_tokens(T);
   if (st != UMEM_OK || T == 0) return st;
@@ -116,6 +122,7 @@ umem_status check_gather(int64_t n_values, int32_t dv, int32_t vdtype, const voi
   if (n_values * expand > (INT64_C(1) << 31)) return UMEM_ERR_UNSUPPORTED;
   if (bag > kMaxBag || expand > kMaxExpand) return UMEM_ERR_UNSUPPORTED;
   if (!gather_row_supported(dv, vdtype)) return UMEM_ERR_UNSUPPORTED;
+  if (cores > 1 && !cores_supported(dv, vdtype, cores)) return UMEM_ERR_UNSUPPORTED;
   return UMEM_OK;
 }
 
@@ -236,13 +243,14 @@ UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const flo
 UMEM_API umem_status umem_gather_sum(int64_t n_values, int32_t dv, int32_t vdtype,
                                      const void* values, int32_t T, int32_t bag,
                                      const int32_t* idx, const float* w, const int32_t* perm,
-                                     int32_t expand, float* out, hipStream_t stream) {
-  umem_status st = check_gather(n_values, dv, vdtype, values, T, bag, idx, w, expand, out);
+                                     int32_t expand, int32_t cores, float* out,
+                                     hipStream_t stream) {
+  umem_status st = check_gather(n_values, dv, vdtype, values, T, bag, idx, w, expand, cores, out);
   if (st != UMEM_OK || T == 0) return st;
   if (st == UMEM_OK && perm != nullptr && !aligned(perm, 4)) st = UMEM_ERR_INVALID_ARG;
   if (st != UMEM_OK) return st;
-  return hip_status(launch_gather(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, out,
-                                  stream));
+  return hip_status(launch_gather(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand,
+                                  cores > 1 ? cores : 1, out, stream));
 }
 
 UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt,
@@ -281,7 +289,7 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
   float* w = w_out_scores ? w_out_scores : reinterpret_cast<float*>(base + L.w);
   float* pooled = project ? reinterpret_cast<float*>(base + L.pooled) : out;
   st = check_gather(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, desc->expand,
-                    out);
+                    n_cores(*desc), out);
   if (st != UMEM_OK) return st;
 
   float* factors = reinterpret_cast<float*>(base + L.factors);
@@ -299,7 +307,7 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
                       fused ? values : nullptr, fused ? out : nullptr, stream);
   if (e == hipSuccess && !fused)
     e = launch_gather(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, perm,
-                      desc->expand, pooled, stream);
+                      desc->expand, n_cores(*desc), pooled, stream);
   if (e == hipSuccess && project)
     e = run_project(T, desc->expand, desc->dv, desc->dv_virt, desc->d_out, pooled, w_proj, w_out,
                     out, base + L.tmp, stream);

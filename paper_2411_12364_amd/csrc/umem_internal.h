@@ -13,6 +13,7 @@ constexpr int kMaxSelect = 8192;     // max(n, k*k): one selection's keys in 32 
 constexpr int kMaxTopK = 90;         // k*k <= kMaxSelect
 constexpr int kMaxTopKTucker = 64;   // Tucker: the k*k candidate keys in 16 KiB of LDS
 constexpr int kMaxTopM = 256;
+constexpr int kMaxCores = 8;          // multi-core scoring: component cores per head
 constexpr int kMaxPoolTopM = 64;      // the selection kernel pools rows itself up to this topm
 constexpr int kMaxPoolTokens = 512;   // ... and umem_forward lets it up to this many tokens
 constexpr int kMaxRank = 4;
@@ -56,9 +57,15 @@ hipError_t launch_select(const umem_desc& d, int T, const float* sel, const floa
 // atomic adds onto zero give the same bits in either order), topm <= 64 and rows of 1 or 2 KiB.
 bool select_pools(const umem_desc& d);
 
+// cores: 1, or the h of multi-core scoring (w is then [T, bag, h]; column slice i takes w[.., i]).
 hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* values, int T,
                          int bag, const int32_t* idx, const float* w, const int32_t* perm,
-                         int expand, float* out, hipStream_t s);
+                         int expand, int cores, float* out, hipStream_t s);
+
+// Multi-core scoring: the number of component cores of a layer (0 counts as 1), and whether
+// rows of this shape can be split into h column slices (each slice whole 16-byte chunks).
+inline int n_cores(const umem_desc& d) { return d.cores > 1 ? d.cores : 1; }
+bool cores_supported(int dv, int vdtype, int cores);
 
 hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const float* pooled,
                           const uint16_t* w_proj, const uint16_t* w_out, float* out, float* tmp,
@@ -112,12 +119,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float x) {
 // then the sign fixed so that u's largest-magnitude component (lowest index among equals) is
 // positive, and t = C^T u / sigma_1.  Writes u and t to u_out[0, r) and t_out[0, r).
 // Single-thread routine; all indexing is static.
-__device__ inline void rank1_factors(const float* C, int r, float* u_out, float* t_out) {
-  double c[4][4];
+__device__ inline void rank1_factors(const float* C, int r, int parts, float* u_out, float* t_out) {
+  double c[4][4];      // the core: the sum, in fp64, of its `parts` component cores [parts][r][r]
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) c[i][j] = (i < r && j < r) ? static_cast<double>(C[i * r + j]) : 0.0;
+    for (int j = 0; j < 4; ++j) {
+      double x = 0.0;
+      if (i < r && j < r)
+        for (int p = 0; p < parts; ++p) x += static_cast<double>(C[(p * r + i) * r + j]);
+      c[i][j] = x;
+    }
   double m[4][4], v[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)

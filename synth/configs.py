@@ -44,6 +44,7 @@ class Layer:
     queries: str = "gauss"        # "gauss" or "clusters"
     n_clusters: int = 8
     cluster_spread: float = 0.1
+    cores: int = 1                # multi-core scoring h (component cores per head; Tucker only)
 
     @property
     def n_slots(self) -> int:
@@ -117,9 +118,12 @@ def keys(cfg: Layer):
 
 
 def core(cfg: Layer) -> Optional[np.ndarray]:
-    """Tucker cores C_h as fp32 [H, r, r] (std 1), or None for the additive grid."""
+    """Tucker cores C_h as fp32 [H, r, r] (std 1), or None for the additive grid; with
+    multi-core scoring the component cores [H, h, r, r] (each std 1; their sum is the core)."""
     if cfg.grid != GRID_TUCKER:
         return None
+    if cfg.cores > 1:
+        return S.tensor_f32(cfg.seed, S.TID_CORE, (cfg.heads, cfg.cores, cfg.rank, cfg.rank), 1.0)
     return S.tensor_f32(cfg.seed, S.TID_CORE, (cfg.heads, cfg.rank, cfg.rank), 1.0)
 
 

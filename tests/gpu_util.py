@@ -13,8 +13,13 @@ def desc_for(cfg: CF.Layer) -> U.umem_desc:
     d.heads, d.dk, d.n_keys, d.rank = cfg.heads, cfg.dk, cfg.n_keys, cfg.rank
     d.topk, d.topm, d.grid, d.weight = cfg.topk, cfg.topm, cfg.grid, cfg.weight
     d.n_values, d.dv, d.vdtype, d.expand = cfg.n_values, cfg.dv, cfg.vdtype, cfg.expand
-    d.dv_virt, d.d_out, d.reserved = cfg.dv_virt, cfg.d_out, 0
+    d.dv_virt, d.d_out, d.cores = cfg.dv_virt, cfg.d_out, cfg.cores
     return d
+
+
+def weights_shape(cfg: CF.Layer, T: int):
+    """[T, H, m], or [T, H, m, h] with multi-core scoring."""
+    return (T, cfg.heads, cfg.topm) + ((cfg.cores,) if cfg.cores > 1 else ())
 
 
 def workspace(desc, T) -> torch.Tensor:
@@ -27,7 +32,7 @@ def score_topk(dl, T, batch=0, with_axis=True):
     cfg = dl.cfg
     desc = desc_for(cfg)
     idx = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda")
-    w = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.float32, device="cuda")
+    w = torch.empty(weights_shape(cfg, T), dtype=torch.float32, device="cuda")
     ax = torch.empty((2, T, cfg.heads, cfg.topk), dtype=torch.int32, device="cuda") if with_axis else None
     ws = workspace(desc, T)
     U.check(U.umem_score_topk(desc, T, dl.q_row[batch, :T], dl.q_col[batch, :T], dl.k_row, dl.k_col,
@@ -39,7 +44,7 @@ def gather(dl, idx, w, T):
     cfg = dl.cfg
     out = torch.empty((T, cfg.expand, cfg.dv), dtype=torch.float32, device="cuda")
     U.check(U.umem_gather_sum(cfg.n_values, cfg.dv, cfg.vdtype, dl.values, T, cfg.bag, idx, w,
-                              dl.perm, cfg.expand, out), "umem_gather_sum")
+                              dl.perm, cfg.expand, cfg.cores, out), "umem_gather_sum")
     return out
 
 
@@ -49,7 +54,7 @@ def forward(dl, T, batch=0):
     width = cfg.d_out if cfg.d_out else (cfg.dv_virt if cfg.dv_virt else cfg.dv)
     out = torch.empty((T, width), dtype=torch.float32, device="cuda")
     idx = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda")
-    w = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.float32, device="cuda")
+    w = torch.empty(weights_shape(cfg, T), dtype=torch.float32, device="cuda")
     ws = workspace(desc, T)
     U.check(U.umem_forward(desc, T, dl.q_row[batch, :T], dl.q_col[batch, :T], dl.k_row, dl.k_col,
                            dl.core, dl.values, dl.perm, dl.w_proj, dl.w_out, out, idx, w, ws,

@@ -40,10 +40,17 @@ def _check_sorted(scores, ids, gap, what):
 
 def check_selection(cfg, q_row, q_col, K_row, K_col, core, gpu_idx, gpu_w, gpu_axis=None,
                     gap=GAP, w_rtol=1e-5):
-    """Stages A-C for tokens whose queries are q_row/q_col [T, H, Dk].  gpu_idx, gpu_w:
-    [T, H, m]; gpu_axis: [2, T, H, k] or None.  Returns (oracle result, report)."""
-    ref = O.score_topk(q_row, q_col, K_row, K_col, cfg.topk, cfg.topm, cfg.grid, cfg.weight, core,
-                       cfg.rank)
+    """Stages A-C for tokens whose queries are q_row/q_col [T, H, Dk].  gpu_idx: [T, H, m];
+    gpu_w: [T, H, m], or [T, H, m, h] with multi-core scoring (core then holds the component
+    cores [H, h, r, r]); gpu_axis: [2, T, H, k] or None.  Returns (oracle result, report)."""
+    parts = None
+    if cfg.cores > 1:
+        parts, core = np.asarray(core, np.float64), np.asarray(core, np.float64).sum(axis=1)
+        ref = O.score_topk(q_row, q_col, K_row, K_col, cfg.topk, cfg.topm, cfg.grid, cfg.weight,
+                           None, cfg.rank, core_parts=parts)
+    else:
+        ref = O.score_topk(q_row, q_col, K_row, K_col, cfg.topk, cfg.topm, cfg.grid, cfg.weight,
+                           core, cfg.rank)
     T, H, m = gpu_idx.shape
     n, k = cfg.n_keys, cfg.topk
     rep = dict(tokens=T, axis_exempt=0, grid_exempt=0, e2e_slot_mismatch=0, max_w_err=0.0)
@@ -77,7 +84,11 @@ def check_selection(cfg, q_row, q_col, K_row, K_col, core, gpu_idx, gpu_w, gpu_a
                 assert abs(gx - theta_m) < gap, ("stage B", t, h, x, gx, theta_m)
                 rep["grid_exempt"] += 1
             _check_sorted(g_gpu, gi, gap, f"grid order t={t} h={h}")
-            if cfg.weight == O.W_RAW:
+            if parts is not None:
+                # eq. (16): each core's exact score of the GPU's slots
+                w_ref = O.core_scores(ref["S_row"][t, h], ref["S_col"][t, h], gi, n, parts[h])
+                scale = max(np.abs(w_ref).max(), 1e-30)
+            elif cfg.weight == O.W_RAW:
                 w_ref = g_gpu
                 scale = max(np.abs(g_gpu).max(), 1e-30)
             else:
@@ -95,7 +106,8 @@ def check_pooled(cfg, value_rows, gpu_idx, gpu_w, gpu_pooled, perm=None, rtol=1e
     Error per token: max |diff| / max |reference|."""
     T = gpu_idx.shape[0]
     idx = np.asarray(gpu_idx).reshape(T, -1)
-    w = np.asarray(gpu_w, np.float64).reshape(T, -1)
+    w = np.asarray(gpu_w, np.float64)
+    w = w.reshape(T, idx.shape[1], -1) if cfg.cores > 1 else w.reshape(T, -1)
     ref = O.gather_sum(value_rows, idx, w, perm, cfg.n_values, cfg.expand)
     got = np.asarray(gpu_pooled, np.float64).reshape(ref.shape)
     worst = 0.0

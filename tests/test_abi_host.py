@@ -35,7 +35,7 @@ def test_only_abi_symbols_exported():
 def desc(**kw):
     d = U.umem_desc()
     base = dict(heads=2, dk=128, n_keys=4480, rank=1, topk=32, topm=32, grid=0, weight=0,
-                n_values=4480 * 4480, dv=512, vdtype=1, expand=1, dv_virt=0, d_out=0, reserved=0)
+                n_values=4480 * 4480, dv=512, vdtype=1, expand=1, dv_virt=0, d_out=0, cores=0)
     base.update(kw)
     for k, v in base.items():
         setattr(d, k, v)
@@ -73,7 +73,15 @@ def test_workspace_size_layout():
     (dict(expand=4, n_values=4480 * 1120), U.UMEM_ERR_INVALID_ARG),              # no D'v
     (dict(n_values=1000), U.UMEM_ERR_INVALID_ARG),             # N_p * E != n^2
     (dict(vdtype=2), U.UMEM_ERR_INVALID_ARG),
-    (dict(reserved=1), U.UMEM_ERR_INVALID_ARG),
+    (dict(cores=-1), U.UMEM_ERR_INVALID_ARG),
+    (dict(cores=2), U.UMEM_ERR_INVALID_ARG),                               # MCS needs the Tucker grid
+    (dict(cores=2, grid=1, rank=2, weight=1), U.UMEM_ERR_INVALID_ARG),     # ... and raw weights
+    (dict(cores=3, grid=1, rank=2), U.UMEM_ERR_INVALID_ARG),               # dv % h != 0
+    (dict(cores=16, grid=1, rank=2), U.UMEM_ERR_UNSUPPORTED),              # h <= 8
+    (dict(cores=8, grid=1, rank=2, dv=32), U.UMEM_ERR_UNSUPPORTED),        # 8-byte slices
+    (dict(cores=8, grid=1, rank=2, dv=64), U.UMEM_OK),                     # 16-byte slices
+    (dict(cores=2, grid=1, rank=2), U.UMEM_OK),
+    (dict(cores=1), U.UMEM_OK),
     (dict(n_keys=20000, n_values=20000 * 20000), U.UMEM_ERR_UNSUPPORTED),
     (dict(topk=111, topm=8), U.UMEM_ERR_UNSUPPORTED),
     (dict(topm=300, topk=32), U.UMEM_ERR_UNSUPPORTED),
@@ -83,7 +91,7 @@ def test_workspace_size_layout():
 ])
 def test_descriptor_validation(kw, want):
     st, n = U.umem_workspace_size(desc(**kw), 8)
-    assert st == want and n == 0
+    assert st == want and (n == 0) == (st != U.UMEM_OK)
 
 
 def test_entry_points_reject_before_launch():
@@ -105,11 +113,16 @@ def test_entry_points_reject_before_launch():
     assert U.umem_select(desc(heads=3), 8, fake, None, None, None, None, None, fake, fake, None, fake, fake, 0) == U.UMEM_ERR_UNSUPPORTED
     assert U.umem_select(desc(topm=65, topk=16), 8, fake, None, None, None, None, None, fake, fake, None, fake, fake, 0) == U.UMEM_ERR_UNSUPPORTED
     # gather: bad sizes, misaligned values, bag beyond the limit, unsupported row
-    assert U.umem_gather_sum(100, 512, 1, fake, 4, 0, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
-    assert U.umem_gather_sum(100, 512, 1, fake + 8, 4, 64, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
-    assert U.umem_gather_sum(100, 512, 1, fake, 4, 4096, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_UNSUPPORTED
-    assert U.umem_gather_sum(100, 100, 1, fake, 4, 64, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_UNSUPPORTED
-    assert U.umem_gather_sum(100, 512, 3, fake, 4, 64, fake, fake, None, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_gather_sum(100, 512, 1, fake, 4, 0, fake, fake, None, 1, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_gather_sum(100, 512, 1, fake + 8, 4, 64, fake, fake, None, 1, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_gather_sum(100, 512, 1, fake, 4, 4096, fake, fake, None, 1, 1, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_gather_sum(100, 100, 1, fake, 4, 64, fake, fake, None, 1, 1, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_gather_sum(100, 512, 3, fake, 4, 64, fake, fake, None, 1, 1, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    # multi-core weights: dv % h, 16-byte slices, h <= 8
+    assert U.umem_gather_sum(100, 512, 1, fake, 4, 64, fake, fake, None, 1, 3, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_gather_sum(100, 8, 1, fake, 4, 64, fake, fake, None, 1, 2, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_gather_sum(100, 512, 1, fake, 4, 64, fake, fake, None, 1, 16, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_gather_sum(100, 512, 1, fake, 4, 64, fake, fake, None, 1, -1, fake, 0) == U.UMEM_ERR_INVALID_ARG
     # projection: missing weights / workspace
     assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, fake, fake, fake, 64, 0) == U.UMEM_ERR_WORKSPACE
@@ -126,7 +139,7 @@ def test_zero_tokens_is_a_noop():
     d = desc()
     assert U.umem_score_topk(d, 0, None, None, None, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
     assert U.umem_forward(d, 0, None, None, None, None, None, None, None, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
-    assert U.umem_gather_sum(100, 512, 1, None, 0, 64, None, None, None, 1, None, 0) == U.UMEM_OK
+    assert U.umem_gather_sum(100, 512, 1, None, 0, 64, None, None, None, 1, 1, None, 0) == U.UMEM_OK
 
 
 def test_one_hip_runtime_in_process():

@@ -190,6 +190,29 @@ def test_axis_scores_kernels(kw):
         assert err.max() <= 1e-5, (a, err.max())
 
 
+# ---------------------------------------------------------------- multi-core scoring
+
+@pytest.mark.parametrize("kw", [
+    # pooled inside the selection (two heads, 1 KiB rows)
+    dict(T=40, heads=2, dk=128, n_keys=150, rank=2, grid=CF.GRID_TUCKER, topk=16, topm=24,
+         dv=512, vdtype=CF.BF16, cores=2),
+    # the gather kernel (three heads), four cores, fp32 rows
+    dict(T=20, heads=3, dk=64, n_keys=90, rank=2, grid=CF.GRID_TUCKER, topk=10, topm=30, dv=256,
+         vdtype=CF.F32, cores=4),
+    # with IVE and the projection: the physical rows are split
+    dict(T=24, heads=2, dk=128, n_keys=128, rank=2, grid=CF.GRID_TUCKER, topk=16, topm=32,
+         dv=512, vdtype=CF.BF16, expand=4, dv_virt=256, d_out=192, cores=2),
+], ids=["pooled-in-select", "gather-4-cores", "ive-projection"])
+def test_multi_core_scoring(kw):
+    run_and_check(small("mcs", **kw))
+
+
+def test_c5_tucker_ive_mcs_sampled():
+    """The rank-2 Tucker + IVE layer with the paper's default two component cores."""
+    cfg = dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M")
+    run_and_check(cfg, tokens=np.array([0, 1, 2, 1023, 2048, 4095]))
+
+
 # ---------------------------------------------------------------- a7 inside the selection
 
 @pytest.mark.parametrize("kw", [
@@ -231,32 +254,36 @@ def test_select_pools_like_gather(kw):
 
 # ---------------------------------------------------------------- gather and projection alone
 
-@pytest.mark.parametrize("dv,vdtype,expand,bag,T", [
-    (512, CF.BF16, 1, 64, 37), (1024, CF.BF16, 1, 77, 37), (256, CF.F32, 1, 5, 37),
-    (512, CF.BF16, 4, 256, 37), (128, CF.BF16, 9, 40, 37), (3072, CF.BF16, 1, 33, 37),
-    (8, CF.BF16, 4, 130, 37),
+@pytest.mark.parametrize("dv,vdtype,expand,bag,T,cores", [
+    (512, CF.BF16, 1, 64, 37, 1), (1024, CF.BF16, 1, 77, 37, 1), (256, CF.F32, 1, 5, 37, 1),
+    (512, CF.BF16, 4, 256, 37, 1), (128, CF.BF16, 9, 40, 37, 1), (3072, CF.BF16, 1, 33, 37, 1),
+    (8, CF.BF16, 4, 130, 37, 1),
     # thousands of tokens: a wave per token (ragged last workgroup, sub-rows, long rows)
-    (512, CF.BF16, 1, 64, 4099), (64, CF.BF16, 1, 33, 4100), (2048, CF.BF16, 1, 20, 4096),
-    (256, CF.F32, 1, 7, 5001)])
-def test_gather_standalone(dv, vdtype, expand, bag, T):
-    rng = np.random.default_rng(dv + bag + T)
+    (512, CF.BF16, 1, 64, 4099, 1), (64, CF.BF16, 1, 33, 4100, 1), (2048, CF.BF16, 1, 20, 4096, 1),
+    (256, CF.F32, 1, 7, 5001, 1),
+    # multi-core weights (eq. (17)): column slices, with IVE, sub-rows, many tokens
+    (512, CF.BF16, 1, 64, 37, 2), (1024, CF.BF16, 4, 100, 37, 4), (64, CF.BF16, 1, 33, 70, 4),
+    (256, CF.F32, 1, 33, 4099, 2), (3072, CF.BF16, 1, 20, 9, 8)])
+def test_gather_standalone(dv, vdtype, expand, bag, T, cores):
+    rng = np.random.default_rng(dv + bag + T + cores)
     Np = 5000
     vdt = torch.float32 if vdtype == CF.F32 else torch.bfloat16
     values = torch.empty((Np, dv), dtype=vdt, device="cuda")
     SD.fill_normal_(values, 21, S.TID_VALUES, 1 / np.sqrt(dv))
     idx = rng.integers(0, Np * expand, size=(T, bag)).astype(np.int32)
     idx[:, 1] = idx[:, 0]
-    w = rng.standard_normal((T, bag)).astype(np.float32)
+    w = rng.standard_normal((T, bag) + ((cores,) if cores > 1 else ())).astype(np.float32)
     perm = rng.permutation(Np * expand).astype(np.int32) if expand > 1 else None
     out = torch.empty((T, expand, dv), dtype=torch.float32, device="cuda")
     U.check(U.umem_gather_sum(Np, dv, vdtype, values, T, bag, torch.from_numpy(idx).cuda(),
                               torch.from_numpy(w).cuda(),
-                              None if perm is None else torch.from_numpy(perm).cuda(), expand, out))
+                              None if perm is None else torch.from_numpy(perm).cuda(), expand,
+                              cores, out))
     torch.cuda.synchronize()
     vals = values.float().cpu().numpy().astype(np.float64)
     ref = O.gather_sum(lambda r: vals[r], idx, w, perm, Np, expand)
     err = np.abs(out.cpu().numpy() - ref).max() / np.abs(ref).max()
-    log(f"[report] gather T={T} dv={dv} E={expand} bag={bag}: err={err:.2e}")
+    log(f"[report] gather T={T} dv={dv} E={expand} bag={bag} cores={cores}: err={err:.2e}")
     assert err <= 1e-5
 
 
