@@ -8,8 +8,9 @@ enough (over 1 GiB of distinct value rows) that the gathered rows are not cache-
 
 Prints one JSON line.  Besides the headline it carries the roofline of the dominant kernel
 (the average duration of its launches replayed back to back from a HIP graph, between two HIP
-events on the launch stream), the value-gather bandwidth, a decode batch sweep, and the CPU
-oracle's throughput on a bounded sample.  The timed steps are replayed from a captured HIP graph
+events on the launch stream), the value-gather bandwidth, a decode batch sweep, the forwards of the 1M-slot prefill layer and of
+the 4M-slot Tucker + IVE layer (with one and with two component cores), each with the roofline
+of every kernel it launches, and the CPU oracle's throughput on a bounded sample.  The timed steps are replayed from a captured HIP graph
 (--eager launches them one by one from Python instead).
 """
 from __future__ import annotations
@@ -27,6 +28,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
 FP32_PEAK_TFLOPS = 157.3       # MI355X dense fp32 matrix
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix
 METRIC = "memory-layer tokens/sec + value-gather HBM GB/s (% of peak), 20M-slot decode"
 KERNEL_SOURCES = {
     "axis_scores_kernel": "score.hip",
@@ -42,6 +44,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--batches", type=int, default=512, help="distinct query batches rotated")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the prefill and Tucker + IVE (one and two cores) forwards")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -70,8 +74,13 @@ def kernel_work(cfg, T, fused=False):
     return {
         "axis_scores_kernel": dict(bytes=keys + q + sel, flops=2 * 2 * T * H * n * dk),
         "select_kernel": dict(bytes=sel + sel_out + (rows + T * cfg.dv * 4 if fused else 0), flops=0),
-        "gather_kernel": dict(bytes=rows + T * cfg.bag * 8 + T * cfg.expand * cfg.dv * 4,
+        "gather_kernel": dict(bytes=rows + T * cfg.bag * 4 * (1 + cfg.cores) + T * cfg.expand * cfg.dv * 4,
                               flops=2 * T * cfg.bag * cfg.dv, row_bytes=rows),
+        # the IVE projection and the output linear: two bf16 GEMMs with fp32 accumulation
+        "project_kernels": dict(bytes=T * cfg.expand * cfg.dv * 4 + cfg.expand * cfg.dv * cfg.dv_virt * 2
+                                + cfg.dv_virt * cfg.d_out * 2 + T * max(cfg.d_out, cfg.dv_virt) * 4,
+                                flops=2 * T * cfg.expand * cfg.dv * cfg.dv_virt
+                                + 2 * T * cfg.dv_virt * cfg.d_out),
     }
 
 
@@ -112,9 +121,14 @@ class Runner:
         st, nbytes = U.umem_workspace_size(self.desc, T)
         U.check(st)
         self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
-        self.out = torch.empty((T, cfg.dv), dtype=torch.float32, device="cuda")
+        self.project = bool(cfg.dv_virt)
+        # the forward's output: the projected rows, else the pooled rows [T, E, Dv]
+        width = (cfg.d_out or cfg.dv_virt) if self.project else cfg.expand * cfg.dv
+        self.out = torch.empty((T, width), dtype=torch.float32, device="cuda")
+        self.pooled = torch.empty((T, cfg.expand, cfg.dv), dtype=torch.float32, device="cuda")
         self.idx = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda")
-        self.w = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.float32, device="cuda")
+        wshape = (T, cfg.heads, cfg.topm) + ((cfg.cores,) if cfg.cores > 1 else ())
+        self.w = torch.empty(wshape, dtype=torch.float32, device="cuda")
         self.sel = torch.empty((2, T, cfg.heads, cfg.n_keys), dtype=torch.float32, device="cuda")
         self.R = batches
         # umem_forward pools inside the selection kernel for such layers (see umem_select)
@@ -157,9 +171,16 @@ class Runner:
     def gather(self, idx, w):
         U, dl, c = self.U, self.dl, self.cfg
         st = U.umem_gather_sum(c.n_values, c.dv, c.vdtype, dl.values, c.T, c.bag, idx, w, dl.perm,
-                               c.expand, c.cores, self.out)
+                               c.expand, c.cores, self.pooled)
         if st:
             U.check(st, "umem_gather_sum")
+
+    def project_rows(self):
+        U, dl, c = self.U, self.dl, self.cfg
+        st = U.umem_project(c.T, c.expand, c.dv, c.dv_virt, c.d_out, self.pooled, dl.w_proj,
+                            dl.w_out, self.out, self.ws, self.ws.numel())
+        if st:
+            U.check(st, "umem_project")
 
     def _graph_time(self, launches):
         """Average seconds per call of ``launches`` (a list of thunks) replayed from a HIP graph,
@@ -204,7 +225,17 @@ class Runner:
         torch.cuda.synchronize()
         return time.perf_counter() - t0, steps
 
-    def time_kernels(self, launches_per_kernel):
+    def _unique_rows(self, idxs):
+        """Distinct physical value rows one step gathers (averaged over the query batches)."""
+        c, dl = self.cfg, self.dl
+        tot = 0
+        for b in range(self.R):
+            flat = idxs[b].reshape(-1).long()
+            rows = flat if dl.perm is None else dl.perm[flat].long() % c.n_values
+            tot += int(self.torch.unique(rows).numel())
+        return tot / self.R
+
+    def time_kernels(self, launches_per_kernel, queue=True):
         """Average duration (us) of each kernel of the forward, launched back to back from a HIP
         graph with distinct inputs per launch: the scoring over rotating query batches, the
         selection over precomputed score sets, the gather over precomputed selections."""
@@ -227,7 +258,10 @@ class Runner:
             "gather_kernel": self._graph_time([lambda b=b: self.gather(idxs[b % self.R], ws_[b % self.R])
                                                for b in range(n)]),
         }
-        self.queue = self._time_gather_queue(idxs, ws_)
+        if self.project:
+            out["project_kernels"] = self._graph_time([self.project_rows] * n)
+        self.queue = self._time_gather_queue(idxs, ws_) if queue else None
+        self.unique_rows = self._unique_rows(idxs)
         del sels, idxs, ws_
         return {k: v * 1e6 for k, v in out.items()}
 
@@ -240,7 +274,8 @@ class Runner:
         if half < 2:
             return None
         Tq = half * c.T
-        stacks = [(idxs[i * half:(i + 1) * half].reshape(Tq, c.bag), ws_[i * half:(i + 1) * half].reshape(Tq, c.bag))
+        stacks = [(idxs[i * half:(i + 1) * half].reshape(Tq, c.bag),
+                   ws_[i * half:(i + 1) * half].reshape((Tq, c.bag) + tuple(ws_.shape[4:])))
                   for i in (0, 1)]
         outq = torch.empty((Tq, c.expand, c.dv), dtype=torch.float32, device="cuda")
 
@@ -265,6 +300,11 @@ class Runner:
 
 def roofline_for(cfg, T, name, avg_us, workload, fused):
     work = kernel_work(cfg, T, fused)[name]
+    if name == "project_kernels":
+        achieved = work["flops"] / (avg_us * 1e-6) / 1e12
+        return dict(kernel=name, bound="mfma", achieved=round(achieved, 3), peak=BF16_PEAK_TFLOPS,
+                    unit="TFLOP/s", frac=round(achieved / BF16_PEAK_TFLOPS, 4), traffic=None,
+                    avg_us=round(avg_us, 3))
     if name == "axis_scores_kernel" and work["flops"] / work["bytes"] > FP32_PEAK_TFLOPS * 1e3 / HBM_PEAK_GBS:
         achieved = work["flops"] / (avg_us * 1e-6) / 1e12
         return dict(kernel=name, bound="mfma", achieved=round(achieved, 3), peak=FP32_PEAK_TFLOPS,
@@ -275,6 +315,36 @@ def roofline_for(cfg, T, name, avg_us, workload, fused):
                 unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4),
                 traffic=measured_traffic(name, workload), avg_us=round(avg_us, 3),
                 algorithmic_bytes=work["bytes"])
+
+
+def workload_report(cfg, steps=50, warmup=5):
+    """The whole forward of another layer shape (graph-replayed, distinct query batches) and the
+    roofline of each of its kernels.  The gather is priced on the logical rows of its bag (eq.
+    (1)) and, separately, on the distinct rows of a step, which is what HBM must deliver."""
+    R = max(2, distinct_batches(cfg.T, cfg.bag * cfg.dv * cfg.vbytes))
+    r = Runner(cfg, R)
+    secs, n = r.time_forward(steps, warmup)
+    st = r.time_kernels(min(steps, 64), queue=False)
+    kernels = ["axis_scores_kernel", "select_kernel"] + ([] if r.fused else ["gather_kernel"])
+    if r.project:
+        kernels.append("project_kernels")
+    g = kernel_work(cfg, cfg.T)["gather_kernel"]
+    uniq = r.unique_rows * cfg.dv * cfg.vbytes
+    rep = dict(workload=cfg.name, tokens=cfg.T, heads=cfg.heads, n_keys=cfg.n_keys,
+               slots=cfg.n_slots, rank=cfg.rank, grid="tucker" if cfg.grid else "additive",
+               expand=cfg.expand, cores=cfg.cores, topk=cfg.topk, topm=cfg.topm, dv=cfg.dv,
+               query_batches=R, ms_per_step=round(secs / n * 1e3, 4),
+               tokens_per_s=round(cfg.T * n / secs, 1),
+               kernel_us={k: round(v, 3) for k, v in st.items()}, forward_kernels=kernels,
+               rooflines={k: roofline_for(cfg, cfg.T, k, st[k], cfg.name, r.fused) for k in kernels},
+               gather_unique_row_bytes=int(uniq),
+               gather_unique_GBps=round(uniq / (st["gather_kernel"] * 1e-6) / 1e9, 1),
+               gather_logical_GBps=round(g["row_bytes"] / (st["gather_kernel"] * 1e-6) / 1e9, 1))
+    log(f"workload {cfg.name}: {rep}")
+    del r
+    import torch
+    torch.cuda.empty_cache()
+    return rep
 
 
 def distinct_batches(T, row_bytes_per_token):
@@ -380,6 +450,11 @@ def main():
     sw = None if args.no_sweep else sweep(cfg, values)
     del values
     torch.cuda.empty_cache()
+    wl = None
+    if not args.no_workloads:
+        import dataclasses
+        wl = [workload_report(c) for c in
+              (CF.C2, CF.C5, dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M"))]
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, args.cpu_seconds)
     line = {
         "metric": METRIC, "value": round(cfg.T * n / secs, 1), "unit": "tokens/s", "n_gpus": 1,
@@ -396,6 +471,7 @@ def main():
         "gather": gather,
         "gather_queue": queue,
         "batch_sweep": sw,
+        "workloads": wl,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -175,22 +175,23 @@ __device__ __forceinline__ uint32_t wave_kth_largest16(const uint32_t (&v)[G], i
 }
 
 // A valid threshold for a top-k from V maxima per lane (maxima of disjoint sets) in LDS:
-// lane-wise they are merged into G = ceil(k / 64) maxima of unions (still disjoint sets), and
-// L, the k-th largest of those 64 G values with its low 16 bits cleared, has at least k
-// elements >= L.  One wave.
+// lane-wise they are merged into G = ceil(k / 32) (at most V) maxima of unions (still disjoint
+// sets), and L, the k-th largest of those 64 G values with its low 16 bits cleared, has at
+// least k elements >= L.  With at least two groups per wanted element L stays close to the
+// k-th largest element (with one, it falls to the best of the worst group).  One wave.
 template <int V>
 __device__ __forceinline__ uint32_t threshold_from_maxima(const uint32_t* vals, int k) {
   const int lane = threadIdx.x & (kWave - 1);
   uint32_t v[V];
 #pragma unroll
   for (int q = 0; q < V; ++q) v[q] = vals[lane + kWave * q];
-  if (k <= kWave) {
+  if (k <= kWave / 2) {
     uint32_t r[1] = {0u};
 #pragma unroll
     for (int q = 0; q < V; ++q) r[0] = max(r[0], v[q]);
     return wave_kth_largest16<1>(r, k);
   }
-  if (V >= 4 && k <= 2 * kWave) {
+  if (V >= 4 && k <= kWave) {
     uint32_t r[2] = {0u, 0u};
 #pragma unroll
     for (int q = 0; q < V; ++q) r[q & 1] = max(r[q & 1], v[q]);
@@ -263,7 +264,9 @@ __device__ __forceinline__ void additive_tables(int k, int m, SelectShared& sh) 
   if (lane == 0) sh.grid_total = carry;
 }
 
-template <int NV, int VEC>
+// MODE only gives each kernel variant its own copy (with a single caller, the inliner treats it
+// as it would in a single-variant build).
+template <int NV, int VEC, int MODE>
 __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, int h, int n, int k,
                             int m, bool tables, uint64_t* comp_all, SelectShared& sh) {
   constexpr int NE = NV * VEC;
@@ -505,17 +508,23 @@ __device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool s
 
 // ---------------------------------------------------------------- the kernel
 
-template <int NV, int VEC>
+// Kernel variants: kModePool pools the value rows when given them and takes the grid from its
+// argument; its row loads in flight take many registers.  kModeAdd and kModeTucker never pool
+// and are specialised to one grid: fewer registers, more workgroups per CU for many tokens.
+constexpr int kModePool = 0, kModeAdd = 1, kModeTucker = 2;
+
+template <int NV, int VEC, int MODE>
 __global__ __launch_bounds__(THREADS) void select_kernel(
     const float* __restrict__ sel, const float* __restrict__ q_row,
     const float* __restrict__ q_col, const float* __restrict__ k_row,
     const float* __restrict__ k_col, const float* __restrict__ core_all,
     int32_t* __restrict__ idx_out, float* __restrict__ w_out, int32_t* __restrict__ axis_out,
     const void* __restrict__ values, int vbf16, int dv, float* __restrict__ pooled,
-    int T, int H, int n, int dk, int rank, int k, int m, int tucker, int softmax, int n_cand,
+    int T, int H, int n, int dk, int rank, int k, int m, int grid_tucker, int softmax, int n_cand,
     int cores) {
   extern __shared__ __align__(16) unsigned char dyn[];
   __shared__ SelectShared sh;
+  const int tucker = MODE == kModePool ? grid_tucker : MODE == kModeTucker;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
@@ -535,7 +544,7 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
   }
   if (tid < 2) sh.ax_cnt[tid] = 0;
   if (tid == 0) sh.grid_cnt = 0;
-  select_axes<NV, VEC>(sel, T, H, t, h, n, k, m, !tucker, reinterpret_cast<uint64_t*>(dyn), sh);
+  select_axes<NV, VEC, MODE>(sel, T, H, t, h, n, k, m, !tucker, reinterpret_cast<uint64_t*>(dyn), sh);
   if (axis_out != nullptr)
     for (int a = tid; a < 2 * k; a += THREADS)
       axis_out[((static_cast<size_t>(a / k) * T + t) * H + h) * k + a % k] = sh.ax_idx[a / k][a % k];
@@ -631,12 +640,14 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     }
     sh.mx[tid] = mx;
     __syncthreads();
-    if (wave == 0) {
-      const uint32_t L = threshold_from_maxima<8>(sh.mx, m);
-      if (lane == 0) sh.thr[0] = L;
-    }
-    __syncthreads();
-    const uint32_t L = sh.thr[0];
+    // The threshold from all 512 thread maxima, unmerged: each covers 8 candidates of one column
+    // (rows 8 apart), and the m-th largest of them lies close to the m-th largest candidate.
+    // Merged lane-wise they would be column maxima, whose m-th largest (m = k) is the best score
+    // of the worst column, below most of the grid.  Every wave takes it itself.
+    uint32_t mxs[CPT];
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) mxs[q] = sh.mx[lane + kWave * q];
+    const uint32_t L = wave_kth_largest16<CPT>(mxs, m);
     int cnt = 0;
 #pragma unroll
     for (int j = 0; j < CPT; ++j) cnt += (tid + THREADS * j < kk) & (k32[j] >= L);
@@ -746,7 +757,9 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     __syncthreads();
   }
   // ---- a7 fused: pool this head's rows into the token's output (the axes' LDS is free now)
-  if (pooled != nullptr) {
+  // (a run-time test also in the pooling variant: the decode kernel measured faster with it than
+  // with the branch resolved at compile time)
+  if (MODE == kModePool && pooled != nullptr) {
     float* red = reinterpret_cast<float*>(dyn);
     float* out_t = pooled + static_cast<size_t>(t) * dv;
     if (vbf16) pool_rows<true>(values, dv, m, softmax, cores, sh, red, out_t);
@@ -787,11 +800,17 @@ hipError_t launch_select(const umem_desc& d, int T, const float* sel, const floa
   if (tucker && n_cand > KK_MAX) return hipErrorInvalidValue;
   const size_t lds = select_lds_bytes(n_cand, tucker, pooled ? d.dv : 0);
   const dim3 grid(static_cast<unsigned>(T) * d.heads), block(THREADS);
-#define UMEM_SELECT(NV, VEC)                                                                      \
-  hipLaunchKernelGGL((select_kernel<NV, VEC>), grid, block, lds, s, sel, q_row, q_col, k_row,    \
-                     k_col, core, idx, w, axis_idx, values, d.vdtype == UMEM_BF16, d.dv, pooled,  \
-                     T, d.heads, d.n_keys, d.dk, d.rank, d.topk,                                 \
+#define UMEM_SELECT_P(NV, VEC, MODE)                                                              \
+  hipLaunchKernelGGL((select_kernel<NV, VEC, MODE>), grid, block, lds, s, sel, q_row, q_col,     \
+                     k_row, k_col, core, idx, w, axis_idx, values, d.vdtype == UMEM_BF16, d.dv,   \
+                     pooled, T, d.heads, d.n_keys, d.dk, d.rank, d.topk,                         \
                      d.topm, tucker, d.weight == UMEM_W_SOFTMAX, n_cand, n_cores(d))
+#define UMEM_SELECT(NV, VEC)                                                                      \
+  do {                                                                                            \
+    if (pooled != nullptr) UMEM_SELECT_P(NV, VEC, kModePool);                                     \
+    else if (tucker) UMEM_SELECT_P(NV, VEC, kModeTucker);                                         \
+    else UMEM_SELECT_P(NV, VEC, kModeAdd);                                                        \
+  } while (0)
   const int n = d.n_keys;
   if (n % 4 == 0) {
     const int nv = (n + 1023) / 1024;
@@ -815,6 +834,7 @@ hipError_t launch_select(const umem_desc& d, int T, const float* sel, const floa
     else return hipErrorInvalidValue;
   }
 #undef UMEM_SELECT
+#undef UMEM_SELECT_P
   return hipGetLastError();
 }
 
