@@ -64,7 +64,8 @@ enum { UMEM_W_RAW = 0, UMEM_W_SOFTMAX = 1 };      /* Trick 1 (raw scores) / eq. 
  *   topk <= 90 (64 for the Tucker grid); topm <= 256; rank <= 4; (dk / rank) % 4 == 0; dk <= 1024; heads <= 64;
  *   heads * topm <= 2048; expand <= 64; a value row (dv * element size) of 16 * 2^j <= 1024
  *   bytes or a multiple of 1024 up to 8192 bytes; T <= 2^20; cores <= 8, each core's column
- *   slice (dv / h elements) a multiple of 16 bytes. */
+ *   slice (dv / h elements) a multiple of 16 bytes; dv_virt and d_out multiples of 8 (weight
+ *   rows of 16-byte pieces). */
 typedef struct umem_desc {
   int32_t heads;    /* H: key sets (each with its own keys and core) sharing one value table */
   int32_t dk;       /* query/key dimension per axis per head */
@@ -158,14 +159,17 @@ UMEM_API umem_status umem_gather_sum(int64_t n_values, int32_t dv, int32_t vdtyp
  * fp32 pooled sums and the intermediate are rounded to bf16, nearest even), fp32 accumulation.
  *   pooled  fp32 [T, E, dv]; w_proj bf16 bits [E, dv, dv_virt]; w_out bf16 bits [dv_virt, d_out]
  *           or NULL; out fp32 [T, d_out] (or [T, dv_virt] without w_out)
- *   ws      scratch for the intermediate: T * dv_virt * 4 bytes (may be NULL without w_out) */
+ *   ws      scratch for the intermediate: T * dv_virt * 4 bytes (may be NULL without w_out)
+ * UMEM_ERR_UNSUPPORTED unless pooled, w_proj and w_out are 16-byte aligned, expand * dv is a
+ * multiple of 4 and dv_virt, d_out are multiples of 8. */
 UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
                          const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
                          float* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* a1 .. a8: the whole forward of the layer for T tokens.
  *   values, perm     as for umem_gather_sum (perm required iff expand > 1)
- *   w_proj, w_out    as for umem_project (w_proj required iff dv_virt > 0; w_out iff d_out > 0)
+ *   w_proj, w_out    as for umem_project (w_proj required iff dv_virt > 0; w_out iff d_out > 0;
+ *                    16-byte aligned, else UMEM_ERR_UNSUPPORTED)
  *   out              fp32: [T, dv] without projection, else [T, d_out] (or [T, dv_virt])
  *   idx_out, w_out_scores  optional (NULL) copies of the selection, [T, H, m] each
  *                    (w_out_scores [T, H, m, h] with multi-core scoring)

@@ -2,97 +2,135 @@
 //
 // y = sum_p pooled[:, p, :] W_p (eq. (15)) is one GEMM of [T, E*Dv] by [E*Dv, D'v] because
 // pooled [T, E, Dv] and W_proj [E, Dv, D'v] are both contiguous; the output linear of Trick 6 is
-// a second GEMM of y by W_out [D'v, d_out].  A (fp32) is rounded to bf16 (nearest even) as it is
-// staged into LDS; B is bf16.  Tiles: 64 x 64 per workgroup, four waves of 32 x 32, K in steps
-// of 32, v_mfma_f32_16x16x16_bf16.
+// a second GEMM of y by W_out [D'v, d_out].
+//
+// Tiles of 128 x 64 per workgroup, four waves of 64 x 32 (4 x 2 v_mfma_f32_16x16x16_bf16
+// tiles), K in steps of 32.  A (fp32) is read with 16-byte loads and rounded to bf16 (nearest
+// even) as it is staged into LDS; B (bf16, rows of N) with 16-byte loads, transposed into LDS
+// so that each lane's four k of one column are contiguous.  The next K-slice is fetched into
+// registers while the current one is multiplied.  Workgroups are dealt round-robin to the
+// eight XCDs, so tile t is given to workgroup (t mod per) * 8 + t / per: each XCD takes a
+// contiguous band of M-blocks across all N-tiles and finds A's rows and B in its own L2.
 #include "umem_internal.h"
 
 namespace umem {
 namespace {
 
-constexpr int BM = 64, BN = 64, BK = 32;
+constexpr int BM = 128, BN = 64, BK = 32;
 constexpr int THREADS = 256;
-constexpr int APAD = 4;   // bf16 elements of padding per LDS row
+constexpr int LDA = BK + 8;   // LDS pitch of A's rows in bf16 (80 B: fragment reads conflict-free)
+constexpr int LDB = BK + 4;   // LDS pitch of B's columns in bf16 (72 B)
+constexpr int kXcds = 8;
 
 typedef short bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// One K-slice of the operands in registers: four 16-byte pieces of A (thread t, piece i: row
+// (t + 256 i) / 8, k (t % 8) * 4) and one of B (row k t / 8, columns (t % 8) * 8 ...).
+struct Slice {
+  f32x4 a[4];
+  u32x4 b;
+};
+
+__device__ __forceinline__ void fetch(const float* __restrict__ A, const uint16_t* __restrict__ B,
+                                      int M, int N, int K, int m0, int n0, int k0, int tid,
+                                      Slice& sl) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int f = tid + THREADS * i;
+    const int gm = m0 + (f >> 3), gk = k0 + (f & 7) * 4;
+    sl.a[i] = (gm < M && gk < K) ? *reinterpret_cast<const f32x4*>(A + static_cast<size_t>(gm) * K + gk)
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int gk = k0 + (tid >> 3), gn = n0 + (tid & 7) * 8;
+  sl.b = (gk < K && gn < N) ? *reinterpret_cast<const u32x4*>(B + static_cast<size_t>(gk) * N + gn)
+                            : u32x4{0u, 0u, 0u, 0u};
+}
+
+__device__ __forceinline__ void stage(const Slice& sl, uint16_t* As, uint16_t* Bs, int tid) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int f = tid + THREADS * i;
+    u32x2 v;
+    v.x = static_cast<uint32_t>(f32_to_bf16(sl.a[i].x)) | (static_cast<uint32_t>(f32_to_bf16(sl.a[i].y)) << 16);
+    v.y = static_cast<uint32_t>(f32_to_bf16(sl.a[i].z)) | (static_cast<uint32_t>(f32_to_bf16(sl.a[i].w)) << 16);
+    *reinterpret_cast<u32x2*>(As + (f >> 3) * LDA + (f & 7) * 4) = v;
+  }
+  const int kk = tid >> 3, nc = (tid & 7) * 8;
+  const uint32_t w[4] = {sl.b.x, sl.b.y, sl.b.z, sl.b.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    Bs[(nc + 2 * e) * LDB + kk] = static_cast<uint16_t>(w[e] & 0xFFFFu);
+    Bs[(nc + 2 * e + 1) * LDB + kk] = static_cast<uint16_t>(w[e] >> 16);
+  }
+}
 
 __global__ __launch_bounds__(THREADS) void gemm_bf16_kernel(const float* __restrict__ A,
                                                             const uint16_t* __restrict__ B,
                                                             float* __restrict__ C, int M, int N,
-                                                            int K) {
-  __shared__ uint16_t As[BM][BK + APAD];   // [m][k]
-  __shared__ uint16_t Bs[BN][BK + APAD];   // [n][k]
+                                                            int K, int n_tiles_n, int per_xcd,
+                                                            int n_tiles) {
+  __shared__ __align__(16) uint16_t As[BM * LDA];   // [m][k]
+  __shared__ __align__(16) uint16_t Bs[BN * LDB];   // [n][k]
+  const int tile = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (tile >= n_tiles) return;                     // the whole workgroup: no barrier is skipped
+  const int m0 = (tile / n_tiles_n) * BM, n0 = (tile % n_tiles_n) * BN;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int wm = wave >> 1, wn = wave & 1;         // this wave's 64 x 32 block of the tile
 
-  f32x4 acc[2][2];
+  f32x4 acc[4][2];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  Slice sl;
+  fetch(A, B, M, N, K, m0, n0, 0, tid, sl);
   for (int k0 = 0; k0 < K; k0 += BK) {
-    // A tile: 64 x 32 fp32 -> bf16; each thread 8 consecutive k of one row
-    {
-      const int r = tid >> 2, c = (tid & 3) * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int gm = m0 + r, gk = k0 + c + e;
-        const float x = (gm < M && gk < K) ? A[static_cast<size_t>(gm) * K + gk] : 0.0f;
-        As[r][c + e] = f32_to_bf16(x);
-      }
-    }
-    // B tile: 32 x 64 bf16, stored transposed; each thread 8 consecutive n of one k
-    {
-      const int kk = tid >> 3, c = (tid & 7) * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int gk = k0 + kk, gn = n0 + c + e;
-        Bs[c + e][kk] = (gk < K && gn < N) ? B[static_cast<size_t>(gk) * N + gn] : uint16_t(0);
-      }
-    }
+    stage(sl, As, Bs, tid);
     __syncthreads();
+    if (k0 + BK < K) fetch(A, B, M, N, K, m0, n0, k0 + BK, tid, sl);
 #pragma unroll
     for (int ks = 0; ks < BK; ks += 16) {
-      bf16x4 af[2], bfr[2];
+      // lane: row (or column) lane % 16 of a 16-block, k = ks + 4 (lane / 16) ... + 3
+      bf16x4 af[4], bfr[2];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) {
-        const uint16_t* p = &As[wm * 32 + a * 16 + (lane & 15)][ks + 4 * (lane >> 4)];
-        af[a] = *reinterpret_cast<const bf16x4*>(p);
-      }
+      for (int a = 0; a < 4; ++a)
+        af[a] = *reinterpret_cast<const bf16x4*>(As + (wm * 64 + a * 16 + (lane & 15)) * LDA + ks + 4 * (lane >> 4));
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const uint16_t* p = &Bs[wn * 32 + b * 16 + (lane & 15)][ks + 4 * (lane >> 4)];
-        bfr[b] = *reinterpret_cast<const bf16x4*>(p);
-      }
+      for (int b = 0; b < 2; ++b)
+        bfr[b] = *reinterpret_cast<const bf16x4*>(Bs + (wn * 32 + b * 16 + (lane & 15)) * LDB + ks + 4 * (lane >> 4));
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < 2; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(af[a], bfr[b], acc[a][b], 0, 0, 0);
     }
     __syncthreads();
   }
-  // D layout: lane holds rows 4*(lane/16) + r of column lane%16
+  // D layout: lane holds rows 4 (lane / 16) + r of column lane % 16
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int gm = m0 + wm * 32 + a * 16 + 4 * (lane >> 4) + r;
+        const int gm = m0 + wm * 64 + a * 16 + 4 * (lane >> 4) + r;
         const int gn = n0 + wn * 32 + b * 16 + (lane & 15);
         if (gm < M && gn < N) C[static_cast<size_t>(gm) * N + gn] = acc[a][b][r];
       }
 }
 
 hipError_t gemm(const float* A, const uint16_t* B, float* C, int M, int N, int K, hipStream_t s) {
-  dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
-  hipLaunchKernelGGL(gemm_bf16_kernel, grid, dim3(THREADS), 0, s, A, B, C, M, N, K);
+  const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
+  const int tiles = tm * tn;
+  const int per = (tiles + kXcds - 1) / kXcds;
+  hipLaunchKernelGGL(gemm_bf16_kernel, dim3(per * kXcds), dim3(THREADS), 0, s, A, B, C, M, N, K,
+                     tn, per, tiles);
   return hipGetLastError();
 }
 

@@ -53,6 +53,7 @@ umem_status check_desc(const umem_desc* d) {
   if (d->heads > kMaxHeads || d->heads * d->topm > kMaxBag) return UMEM_ERR_UNSUPPORTED;
   if (d->expand > kMaxExpand) return UMEM_ERR_UNSUPPORTED;
   if (!gather_row_supported(d->dv, d->vdtype)) return UMEM_ERR_UNSUPPORTED;
+  if (d->dv_virt % 8 != 0 || d->d_out % 8 != 0) return UMEM_ERR_UNSUPPORTED;   // 16-byte weight rows
   return UMEM_OK;
 }
 
@@ -145,6 +146,10 @@ umem_status check_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt
       if (need > 0 && (ws == nullptr || !aligned(ws, 16) || ws_bytes < need)) return UMEM_ERR_WORKSPACE;
     }
   }
+  // the GEMMs read 16-byte pieces: 4 fp32 of a pooled row, 8 bf16 of a weight row
+  if (!aligned(pooled, 16) || !aligned(w_proj, 16) || !aligned(w_out, 16)) return UMEM_ERR_UNSUPPORTED;
+  if ((static_cast<int64_t>(expand) * dv) % 4 != 0 || dv_virt % 8 != 0 || d_out % 8 != 0)
+    return UMEM_ERR_UNSUPPORTED;
   return UMEM_OK;
 }
 
@@ -281,6 +286,7 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
     return UMEM_ERR_INVALID_ARG;
   if (!aligned(idx_out, 4) || !aligned(w_out_scores, 4) || !aligned(perm, 4))
     return UMEM_ERR_INVALID_ARG;
+  if (!aligned(w_proj, 16) || !aligned(w_out, 16)) return UMEM_ERR_UNSUPPORTED;
   const int bag = desc->heads * desc->topm;
   const Layout L = layout(desc, T);
   char* base = static_cast<char*>(ws);

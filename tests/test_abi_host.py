@@ -87,6 +87,8 @@ def test_workspace_size_layout():
     (dict(topm=300, topk=32), U.UMEM_ERR_UNSUPPORTED),
     (dict(grid=1, rank=8), U.UMEM_ERR_UNSUPPORTED),
     (dict(dv=100), U.UMEM_ERR_UNSUPPORTED),                    # 200-byte rows
+    (dict(d_out=100), U.UMEM_ERR_UNSUPPORTED),                 # weight rows of 16-byte pieces
+    (dict(expand=4, n_values=4480 * 1120, dv_virt=260), U.UMEM_ERR_UNSUPPORTED),
     (dict(heads=64, topm=64), U.UMEM_ERR_UNSUPPORTED),         # bag 4096
 ])
 def test_descriptor_validation(kw, want):
@@ -126,6 +128,12 @@ def test_entry_points_reject_before_launch():
     # projection: missing weights / workspace
     assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, fake, fake, fake, 64, 0) == U.UMEM_ERR_WORKSPACE
+    # the GEMMs read 16-byte pieces of pooled rows and weight rows
+    assert U.umem_project(8, 4, 512, 516, 2048, fake, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_project(8, 4, 512, 512, 2044, fake, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_project(8, 1, 6, 0, 64, fake, None, fake, fake, None, 0, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_project(8, 4, 512, 512, 2048, fake, fake + 8, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_project(8, 4, 512, 512, 2048, fake + 4, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
     # forward: perm required iff expand > 1, projection weights iff D'v / d_out
     ive = desc(heads=4, n_keys=2048, rank=2, grid=1, topk=64, topm=64, n_values=1 << 20, expand=4,
                dv_virt=512, d_out=2048)
