@@ -236,7 +236,9 @@ __global__ __launch_bounds__(THREADS) void axis_scores_mfma(
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int t = t0 + mt * 16 + 4 * g + r;
-      if (t < T && key < n) sel[((static_cast<size_t>(axis) * T + t) * H + h) * n + key] = out[mt][r];
+      // nontemporal: the scores stream through once, the keys should stay in L2
+      if (t < T && key < n)
+        __builtin_nontemporal_store(out[mt][r], sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n + key);
     }
   }
 }

@@ -47,6 +47,13 @@ constexpr int KK_MAX = 4096;        // Tucker: k*k candidates
 constexpr int ADD_MAX = 2048;       // additive candidates (a+1)(b+1) <= m, a, b < k
 constexpr int CPT = KK_MAX / THREADS;   // Tucker candidates per thread
 
+// Kernel variants: kModePool pools the value rows when given them and takes the grid from its
+// argument; its row loads in flight take many registers.  kModeAdd and kModeTucker never pool
+// and are specialised to one grid: fewer registers, more workgroups per CU for many tokens.
+constexpr int kModePool = 0, kModeAdd = 1, kModeTucker = 2;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 struct SelectShared {
   uint32_t mx[THREADS];               // thread maxima (both axes, or the grid)
   int wave_tot[NWAVES];
@@ -279,14 +286,18 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
   uint32_t key[NE];
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
+    // the many-token variants read the scores nontemporally (they stream through once; the keys
+    // the Tucker grid reads back should stay in L2)
     if (VEC == 4) {
-      const float4 v = *reinterpret_cast<const float4*>(src + min(1024 * j + 4 * g, n - 4));
+      const f32x4* p = reinterpret_cast<const f32x4*>(src + min(1024 * j + 4 * g, n - 4));
+      const f32x4 v = MODE == kModePool ? *p : __builtin_nontemporal_load(p);
       key[4 * j + 0] = order_key(v.x);
       key[4 * j + 1] = order_key(v.y);
       key[4 * j + 2] = order_key(v.z);
       key[4 * j + 3] = order_key(v.w);
     } else {
-      key[j] = order_key(src[min(GROUP * j + g, n - 1)]);
+      const float* p = src + min(GROUP * j + g, n - 1);
+      key[j] = order_key(MODE == kModePool ? *p : __builtin_nontemporal_load(p));
     }
   }
   if (tables && tid < kWave) additive_tables(k, m, sh);
@@ -508,11 +519,6 @@ __device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool s
 
 // ---------------------------------------------------------------- the kernel
 
-// Kernel variants: kModePool pools the value rows when given them and takes the grid from its
-// argument; its row loads in flight take many registers.  kModeAdd and kModeTucker never pool
-// and are specialised to one grid: fewer registers, more workgroups per CU for many tokens.
-constexpr int kModePool = 0, kModeAdd = 1, kModeTucker = 2;
-
 template <int NV, int VEC, int MODE>
 __global__ __launch_bounds__(THREADS) void select_kernel(
     const float* __restrict__ sel, const float* __restrict__ q_row,
@@ -589,26 +595,49 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     __syncthreads();
     S = sh.grid_cnt;
   } else {
-    // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32
-    const int width = dk / rank;
-    for (int job = tid; job < 2 * rank * k; job += THREADS) {
-      const int axis = job / (rank * k);
-      const int rho = (job / k) % rank;
-      const int a = job % k;
-      const float* K = axis ? k_col : k_row;
-      const float* q = axis ? q_col : q_row;
-      const float* kr = K + (static_cast<size_t>(h) * n + sh.ax_idx[axis][a]) * dk + rho * width;
-      const float* qr = q + (static_cast<size_t>(t) * H + h) * dk + rho * width;
-      float s = 0.0f;
-      for (int d = 0; d < width; d += 4) {
-        const float4 kv = *reinterpret_cast<const float4*>(kr + d);
-        const float4 qv = *reinterpret_cast<const float4*>(qr + d);
-        s = fmaf(kv.x, qv.x, s);
-        s = fmaf(kv.y, qv.y, s);
-        s = fmaf(kv.z, qv.z, s);
-        s = fmaf(kv.w, qv.w, s);
+    // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32.  Four
+    // lanes (a quad) per (axis, key) row, each a quarter of its dk elements in 16-byte pieces
+    // (four in flight at a time); the quad's partial sums are added with DPP.
+    {
+      const int width = dk / rank;
+      const int n4 = dk >> 2;                           // 16-byte pieces per row
+      for (int job = tid; job < 8 * k; job += THREADS) {   // whole quads: 8k is a multiple of 4
+        const int part = job & 3, row = job >> 2;
+        const int axis = row >= k, a = row - (axis ? k : 0);
+        const float4* kr = reinterpret_cast<const float4*>(
+            (axis ? k_col : k_row) + (static_cast<size_t>(h) * n + sh.ax_idx[axis][a]) * dk);
+        const float4* qr = reinterpret_cast<const float4*>(
+            (axis ? q_col : q_row) + (static_cast<size_t>(t) * H + h) * dk);
+        const int f1 = ((part + 1) * n4) >> 2;
+        float acc[kMaxRank] = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int f0 = (part * n4) >> 2; f0 < f1; f0 += 4) {
+          float4 kv[4], qv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (f0 + i < f1) {
+              kv[i] = kr[f0 + i];
+              qv[i] = qr[f0 + i];
+            }
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (f0 + i < f1) {
+              float d = kv[i].x * qv[i].x;
+              d = fmaf(kv[i].y, qv[i].y, d);
+              d = fmaf(kv[i].z, qv[i].z, d);
+              d = fmaf(kv[i].w, qv[i].w, d);
+              const int rho = (4 * (f0 + i)) / width;   // a piece never straddles two slices
+#pragma unroll
+              for (int r = 0; r < kMaxRank; ++r) acc[r] += rho == r ? d : 0.0f;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < kMaxRank; ++r) {
+          acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0xB1, 0xF, 0xF, false));
+          acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0x4E, 0xF, 0xF, false));
+        }
+        if (part == 0)
+          for (int r = 0; r < rank; ++r) sh.s_ex[axis][r][a] = acc[r];
       }
-      sh.s_ex[axis][rho][a] = s;
     }
     __syncthreads();
     for (int job = tid; job < rank * k; job += THREADS) {
@@ -619,48 +648,60 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       sh.p_col[rho][b] = p;
     }
     __syncthreads();
-    // candidate c = tid + 512 j (j < CPT) of the k*k grid, held in registers
-    const int kk = k * k;
+    // Candidates in registers: thread tid < R k takes column b = tid mod k and rows a0 + R j
+    // (a0 = tid / k, R = 512 / k, j < CPT; R >= 8 as k <= 64, so CPT = 8 rows cover a column).
+    const int R = THREADS / k;
+    const int b = tid % k, a0 = tid / k;
+    const bool on = tid < R * k;
+    double pc[kMaxRank];
+#pragma unroll
+    for (int r = 0; r < kMaxRank; ++r) pc[r] = (on && r < rank) ? sh.p_col[r][b] : 0.0;
     uint64_t k64[CPT];
     uint32_t k32[CPT];
+    uint32_t valid = 0u;                              // bit j: row a0 + R j exists
     uint32_t mx = 0u;
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
-      const int c = tid + THREADS * j;
+      const int a = a0 + R * j;
       k64[j] = 0ull;
       k32[j] = 0u;
-      if (c < kk) {
-        const int a = c / k, b = c - (c / k) * k;
+      if (on && a < k) {
         double gv = 0.0;
-        for (int rho = 0; rho < rank; ++rho) gv += static_cast<double>(sh.s_ex[0][rho][a]) * sh.p_col[rho][b];
+        for (int rho = 0; rho < rank; ++rho) gv += static_cast<double>(sh.s_ex[0][rho][a]) * pc[rho];
         k64[j] = order_key64(gv);
         k32[j] = order_key(static_cast<float>(gv));
         mx = max(mx, k32[j]);
+        valid |= 1u << j;
       }
     }
     sh.mx[tid] = mx;
     __syncthreads();
-    // The threshold from all 512 thread maxima, unmerged: each covers 8 candidates of one column
-    // (rows 8 apart), and the m-th largest of them lies close to the m-th largest candidate.
-    // Merged lane-wise they would be column maxima, whose m-th largest (m = k) is the best score
-    // of the worst column, below most of the grid.  Every wave takes it itself.
-    uint32_t mxs[CPT];
+    // The threshold from all 512 thread maxima, unmerged (each covers up to 8 candidates of one
+    // column): their m-th largest lies close to the m-th largest candidate.  Merged lane-wise
+    // they would be column maxima, whose m-th largest (m = k) is the best score of the worst
+    // column, below most of the grid.  One wave takes it, the others wait at the barrier.
+    if (wave == 0) {
+      uint32_t mxs[CPT];
 #pragma unroll
-    for (int q = 0; q < CPT; ++q) mxs[q] = sh.mx[lane + kWave * q];
-    const uint32_t L = wave_kth_largest16<CPT>(mxs, m);
+      for (int q = 0; q < CPT; ++q) mxs[q] = sh.mx[lane + kWave * q];
+      const uint32_t L0 = wave_kth_largest16<CPT>(mxs, m);
+      if (lane == 0) sh.thr[0] = L0;
+    }
+    __syncthreads();
+    const uint32_t L = sh.thr[0];
     int cnt = 0;
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) cnt += (tid + THREADS * j < kk) & (k32[j] >= L);
+    for (int j = 0; j < CPT; ++j) cnt += ((valid >> j) & 1u) & (k32[j] >= L);
     const int2 o = group_offsets(cnt, 0, NWAVES, sh);
     if (o.y <= SMAX_S) {
       int pos = o.x;
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
-        const int c = tid + THREADS * j;
-        if ((c < kk) & (k32[j] >= L)) {
+        const int a = a0 + R * j;
+        if (((valid >> j) & 1u) && k32[j] >= L) {
           cand[pos].key = k64[j];
-          cand[pos].id = sh.ax_idx[0][c / k] * n + sh.ax_idx[1][c % k];
-          cand[pos].pad = ((c / k) << 8) | (c % k);
+          cand[pos].id = sh.ax_idx[0][a] * n + sh.ax_idx[1][b];
+          cand[pos].pad = (a << 8) | b;
           ++pos;
         }
       }
@@ -671,48 +712,47 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       // the candidates equal to it.
       int32_t fl[CPT];
 #pragma unroll
-      for (int j = 0; j < CPT; ++j) {
-        const int c = tid + THREADS * j;
-        fl[j] = c < kk ? sh.ax_idx[0][c / k] * n + sh.ax_idx[1][c % k] : 0x7FFFFFFF;
-      }
+      for (int j = 0; j < CPT; ++j)
+        fl[j] = ((valid >> j) & 1u) ? sh.ax_idx[0][a0 + R * j] * n + sh.ax_idx[1][b] : 0x7FFFFFFF;
       uint64_t prefix = 0ull;
-      for (int b = 63; b >= 0; --b) {
-        const uint64_t cb = prefix | (1ull << b);
+      for (int bit = 63; bit >= 0; --bit) {
+        const uint64_t cb = prefix | (1ull << bit);
         int cl = 0;
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) cl += (tid + THREADS * j < kk) & (k64[j] >= cb);
+        for (int j = 0; j < CPT; ++j) cl += ((valid >> j) & 1u) & (k64[j] >= cb);
         if (group_offsets(cl, 0, NWAVES, sh).y >= m) prefix = cb;
       }
       const uint64_t theta = prefix;
       int gl = 0;
 #pragma unroll
-      for (int j = 0; j < CPT; ++j) gl += (tid + THREADS * j < kk) & (k64[j] > theta);
+      for (int j = 0; j < CPT; ++j) gl += ((valid >> j) & 1u) & (k64[j] > theta);
       const int need = m - group_offsets(gl, 0, NWAVES, sh).y;
       uint32_t ylim = 0u;     // the need-th smallest flat index among the keys equal to theta
-      for (int b = 31; b >= 0; --b) {
-        const uint32_t cb = ylim | (1u << b);
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cb = ylim | (1u << bit);
         int cl = 0;
 #pragma unroll
         for (int j = 0; j < CPT; ++j)
-          cl += (tid + THREADS * j < kk) & (k64[j] == theta) & (static_cast<uint32_t>(fl[j]) < cb);
+          cl += ((valid >> j) & 1u) & (k64[j] == theta) & (static_cast<uint32_t>(fl[j]) < cb);
         if (group_offsets(cl, 0, NWAVES, sh).y < need) ylim = cb;
       }
       int tk = 0;
+      uint32_t take = 0u;
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
-        const bool ok = tid + THREADS * j < kk;
-        tk += ok & ((k64[j] > theta) | ((k64[j] == theta) & (static_cast<uint32_t>(fl[j]) <= ylim)));
+        const bool ok = ((valid >> j) & 1u) &&
+                        ((k64[j] > theta) | ((k64[j] == theta) & (static_cast<uint32_t>(fl[j]) <= ylim)));
+        take |= static_cast<uint32_t>(ok) << j;
+        tk += ok;
       }
       const int2 ot = group_offsets(tk, 0, NWAVES, sh);
       int pos = ot.x;
 #pragma unroll
       for (int j = 0; j < CPT; ++j) {
-        const bool ok = tid + THREADS * j < kk;
-        if (ok & ((k64[j] > theta) | ((k64[j] == theta) & (static_cast<uint32_t>(fl[j]) <= ylim)))) {
-          const int c = tid + THREADS * j;
+        if ((take >> j) & 1u) {
           cand[pos].key = k64[j];
           cand[pos].id = fl[j];
-          cand[pos].pad = ((c / k) << 8) | (c % k);
+          cand[pos].pad = ((a0 + R * j) << 8) | b;
           ++pos;
         }
       }
