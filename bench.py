@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the prefill and Tucker + IVE (one and two cores) forwards")
+    ap.add_argument("--only-workload", default=None,
+                    help="time only this layer's forward (prefill-1M, tucker-ive-4M, "
+                         "tucker-ive-mcs-4M) and print its report as the JSON line")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -347,6 +350,12 @@ def workload_report(cfg, steps=50, warmup=5):
     return rep
 
 
+def extra_workloads(CF):
+    """The layer shapes reported beside the decode headline."""
+    import dataclasses
+    return (CF.C2, CF.C5, dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M"))
+
+
 def distinct_batches(T, row_bytes_per_token):
     """Enough query batches that one rotation touches over 1 GiB of value rows (capped)."""
     return int(min(4096, max(1, math.ceil((1 << 30) / (T * row_bytes_per_token)))))
@@ -424,6 +433,14 @@ def main():
         torch.cuda.synchronize()
         log("copy calibration: 3 x 256 MiB device copies done")
         del a, b
+    if args.only_workload:
+        layers = {c.name: c for c in extra_workloads(CF)}
+        if args.only_workload not in layers:
+            print(f"unknown workload {args.only_workload}; one of {sorted(layers)}", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps(workload_report(layers[args.only_workload], args.steps, args.warmup)),
+              flush=True)
+        return
     r = Runner(cfg, args.batches)
     secs, n = r.time_forward(args.steps, args.warmup, graph=not args.eager)
     ms = secs / n * 1e3
@@ -450,11 +467,7 @@ def main():
     sw = None if args.no_sweep else sweep(cfg, values)
     del values
     torch.cuda.empty_cache()
-    wl = None
-    if not args.no_workloads:
-        import dataclasses
-        wl = [workload_report(c) for c in
-              (CF.C2, CF.C5, dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M"))]
+    wl = None if args.no_workloads else [workload_report(c) for c in extra_workloads(CF)]
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, args.cpu_seconds)
     line = {
         "metric": METRIC, "value": round(cfg.T * n / secs, 1), "unit": "tokens/s", "n_gpus": 1,
