@@ -8,9 +8,10 @@ enough (over 1 GiB of distinct value rows) that the gathered rows are not cache-
 
 Prints one JSON line.  Besides the headline it carries the roofline of the dominant kernel
 (the average duration of its launches replayed back to back from a HIP graph, between two HIP
-events on the launch stream), the value-gather bandwidth, a decode batch sweep, the forwards of the 1M-slot prefill layer and of
-the 4M-slot Tucker + IVE layer (with one and with two component cores), each with the roofline
-of every kernel it launches, and the CPU oracle's throughput on a bounded sample.  The timed steps are replayed from a captured HIP graph
+events on the launch stream), the value-gather bandwidth, a decode batch sweep, the forwards of the 1M-slot prefill layer, of the
+4M-slot Tucker + IVE layer (with one and with two component cores) and of one memory layer of the
+paper's UltraMem-1.6B-x12 model, each with the roofline of every kernel it launches, and the CPU
+oracle's throughput on a bounded sample.  The timed steps are replayed from a captured HIP graph
 (--eager launches them one by one from Python instead).
 """
 from __future__ import annotations
@@ -48,7 +49,8 @@ def parse():
                     help="skip the prefill and Tucker + IVE (one and two cores) forwards")
     ap.add_argument("--only-workload", default=None,
                     help="time only this layer's forward (prefill-1M, tucker-ive-4M, "
-                         "tucker-ive-mcs-4M) and print its report as the JSON line")
+                         "tucker-ive-mcs-4M, ultramem-1.6B-x12) and print its report as the "
+                         "JSON line")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -353,7 +355,7 @@ def workload_report(cfg, steps=50, warmup=5):
 def extra_workloads(CF):
     """The layer shapes reported beside the decode headline."""
     import dataclasses
-    return (CF.C2, CF.C5, dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M"))
+    return (CF.C2, CF.C5, dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M"), CF.C6)
 
 
 def distinct_batches(T, row_bytes_per_token):

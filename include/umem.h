@@ -155,11 +155,19 @@ UMEM_API umem_status umem_gather_sum(int64_t n_values, int32_t dv, int32_t vdtyp
                             const int32_t* perm, int32_t expand, int32_t cores, float* out,
                             hipStream_t stream);
 
+/* Scratch bytes umem_project needs for these sizes (the intermediate of the output linear and
+ * the partial sums of split reductions over long K); dv_virt == 0 sizes the output linear alone.
+ * Same shape requirements as umem_project. */
+UMEM_API umem_status umem_project_workspace_size(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt,
+                                        int32_t d_out, size_t* bytes);
+
 /* a8: y = sum_p pooled[:, p, :] W_p (eq. (15)), then y W_out (Trick 6).  bf16 operands (the
  * fp32 pooled sums and the intermediate are rounded to bf16, nearest even), fp32 accumulation.
  *   pooled  fp32 [T, E, dv]; w_proj bf16 bits [E, dv, dv_virt]; w_out bf16 bits [dv_virt, d_out]
- *           or NULL; out fp32 [T, d_out] (or [T, dv_virt] without w_out)
- *   ws      scratch for the intermediate: T * dv_virt * 4 bytes (may be NULL without w_out)
+ *           or NULL; out fp32 [T, d_out] (or [T, dv_virt] without w_out).  With w_proj NULL
+ *           (dv_virt 0, expand 1) the output linear alone: out = pooled [T, dv] by w_out [dv, d_out]
+ *   ws      16-byte aligned scratch of umem_project_workspace_size(...) bytes (NULL if 0)
+ * The result does not depend on timing (split reductions add their partials in a fixed order).
  * UMEM_ERR_UNSUPPORTED unless pooled, w_proj and w_out are 16-byte aligned, expand * dv is a
  * multiple of 4 and dv_virt, d_out are multiples of 8. */
 UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,

@@ -31,7 +31,8 @@ UMEM_GRID_ADD, UMEM_GRID_TUCKER = 0, 1
 UMEM_W_RAW, UMEM_W_SOFTMAX = 0, 1
 
 EXPORTED = ("umem_workspace_size", "umem_axis_scores", "umem_select", "umem_score_topk",
-            "umem_gather_sum", "umem_project", "umem_forward", "umem_status_string")
+            "umem_gather_sum", "umem_project_workspace_size", "umem_project", "umem_forward",
+            "umem_status_string")
 
 
 class umem_desc(ctypes.Structure):
@@ -62,6 +63,7 @@ def _load() -> ctypes.CDLL:
         "umem_select": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P],
         "umem_score_topk": [D, I32, P, P, P, P, P, P, P, P, P, SZ, P],
         "umem_gather_sum": [I64, I32, I32, P, I32, I32, P, P, P, I32, I32, P, P],
+        "umem_project_workspace_size": [I32, I32, I32, I32, I32, ctypes.POINTER(SZ)],
         "umem_project": [I32, I32, I32, I32, I32, P, P, P, P, P, SZ, P],
         "umem_forward": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
     }
@@ -141,6 +143,13 @@ def umem_gather_sum(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, 
                     stream=None) -> int:
     return _lib.umem_gather_sum(n_values, dv, vdtype, _p(values), T, bag, _p(idx), _p(w), _p(perm),
                                 expand, cores, _p(out), _s(stream))
+
+
+def umem_project_workspace_size(T, expand, dv, dv_virt, d_out):
+    """Returns (status, bytes)."""
+    out = ctypes.c_size_t(0)
+    st = _lib.umem_project_workspace_size(T, expand, dv, dv_virt, d_out, ctypes.byref(out))
+    return st, out.value
 
 
 def umem_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws, ws_bytes,

@@ -427,7 +427,8 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
 #undef UMEM_WIDE
     return hipGetLastError();
   }
-  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && width % 16 == 0) {
+  // the key widths of the paper's UltraMem models (Kdim 256, 384, 448) and smaller powers of two
+  if ((d.dk == 64 || d.dk == 128 || d.dk == 256 || d.dk == 384 || d.dk == 448) && width % 16 == 0) {
     int mt = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
     while (mt > 1 && static_cast<size_t>(16 * mt) * (d.dk + 4) * 4 > 65536) mt /= 2;
     const size_t lds = static_cast<size_t>(16 * mt) * (d.dk + 4) * 4;
@@ -438,7 +439,9 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
 #define UMEM_SCORE_DK(MT)                  \
   if (d.dk == 64) UMEM_SCORE(MT, 4);       \
   else if (d.dk == 128) UMEM_SCORE(MT, 8); \
-  else UMEM_SCORE(MT, 16)
+  else if (d.dk == 256) UMEM_SCORE(MT, 16); \
+  else if (d.dk == 384) UMEM_SCORE(MT, 24); \
+  else UMEM_SCORE(MT, 28)
     if (mt == 1) { UMEM_SCORE_DK(1); }
     else if (mt == 2) { UMEM_SCORE_DK(2); }
     else { UMEM_SCORE_DK(4); }

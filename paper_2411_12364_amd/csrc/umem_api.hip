@@ -73,10 +73,11 @@ umem_status check_scoring_ptrs(const umem_desc* d, const float* q_row, const flo
 }
 
 struct Layout {
-  size_t factors, sel, idx, w, pooled, tmp, total;
+  size_t factors, sel, idx, w, pooled, proj, total;
 };
 
-// Workspace: [rank-1 factors (Tucker)] [selection scores] [idx] [w] [pooled] [intermediate]
+// Workspace: [rank-1 factors (Tucker)] [selection scores] [idx] [w] [pooled] [projection
+// scratch: the intermediate and split-K partials]
 Layout layout(const umem_desc* d, int32_t T) {
   Layout L{};
   const size_t th = static_cast<size_t>(T) * d->heads;
@@ -92,8 +93,9 @@ Layout layout(const umem_desc* d, int32_t T) {
   L.pooled = off;
   if (d->dv_virt > 0 || d->d_out > 0)
     off += round_up(static_cast<size_t>(T) * d->expand * d->dv * sizeof(float));
-  L.tmp = off;
-  if (d->dv_virt > 0 && d->d_out > 0) off += round_up(static_cast<size_t>(T) * d->dv_virt * sizeof(float));
+  L.proj = off;
+  if (d->dv_virt > 0 || d->d_out > 0)
+    off += round_up(project_workspace_bytes(T, d->expand, d->dv, d->dv_virt, d->d_out));
   L.total = off;
   return L;
 }
@@ -127,39 +129,36 @@ umem_status check_gather(int64_t n_values, int32_t dv, int32_t vdtype, const voi
   return UMEM_OK;
 }
 
-umem_status check_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
-                          const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
-                          const float* out, const void* ws, size_t ws_bytes) {
+// The shape of a projection: w_proj given iff dv_virt > 0 (else the output linear alone, which
+// needs expand == 1 and d_out > 0); w_out given iff d_out > 0.
+umem_status check_project_shape(int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
+                                bool has_proj, bool has_out) {
   if (expand < 1 || dv < 1 || dv_virt < 0 || d_out < 0) return UMEM_ERR_INVALID_ARG;
-  umem_status st = check_tokens(T);
-  if (st != UMEM_OK || T == 0) return st;
-  if (expand < 1 || dv < 1 || dv_virt < 0 || d_out < 0) return UMEM_ERR_INVALID_ARG;
-  if (!pooled || !out) return UMEM_ERR_INVALID_ARG;
-  if (w_proj == nullptr) {
-    // output linear only: [T, dv] by [dv, d_out]
-    if (expand != 1 || dv_virt != 0 || d_out == 0 || w_out == nullptr) return UMEM_ERR_INVALID_ARG;
-  } else {
-    if (dv_virt == 0) return UMEM_ERR_INVALID_ARG;
-    if ((w_out == nullptr) != (d_out == 0)) return UMEM_ERR_INVALID_ARG;
-    if (w_out != nullptr) {
-      const size_t need = static_cast<size_t>(T) * dv_virt * sizeof(float);
-      if (need > 0 && (ws == nullptr || !aligned(ws, 16) || ws_bytes < need)) return UMEM_ERR_WORKSPACE;
-    }
-  }
+  if (has_proj != (dv_virt > 0) || has_out != (d_out > 0)) return UMEM_ERR_INVALID_ARG;
+  if (!has_proj && (expand != 1 || d_out == 0)) return UMEM_ERR_INVALID_ARG;
   // the GEMMs read 16-byte pieces: 4 fp32 of a pooled row, 8 bf16 of a weight row
-  if (!aligned(pooled, 16) || !aligned(w_proj, 16) || !aligned(w_out, 16)) return UMEM_ERR_UNSUPPORTED;
   if ((static_cast<int64_t>(expand) * dv) % 4 != 0 || dv_virt % 8 != 0 || d_out % 8 != 0)
     return UMEM_ERR_UNSUPPORTED;
   return UMEM_OK;
 }
 
+umem_status check_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
+                          const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
+                          const float* out, const void* ws, size_t ws_bytes) {
+  umem_status st = check_project_shape(expand, dv, dv_virt, d_out, w_proj != nullptr, w_out != nullptr);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  if (!pooled || !out) return UMEM_ERR_INVALID_ARG;
+  const size_t need = project_workspace_bytes(T, expand, dv, dv_virt, d_out);
+  if (need > 0 && (ws == nullptr || !aligned(ws, 16) || ws_bytes < need)) return UMEM_ERR_WORKSPACE;
+  if (!aligned(pooled, 16) || !aligned(w_proj, 16) || !aligned(w_out, 16)) return UMEM_ERR_UNSUPPORTED;
+  return UMEM_OK;
+}
+
 hipError_t run_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
                        const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
-                       float* out, void* tmp, hipStream_t s) {
-  if (w_proj == nullptr)   // the output linear alone is the same GEMM with [dv, d_out] weights
-    return launch_project(T, 1, dv, d_out, 0, pooled, w_out, nullptr, out, nullptr, s);
-  return launch_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out,
-                        static_cast<float*>(tmp), s);
+                       float* out, void* ws, hipStream_t s) {
+  return launch_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws, s);
 }
 
 }  // namespace
@@ -258,6 +257,18 @@ UMEM_API umem_status umem_gather_sum(int64_t n_values, int32_t dv, int32_t vdtyp
                                   cores > 1 ? cores : 1, out, stream));
 }
 
+UMEM_API umem_status umem_project_workspace_size(int32_t T, int32_t expand, int32_t dv,
+                                                 int32_t dv_virt, int32_t d_out, size_t* bytes) {
+  if (bytes == nullptr) return UMEM_ERR_INVALID_ARG;
+  *bytes = 0;
+  // the output linear alone has dv_virt == 0; with dv_virt > 0 the projector is given
+  umem_status st = check_project_shape(expand, dv, dv_virt, d_out, dv_virt > 0, d_out > 0);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK) return st;
+  *bytes = project_workspace_bytes(T, expand, dv, dv_virt, d_out);
+  return UMEM_OK;
+}
+
 UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt,
                                   int32_t d_out, const float* pooled, const uint16_t* w_proj,
                                   const uint16_t* w_out, float* out, void* ws, size_t ws_bytes,
@@ -316,7 +327,7 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
                       desc->expand, n_cores(*desc), pooled, stream);
   if (e == hipSuccess && project)
     e = run_project(T, desc->expand, desc->dv, desc->dv_virt, desc->d_out, pooled, w_proj, w_out,
-                    out, base + L.tmp, stream);
+                    out, base + L.proj, stream);
   return hip_status(e);
 }
 

@@ -67,8 +67,11 @@ hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* value
 inline int n_cores(const umem_desc& d) { return d.cores > 1 ? d.cores : 1; }
 bool cores_supported(int dv, int vdtype, int cores);
 
+// a8.  ws: project_workspace_bytes(...) bytes, 256-byte aligned (the intermediate and the
+// split-K partials); w_proj == nullptr is the output linear alone ([T, dv] by [dv, d_out]).
+size_t project_workspace_bytes(int T, int expand, int dv, int dv_virt, int d_out);
 hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const float* pooled,
-                          const uint16_t* w_proj, const uint16_t* w_out, float* out, float* tmp,
+                          const uint16_t* w_proj, const uint16_t* w_out, float* out, void* ws,
                           hipStream_t s);
 
 // ---------------------------------------------------------------- device helpers

@@ -78,7 +78,16 @@ C5 = Layer("tucker-ive-4M", T=4096, heads=4, dk=128, n_keys=2048, topk=64, topm=
            vdtype=BF16, seed=3, rank=2, grid=GRID_TUCKER, expand=4, dv_virt=512, d_out=2048,
            queries="clusters")
 
-CONFIGS = {c.name: c for c in (C1, C2, C3, C5)}
+# One memory layer of the paper's UltraMem-1.6B-x12 model (its model table: Kdim 448, Knum 1792,
+# top-m 42 x 2 heads; common configuration r = 2, h = 2, E = 4) at the decode batch of 512 tokens
+# the paper times inference with.  Knum^2 counts the virtual slots, so N_p = 1792^2 / 4 physical
+# rows; Dv = 4096 puts the six layers' tables at the model's ~19.7 B sparse parameters, and
+# D'v = 1024 is half the 2048 hidden width (the halved value dimension), projected back to 2048.
+C6 = Layer("ultramem-1.6B-x12", T=512, heads=2, dk=448, n_keys=1792, topk=42, topm=42, dv=4096,
+           vdtype=BF16, seed=6, rank=2, grid=GRID_TUCKER, expand=4, dv_virt=1024, d_out=2048,
+           cores=2)
+
+CONFIGS = {c.name: c for c in (C1, C2, C3, C5, C6)}
 
 
 def _tid(base: int, batch: int) -> int:

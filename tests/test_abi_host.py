@@ -128,6 +128,17 @@ def test_entry_points_reject_before_launch():
     # projection: missing weights / workspace
     assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, fake, fake, fake, 64, 0) == U.UMEM_ERR_WORKSPACE
+    # workspace of the projection: the intermediate plus split-K partials where K is long
+    st, n = U.umem_project_workspace_size(8, 4, 512, 512, 2048)
+    assert st == U.UMEM_OK and n >= 8 * 512 * 4
+    st, n1 = U.umem_project_workspace_size(512, 4, 4096, 1024, 2048)
+    assert st == U.UMEM_OK and n1 >= 512 * 1024 * 4 * 2       # K = 16384 over 64 tiles: split
+    st, n2 = U.umem_project_workspace_size(1 << 16, 4, 512, 512, 2048)
+    assert st == U.UMEM_OK and n2 == ((1 << 16) * 512 * 4 + 255) // 256 * 256   # many tiles: none
+    assert U.umem_project_workspace_size(0, 4, 512, 512, 2048) == (U.UMEM_OK, 0)
+    assert U.umem_project_workspace_size(8, 4, 512, 516, 2048)[0] == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_project_workspace_size(8, 2, 512, 0, 2048)[0] == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_project(8, 4, 512, 512, 2048, fake, fake, fake, fake, fake, n - 16, 0) == U.UMEM_ERR_WORKSPACE
     # the GEMMs read 16-byte pieces of pooled rows and weight rows
     assert U.umem_project(8, 4, 512, 516, 2048, fake, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
     assert U.umem_project(8, 4, 512, 512, 2044, fake, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED

@@ -207,6 +207,13 @@ def test_multi_core_scoring(kw):
     run_and_check(small("mcs", **kw))
 
 
+def test_paper_model_layer_sampled():
+    """One memory layer of the paper's UltraMem-1.6B-x12 model (Kdim 448, 1792^2 slots, top-42 of
+    2 heads, r = 2, h = 2, E = 4, 8 KiB rows) at a 512-token decode batch."""
+    rng = np.random.default_rng(6)
+    run_and_check(CF.C6, tokens=np.sort(rng.choice(CF.C6.T, 8, replace=False)))
+
+
 def test_c5_tucker_ive_mcs_sampled():
     """The rank-2 Tucker + IVE layer with the paper's default two component cores."""
     cfg = dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M")
@@ -263,7 +270,9 @@ def test_select_pools_like_gather(kw):
     (256, CF.F32, 1, 7, 5001, 1),
     # multi-core weights (eq. (17)): column slices, with IVE, sub-rows, many tokens
     (512, CF.BF16, 1, 64, 37, 2), (1024, CF.BF16, 4, 100, 37, 4), (64, CF.BF16, 1, 33, 70, 4),
-    (256, CF.F32, 1, 33, 4099, 2), (3072, CF.BF16, 1, 20, 9, 8)])
+    (256, CF.F32, 1, 33, 4099, 2), (3072, CF.BF16, 1, 20, 9, 8),
+    # 8 KiB rows with IVE and two cores (the paper's 1.6B-x12 layer)
+    (4096, CF.BF16, 4, 84, 37, 2)])
 def test_gather_standalone(dv, vdtype, expand, bag, T, cores):
     rng = np.random.default_rng(dv + bag + T + cores)
     Np = 5000
@@ -288,7 +297,9 @@ def test_gather_standalone(dv, vdtype, expand, bag, T, cores):
 
 
 @pytest.mark.parametrize("T,E,dv,dvv,dout", [(70, 4, 512, 512, 2048), (5, 1, 256, 0, 96),
-                                              (130, 9, 64, 80, 0)])
+                                              (130, 9, 64, 80, 0),
+                                              # long K over few tiles: split reductions
+                                              (37, 4, 4096, 1024, 2048), (200, 1, 2048, 0, 64)])
 def test_project_standalone(T, E, dv, dvv, dout):
     rng = np.random.default_rng(T)
     pooled = rng.standard_normal((T, E, dv)).astype(np.float32)
@@ -297,7 +308,9 @@ def test_project_standalone(T, E, dv, dvv, dout):
     wo = S.f32_to_bf16_bits(rng.standard_normal((kin, dout)) / np.sqrt(kin)).reshape(kin, dout) if dout else None
     width = dout if dout else dvv
     out = torch.empty((T, width), dtype=torch.float32, device="cuda")
-    ws = torch.empty(max(T * max(dvv, 1) * 4, 256), dtype=torch.uint8, device="cuda")
+    st, nws = U.umem_project_workspace_size(T, E, dv, dvv, dout)
+    U.check(st)
+    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
     dev = lambda a: None if a is None else torch.from_numpy(a.view(np.int16)).cuda()
     U.check(U.umem_project(T, E, dv, dvv, dout, torch.from_numpy(pooled).cuda(), dev(wp), dev(wo), out,
                            ws, ws.numel()))
