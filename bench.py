@@ -345,11 +345,78 @@ def workload_report(cfg, steps=50, warmup=5):
                gather_unique_row_bytes=int(uniq),
                gather_unique_GBps=round(uniq / (st["gather_kernel"] * 1e-6) / 1e9, 1),
                gather_logical_GBps=round(g["row_bytes"] / (st["gather_kernel"] * 1e-6) / 1e9, 1))
+    fe = front_ends().get(cfg.name)
+    if fe is not None:
+        rep["front_end"] = front_end_report(fe)
+        rep["tokens_per_s_with_front_end"] = round(
+            cfg.T / ((secs / n) + rep["front_end"]["avg_us"] * 1e-6), 1)
     log(f"workload {cfg.name}: {rep}")
     del r
     import torch
     torch.cuda.empty_cache()
     return rep
+
+
+def front_end_report(fe, launches=200):
+    """The query front-end (convolution, query linear, LayerNorm) of ``fe``: the average
+    duration of ``launches`` umem_query calls replayed from a HIP graph, and its roofline."""
+    import numpy as np
+    import torch
+
+    import paper_2411_12364_amd as U
+    from synth import configs as CF
+    inp = CF.front_end_inputs(fe)
+    qd = U.umem_query_desc()
+    qd.d_model, qd.conv_k, qd.heads, qd.dk, qd.shared, qd.eps = (fe.d_model, fe.conv_k, fe.heads,
+                                                                  fe.dk, int(fe.shared), fe.eps)
+    st, nws = U.umem_query_workspace_size(qd, fe.B, fe.L)
+    U.check(st)
+    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
+    dev = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    x, hist, cw = dev(inp["x"]), dev(inp["hist"]), dev(inp["conv_w"])
+    wq, g, b = dev(inp["w_q"].view(np.int16)), dev(inp["gamma"]), dev(inp["beta"])
+    q_row = torch.empty((fe.T, fe.heads, fe.dk), dtype=torch.float32, device="cuda")
+    q_col = None if fe.shared else torch.empty_like(q_row)
+
+    def call():
+        st = U.umem_query(qd, fe.B, fe.L, x, hist, cw, wq, g, b, q_row, q_col, ws, ws.numel())
+        if st:
+            U.check(st, "umem_query")
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(launches):
+            call()
+    graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / launches
+    A = 1 if fe.shared else 2
+    hist_rows = fe.B * (fe.conv_k - 1) if fe.history else 0
+    algo = (4 * (fe.T + hist_rows + fe.conv_k) * fe.d_model + 2 * fe.d_model * fe.n_queries
+            + 4 * 2 * A * fe.heads * fe.dk + 4 * fe.T * fe.n_queries)
+    flops = 2 * fe.T * fe.d_model * fe.n_queries
+    achieved = algo / (us * 1e-6) / 1e9
+    rep = dict(front_end=fe.name, tokens=fe.T, d_model=fe.d_model, conv_k=fe.conv_k,
+               shared=fe.shared, avg_us=round(us, 3), algorithmic_bytes=algo,
+               roofline=dict(kernel="query_front_end", bound="hbm", achieved=round(achieved, 1),
+                             peak=HBM_PEAK_GBS, unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4),
+                             traffic=None, avg_us=round(us, 3)),
+               gemm_TFLOPs=round(flops / (us * 1e-6) / 1e12, 2))
+    log(f"front end {fe.name}: {rep}")
+    return rep
+
+
+def front_ends():
+    """Layer name -> the query front-end timed beside that layer's forward."""
+    from synth import configs as CF
+    return {CF.C6.name: CF.FE6}
 
 
 def extra_workloads(CF):

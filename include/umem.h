@@ -188,6 +188,50 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
                          const uint16_t* w_out, float* out, int32_t* idx_out,
                          float* w_out_scores, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The query front-end of the layer (Sec. 3.2 bag of tricks): a causal depthwise convolution
+ * of the hidden states (Trick 4), the query linear of eq. (2), and a LayerNorm of each head's
+ * query (Trick 2); with `shared` one query serves both key sets (Trick 5). */
+typedef struct umem_query_desc {
+  int32_t d_model;  /* width d of the hidden states */
+  int32_t conv_k;   /* K_c: convolution taps per channel, tap 0 the current token */
+  int32_t heads;    /* H */
+  int32_t dk;       /* D_k per head */
+  int32_t shared;   /* 1: one query per head for both key sets; 0: row and column queries */
+  float eps;        /* LayerNorm epsilon */
+} umem_query_desc;
+/* Requirements (UMEM_ERR_INVALID_ARG otherwise): every count >= 1, shared 0 or 1, eps >= 0.
+ * Limits (UMEM_ERR_UNSUPPORTED beyond them): d_model % 4 == 0; conv_k <= 8; dk <= 1024;
+ *   (shared ? 1 : 2) * heads * dk a multiple of 8. */
+
+/* Scratch bytes umem_query needs for B sequences of L tokens. */
+UMEM_API umem_status umem_query_workspace_size(const umem_query_desc* qd, int32_t B, int32_t L,
+                                      size_t* bytes);
+
+/* Queries of T = B * L tokens (token t = b * L + l of sequence b) from their hidden states.
+ *   x       fp32 [B, L, d_model], 16-byte aligned
+ *   x_hist  fp32 [B, conv_k - 1, d_model], 16-byte aligned: the hidden states before each
+ *           sequence's first token here (oldest first), or NULL for zeros (a sequence start)
+ *   conv_w  fp32 [conv_k, d_model], 16-byte aligned (no bias)
+ *   w_q     bf16 bits [d_model, A * heads * dk], 16-byte aligned, A = 1 if shared else 2: the
+ *           row queries of the H heads, then (A = 2) the column queries; the convolved rows are
+ *           rounded to bf16 (nearest even) for this product, fp32 accumulation
+ *   gamma, beta  fp32 [A, heads, dk]: the LayerNorm of each (axis, head)
+ *   q_row   fp32 [T, heads, dk]; q_col the same, or NULL when shared (pass q_row for both
+ *           key sets to the scoring then)
+ *   ws      16-byte aligned scratch of umem_query_workspace_size(...) bytes */
+UMEM_API umem_status umem_query(const umem_query_desc* qd, int32_t B, int32_t L, const float* x,
+                       const float* x_hist, const float* conv_w, const uint16_t* w_q,
+                       const float* gamma, const float* beta, float* q_row, float* q_col,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The LayerNorm of a key set (Trick 2), computed once since keys are parameters: each of the
+ * heads * n rows of dk elements of keys [heads, n, dk] is normalised (population variance, eps)
+ * and scaled and shifted by its head's gamma, beta [heads, dk].  out may equal keys.
+ * dk <= 1024 (UMEM_ERR_UNSUPPORTED beyond). */
+UMEM_API umem_status umem_key_norm(int32_t heads, int32_t n, int32_t dk, const float* keys,
+                          const float* gamma, const float* beta, float eps, float* out,
+                          hipStream_t stream);
+
 /* A static, human-readable name of a status code. */
 UMEM_API const char* umem_status_string(umem_status status);
 

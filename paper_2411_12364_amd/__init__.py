@@ -32,7 +32,7 @@ UMEM_W_RAW, UMEM_W_SOFTMAX = 0, 1
 
 EXPORTED = ("umem_workspace_size", "umem_axis_scores", "umem_select", "umem_score_topk",
             "umem_gather_sum", "umem_project_workspace_size", "umem_project", "umem_forward",
-            "umem_status_string")
+            "umem_query_workspace_size", "umem_query", "umem_key_norm", "umem_status_string")
 
 
 class umem_desc(ctypes.Structure):
@@ -42,6 +42,13 @@ class umem_desc(ctypes.Structure):
         ("grid", ctypes.c_int32), ("weight", ctypes.c_int32), ("n_values", ctypes.c_int64),
         ("dv", ctypes.c_int32), ("vdtype", ctypes.c_int32), ("expand", ctypes.c_int32),
         ("dv_virt", ctypes.c_int32), ("d_out", ctypes.c_int32), ("cores", ctypes.c_int32),
+    ]
+
+
+class umem_query_desc(ctypes.Structure):
+    _fields_ = [
+        ("d_model", ctypes.c_int32), ("conv_k", ctypes.c_int32), ("heads", ctypes.c_int32),
+        ("dk", ctypes.c_int32), ("shared", ctypes.c_int32), ("eps", ctypes.c_float),
     ]
 
 
@@ -66,6 +73,9 @@ def _load() -> ctypes.CDLL:
         "umem_project_workspace_size": [I32, I32, I32, I32, I32, ctypes.POINTER(SZ)],
         "umem_project": [I32, I32, I32, I32, I32, P, P, P, P, P, SZ, P],
         "umem_forward": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
+        "umem_query_workspace_size": [ctypes.POINTER(umem_query_desc), I32, I32, ctypes.POINTER(SZ)],
+        "umem_query": [ctypes.POINTER(umem_query_desc), I32, I32, P, P, P, P, P, P, P, P, P, SZ, P],
+        "umem_key_norm": [I32, I32, I32, P, P, P, ctypes.c_float, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -163,3 +173,20 @@ def umem_forward(desc, T, q_row, q_col, k_row, k_col, core, values, perm, w_proj
     return _lib.umem_forward(_d(desc), T, _p(q_row), _p(q_col), _p(k_row), _p(k_col), _p(core),
                              _p(values), _p(perm), _p(w_proj), _p(w_out), _p(out), _p(idx_out),
                              _p(w_out_scores), _p(ws), ws_bytes, _s(stream))
+
+
+def umem_query_workspace_size(qd, B, L):
+    """Returns (status, bytes)."""
+    out = ctypes.c_size_t(0)
+    st = _lib.umem_query_workspace_size(ctypes.byref(qd), B, L, ctypes.byref(out))
+    return st, out.value
+
+
+def umem_query(qd, B, L, x, x_hist, conv_w, w_q, gamma, beta, q_row, q_col, ws, ws_bytes,
+               stream=None) -> int:
+    return _lib.umem_query(ctypes.byref(qd), B, L, _p(x), _p(x_hist), _p(conv_w), _p(w_q),
+                           _p(gamma), _p(beta), _p(q_row), _p(q_col), _p(ws), ws_bytes, _s(stream))
+
+
+def umem_key_norm(heads, n, dk, keys, gamma, beta, eps, out, stream=None) -> int:
+    return _lib.umem_key_norm(heads, n, dk, _p(keys), _p(gamma), _p(beta), eps, _p(out), _s(stream))

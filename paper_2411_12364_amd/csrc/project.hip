@@ -160,14 +160,15 @@ int split_count(int M, int N, int K) {
 
 size_t round_up256(size_t x) { return (x + 255) / 256 * 256; }
 
-size_t partial_bytes(int M, int N, int K) {
+}  // namespace
+
+size_t gemm_partial_bytes(int M, int N, int K) {
   const int S = split_count(M, N, K);
   return S > 1 ? round_up256(static_cast<size_t>(S) * M * N * sizeof(float)) : 0;
 }
 
-// C [M, N] = bf16(A [M, K]) B [K, N]; part: split-K scratch of partial_bytes(M, N, K) bytes.
-hipError_t gemm(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
-                hipStream_t s) {
+hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
+                     hipStream_t s) {
   const int tn = (N + BN - 1) / BN;
   const int tiles = n_tiles(M, N);
   const int per = (tiles + kXcds - 1) / kXcds;
@@ -184,14 +185,12 @@ hipError_t gemm(const float* A, const uint16_t* B, float* C, int M, int N, int K
   return hipGetLastError();
 }
 
-}  // namespace
-
 size_t project_workspace_bytes(int T, int expand, int dv, int dv_virt, int d_out) {
   if (T == 0) return 0;
-  if (dv_virt == 0) return partial_bytes(T, d_out, dv);          // the output linear alone
+  if (dv_virt == 0) return gemm_partial_bytes(T, d_out, dv);          // the output linear alone
   const size_t tmp = d_out > 0 ? round_up256(static_cast<size_t>(T) * dv_virt * sizeof(float)) : 0;
-  const size_t p1 = partial_bytes(T, dv_virt, expand * dv);
-  const size_t p2 = d_out > 0 ? partial_bytes(T, d_out, dv_virt) : 0;
+  const size_t p1 = gemm_partial_bytes(T, dv_virt, expand * dv);
+  const size_t p2 = d_out > 0 ? gemm_partial_bytes(T, d_out, dv_virt) : 0;
   return tmp + std::max(p1, p2);
 }
 
@@ -202,15 +201,15 @@ hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, con
   if (T == 0) return hipSuccess;
   char* base = static_cast<char*>(ws);
   if (w_proj == nullptr)   // the output linear alone: [T, dv] by [dv, d_out]
-    return gemm(pooled, w_out, out, T, d_out, dv, reinterpret_cast<float*>(base), s);
+    return gemm_bf16(pooled, w_out, out, T, d_out, dv, reinterpret_cast<float*>(base), s);
   if (w_out == nullptr)
-    return gemm(pooled, w_proj, out, T, dv_virt, expand * dv, reinterpret_cast<float*>(base), s);
+    return gemm_bf16(pooled, w_proj, out, T, dv_virt, expand * dv, reinterpret_cast<float*>(base), s);
   // the two GEMMs use the partial scratch one after the other, in stream order
   float* tmp = reinterpret_cast<float*>(base);
   float* part = reinterpret_cast<float*>(base + round_up256(static_cast<size_t>(T) * dv_virt * sizeof(float)));
-  hipError_t e = gemm(pooled, w_proj, tmp, T, dv_virt, expand * dv, part, s);
+  hipError_t e = gemm_bf16(pooled, w_proj, tmp, T, dv_virt, expand * dv, part, s);
   if (e != hipSuccess) return e;
-  return gemm(tmp, w_out, out, T, d_out, dv_virt, part, s);
+  return gemm_bf16(tmp, w_out, out, T, d_out, dv_virt, part, s);
 }
 
 }  // namespace umem

@@ -2,6 +2,8 @@
 // Every entry point validates everything before it enqueues anything.
 #include <stdint.h>
 
+#include <cmath>
+
 #include "umem_internal.h"
 
 using namespace umem;
@@ -277,6 +279,73 @@ UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t
                                  ws_bytes);
   if (st != UMEM_OK || T == 0) return st;
   return hip_status(run_project(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws, stream));
+}
+
+}  // extern "C"
+
+namespace {
+
+umem_status check_query_desc(const umem_query_desc* qd) {
+  if (qd == nullptr) return UMEM_ERR_INVALID_ARG;
+  if (qd->d_model < 1 || qd->conv_k < 1 || qd->heads < 1 || qd->dk < 1) return UMEM_ERR_INVALID_ARG;
+  if ((qd->shared != 0 && qd->shared != 1) || !(qd->eps >= 0.0f) || qd->eps == INFINITY)
+    return UMEM_ERR_INVALID_ARG;
+  const int64_t nq = static_cast<int64_t>(qd->shared ? 1 : 2) * qd->heads * qd->dk;
+  if (qd->d_model % 4 != 0 || qd->conv_k > 8 || qd->dk > 1024 || nq % 8 != 0 || nq > (1 << 24))
+    return UMEM_ERR_UNSUPPORTED;
+  return UMEM_OK;
+}
+
+umem_status check_query_tokens(int32_t B, int32_t L) {
+  if (B < 0 || L < 0) return UMEM_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(B) * L > kMaxTokens) return UMEM_ERR_UNSUPPORTED;
+  return UMEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+UMEM_API umem_status umem_query_workspace_size(const umem_query_desc* qd, int32_t B, int32_t L,
+                                               size_t* bytes) {
+  if (bytes == nullptr) return UMEM_ERR_INVALID_ARG;
+  *bytes = 0;
+  umem_status st = check_query_desc(qd);
+  if (st == UMEM_OK) st = check_query_tokens(B, L);
+  if (st != UMEM_OK) return st;
+  *bytes = query_workspace_bytes(*qd, static_cast<int64_t>(B) * L);
+  return UMEM_OK;
+}
+
+UMEM_API umem_status umem_query(const umem_query_desc* qd, int32_t B, int32_t L, const float* x,
+                                const float* x_hist, const float* conv_w, const uint16_t* w_q,
+                                const float* gamma, const float* beta, float* q_row, float* q_col,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
+  umem_status st = check_query_desc(qd);
+  if (st == UMEM_OK) st = check_query_tokens(B, L);
+  if (st != UMEM_OK) return st;
+  if (static_cast<int64_t>(B) * L == 0) return UMEM_OK;
+  if (!x || !conv_w || !w_q || !gamma || !beta || !q_row) return UMEM_ERR_INVALID_ARG;
+  if ((q_col == nullptr) != (qd->shared == 1)) return UMEM_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(x_hist, 16) || !aligned(conv_w, 16) || !aligned(w_q, 16))
+    return UMEM_ERR_INVALID_ARG;
+  if (!aligned(gamma, 4) || !aligned(beta, 4) || !aligned(q_row, 4) || !aligned(q_col, 4))
+    return UMEM_ERR_INVALID_ARG;
+  const size_t need = query_workspace_bytes(*qd, static_cast<int64_t>(B) * L);
+  if (ws == nullptr || !aligned(ws, 16) || ws_bytes < need) return UMEM_ERR_WORKSPACE;
+  return hip_status(launch_query(*qd, B, L, x, x_hist, conv_w, w_q, gamma, beta, q_row, q_col, ws,
+                                 stream));
+}
+
+UMEM_API umem_status umem_key_norm(int32_t heads, int32_t n, int32_t dk, const float* keys,
+                                   const float* gamma, const float* beta, float eps, float* out,
+                                   hipStream_t stream) {
+  if (heads < 1 || n < 1 || dk < 1 || !(eps >= 0.0f) || eps == INFINITY) return UMEM_ERR_INVALID_ARG;
+  if (!keys || !gamma || !beta || !out) return UMEM_ERR_INVALID_ARG;
+  if (!aligned(keys, 4) || !aligned(gamma, 4) || !aligned(beta, 4) || !aligned(out, 4))
+    return UMEM_ERR_INVALID_ARG;
+  if (dk > 1024 || static_cast<int64_t>(heads) * n > (INT64_C(1) << 31)) return UMEM_ERR_UNSUPPORTED;
+  return hip_status(launch_key_norm(heads, n, dk, keys, gamma, beta, eps, out, stream));
 }
 
 UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float* q_row,

@@ -67,6 +67,22 @@ hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* value
 inline int n_cores(const umem_desc& d) { return d.cores > 1 ? d.cores : 1; }
 bool cores_supported(int dv, int vdtype, int cores);
 
+// C [M, N] = bf16(A [M, K]) B [K, N] on MFMA with fp32 accumulation (A fp32, B bf16 bits, all
+// 16-byte aligned, K % 4 == 0, N % 8 == 0); part: gemm_partial_bytes(M, N, K) bytes of scratch
+// for the split-K partial sums (unused when that is 0).
+size_t gemm_partial_bytes(int M, int N, int K);
+hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
+                     hipStream_t s);
+
+// The query front-end and the key LayerNorm (query.hip).  ws: query_workspace_bytes bytes.
+size_t query_workspace_bytes(const umem_query_desc& qd, int64_t T);
+hipError_t launch_query(const umem_query_desc& qd, int B, int L, const float* x,
+                        const float* x_hist, const float* conv_w, const uint16_t* w_q,
+                        const float* gamma, const float* beta, float* q_row, float* q_col,
+                        void* ws, hipStream_t s);
+hipError_t launch_key_norm(int heads, int n, int dk, const float* keys, const float* gamma,
+                           const float* beta, float eps, float* out, hipStream_t s);
+
 // a8.  ws: project_workspace_bytes(...) bytes, 256-byte aligned (the intermediate and the
 // split-K partials); w_proj == nullptr is the output linear alone ([T, dv] by [dv, d_out]).
 size_t project_workspace_bytes(int T, int expand, int dv, int dv_virt, int d_out);

@@ -46,6 +46,14 @@ TID_CENTRES_COL = 11
 TID_EPS_ROW = 12
 TID_EPS_COL = 13
 TID_CLUSTER = 14
+TID_HIDDEN = 15
+TID_HIST = 16
+TID_CONV_W = 17
+TID_W_Q = 18
+TID_Q_GAMMA = 19
+TID_Q_BETA = 20
+TID_K_GAMMA = 21
+TID_K_BETA = 22
 
 
 def _fmix_int(z: int) -> int:

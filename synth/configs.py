@@ -90,6 +90,59 @@ C6 = Layer("ultramem-1.6B-x12", T=512, heads=2, dk=448, n_keys=1792, topk=42, to
 CONFIGS = {c.name: c for c in (C1, C2, C3, C5, C6)}
 
 
+@dataclasses.dataclass(frozen=True)
+class FrontEnd:
+    """The query front-end of a layer: B sequences of L tokens of d_model-wide hidden states."""
+    name: str
+    B: int
+    L: int
+    d_model: int
+    conv_k: int        # causal depthwise convolution taps
+    heads: int
+    dk: int
+    shared: bool       # one query for both key sets
+    seed: int
+    history: bool = True   # hidden states before each sequence's first token (else a start)
+    eps: float = 1e-5
+
+    @property
+    def T(self) -> int:
+        return self.B * self.L
+
+    @property
+    def n_queries(self) -> int:
+        return (1 if self.shared else 2) * self.heads * self.dk
+
+
+# The front-end of the UltraMem-1.6B-x12 layer above at its 512-token decode batch: one new token
+# per sequence, the three before it as the convolution's history; hidden width 2048; K_c = 4.
+FE6 = FrontEnd("ultramem-1.6B-x12-query", B=512, L=1, d_model=2048, conv_k=4, heads=2, dk=448,
+               shared=True, seed=6)
+
+
+def front_end_inputs(fe: FrontEnd) -> dict:
+    """x fp32 [B, L, d]; hist fp32 [B, K_c - 1, d] or None; conv_w fp32 [K_c, d];
+    w_q bf16 bits [d, A H Dk]; gamma, beta fp32 [A, H, Dk] (A = 1 shared, else 2)."""
+    A = 1 if fe.shared else 2
+    x = S.tensor_f32(fe.seed, S.TID_HIDDEN, (fe.B, fe.L, fe.d_model), 1.0)
+    hist = (S.tensor_f32(fe.seed, S.TID_HIST, (fe.B, fe.conv_k - 1, fe.d_model), 1.0)
+            if fe.history and fe.conv_k > 1 else None)
+    conv_w = S.tensor_f32(fe.seed, S.TID_CONV_W, (fe.conv_k, fe.d_model), 1.0 / math.sqrt(fe.conv_k))
+    wq = S.tensor_f32(fe.seed, S.TID_W_Q, (fe.d_model, fe.n_queries), 1.0 / math.sqrt(fe.d_model))
+    gamma = (np.float32(1.0) + S.tensor_f32(fe.seed, S.TID_Q_GAMMA, (A, fe.heads, fe.dk), 0.1)).astype(np.float32)
+    beta = S.tensor_f32(fe.seed, S.TID_Q_BETA, (A, fe.heads, fe.dk), 0.05)
+    return dict(x=x, hist=hist, conv_w=conv_w, w_q=S.f32_to_bf16_bits(wq).reshape(wq.shape),
+                gamma=gamma, beta=beta)
+
+
+def key_norm_params(cfg: Layer):
+    """gamma, beta fp32 [H, Dk] of the key LayerNorm (the appendix initialises gamma to
+    1/sqrt(Dk); a spread around that)."""
+    g = S.tensor_f32(cfg.seed, S.TID_K_GAMMA, (cfg.heads, cfg.dk), 0.1 / math.sqrt(cfg.dk))
+    b = S.tensor_f32(cfg.seed, S.TID_K_BETA, (cfg.heads, cfg.dk), 0.01 / math.sqrt(cfg.dk))
+    return (np.float32(1.0 / math.sqrt(cfg.dk)) + g).astype(np.float32), b
+
+
 def _tid(base: int, batch: int) -> int:
     return base + (batch << 8)
 

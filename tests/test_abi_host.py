@@ -167,3 +167,56 @@ def test_one_hip_runtime_in_process():
     with open("/proc/self/maps") as f:
         paths = {line.split()[-1] for line in f if "libamdhip64" in line}
     assert len({os.path.realpath(p) for p in paths}) == 1, paths
+
+
+def qdesc(**kw):
+    d = U.umem_query_desc()
+    base = dict(d_model=2048, conv_k=4, heads=2, dk=448, shared=1, eps=1e-5)
+    base.update(kw)
+    for k, v in base.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(), U.UMEM_OK),
+    (dict(d_model=0), U.UMEM_ERR_INVALID_ARG),
+    (dict(conv_k=0), U.UMEM_ERR_INVALID_ARG),
+    (dict(shared=2), U.UMEM_ERR_INVALID_ARG),
+    (dict(eps=-1.0), U.UMEM_ERR_INVALID_ARG),
+    (dict(eps=float("nan")), U.UMEM_ERR_INVALID_ARG),
+    (dict(d_model=2046), U.UMEM_ERR_UNSUPPORTED),          # 16-byte pieces of a hidden row
+    (dict(conv_k=9), U.UMEM_ERR_UNSUPPORTED),
+    (dict(dk=1028), U.UMEM_ERR_UNSUPPORTED),
+    (dict(heads=1, dk=4), U.UMEM_ERR_UNSUPPORTED),         # 4 query outputs: not whole 16-byte pieces
+    (dict(heads=1, dk=4, shared=0), U.UMEM_OK),
+])
+def test_query_desc_validation(kw, want):
+    st, n = U.umem_query_workspace_size(qdesc(**kw), 512, 1)
+    assert st == want and (n == 0) == (st != U.UMEM_OK)
+
+
+def test_query_workspace_and_entry_validation():
+    qd = qdesc()
+    st, n = U.umem_query_workspace_size(qd, 512, 1)
+    assert st == U.UMEM_OK and n >= 512 * 2048 * 4 + 512 * 2 * 448 * 4
+    assert U.umem_query_workspace_size(qd, 0, 5) == (U.UMEM_OK, 0)
+    assert U.umem_query_workspace_size(qd, -1, 5)[0] == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_query_workspace_size(qd, 1 << 20, 2)[0] == U.UMEM_ERR_UNSUPPORTED
+    fake = 1 << 20
+    args = [fake, fake, fake, fake, fake, fake, fake, None]    # x, hist, conv_w, w_q, gamma, beta, q_row, q_col
+    bad = list(args)
+    bad[0] = None
+    assert U.umem_query(qd, 512, 1, *bad, fake, n, 0) == U.UMEM_ERR_INVALID_ARG
+    bad = list(args)
+    bad[7] = fake                                              # q_col with a shared query
+    assert U.umem_query(qd, 512, 1, *bad, fake, n, 0) == U.UMEM_ERR_INVALID_ARG
+    bad = list(args)
+    bad[3] = fake + 8                                          # w_q not 16-byte aligned
+    assert U.umem_query(qd, 512, 1, *bad, fake, n, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_query(qd, 512, 1, *args, fake, n - 16, 0) == U.UMEM_ERR_WORKSPACE
+    assert U.umem_query(qd, 0, 1, None, None, None, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
+    assert U.umem_key_norm(2, 0, 448, fake, fake, fake, 1e-5, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_key_norm(2, 16, 1100, fake, fake, fake, 1e-5, fake, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_key_norm(2, 16, 448, fake + 2, fake, fake, 1e-5, fake, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_key_norm(2, 16, 448, fake, fake, fake, -1.0, fake, 0) == U.UMEM_ERR_INVALID_ARG
