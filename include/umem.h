@@ -188,6 +188,50 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
                          const uint16_t* w_out, float* out, int32_t* idx_out,
                          float* w_out_scores, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Backward of the gather-sum (eq. (1); eq. (15) per virtual block; eq. (17) per column slice),
+ * for training: with the selection of the forward held fixed,
+ *   dw[t, b(, c)] = <d_pooled[t, p, slice c], V[row, slice c]>   (written)
+ *   d_values[row, slice c] += sum over the entries (t, b) on that row of w[t, b(, c)] d_pooled[t, p, slice c]
+ * where (p, row) is the entry's virtual block and physical row (as umem_gather_sum maps them).
+ *   values, idx, w, perm, expand, cores  as for umem_gather_sum (the forward's selection)
+ *   d_pooled  fp32 [T, expand, dv], 16-byte aligned: the gradient of the pooled rows
+ *   d_values  fp32 [n_values, dv], 16-byte aligned: accumulated into (only the rows the bag
+ *             touches change; clear it between steps as the optimiser needs)
+ *   dw        fp32 [T, bag] or [T, bag, cores]
+ *   ws        16-byte aligned scratch of umem_gather_backward_workspace_size(T, bag) bytes
+ * Entries on one row are summed in their bag order by one writer, so the result does not depend
+ * on timing.  T * bag <= 2^22 (UMEM_ERR_UNSUPPORTED beyond). */
+UMEM_API umem_status umem_gather_backward_workspace_size(int32_t T, int32_t bag, size_t* bytes);
+UMEM_API umem_status umem_gather_backward(int64_t n_values, int32_t dv, int32_t vdtype, const void* values,
+                                 int32_t T, int32_t bag, const int32_t* idx, const float* w,
+                                 const int32_t* perm, int32_t expand, int32_t cores,
+                                 const float* d_pooled, float* d_values, float* dw, void* ws,
+                                 size_t ws_bytes, hipStream_t stream);
+
+/* Backward of the scores (eqs. (2)-(4), (10), (16)) with the forward's selection held fixed: the
+ * gradient reaches q, K and C only through the selected slots' scores (the top-k and top-m are
+ * piecewise constant; the rank-1 factors only select).  Weight gradients become grid-score
+ * gradients (eq. (3)'s SoftMax Jacobian with UMEM_W_SOFTMAX), then
+ *   additive: dS_row[i] += dg, dS_col[j] += dg;  Tucker (per core c with multi-core scoring):
+ *   dS_row[:, i] += dg C S_col[:, j], dS_col[:, j] += dg C^T S_row[:, i], dC += dg S_row[:, i] S_col[:, j]^T
+ *   dq[slice r] = sum_i dS[r, i] K[i, slice r]  (written), dK[i, slice r] += dS[r, i] q[slice r]
+ *   desc, q_row, q_col, k_row, k_col, core  as for the forward
+ *   idx     int32 [T, H, m]: the forward's selection; w fp32 [T, H, m]: its weights (needed with
+ *           UMEM_W_SOFTMAX, else may be NULL)
+ *   dw      fp32 [T, H, m] (or [T, H, m, h] with multi-core scoring): the weight gradients
+ *   dq_row, dq_col  fp32 [T, H, dk] (written); dk_row, dk_col fp32 [H, n_keys, dk], 16-byte
+ *           aligned (accumulated); dcore fp32 [H, r, r] or [H, h, r, r] (accumulated; Tucker
+ *           grid only, else NULL)
+ *   ws      16-byte aligned scratch of umem_score_backward_workspace_size(desc, T) bytes
+ * Sums over tokens (dK, dC) run in a fixed order.  T * H * 2 * m <= 2^22. */
+UMEM_API umem_status umem_score_backward_workspace_size(const umem_desc* desc, int32_t T, size_t* bytes);
+UMEM_API umem_status umem_score_backward(const umem_desc* desc, int32_t T, const float* q_row,
+                                const float* q_col, const float* k_row, const float* k_col,
+                                const float* core, const int32_t* idx, const float* w,
+                                const float* dw, float* dq_row, float* dq_col, float* dk_row,
+                                float* dk_col, float* dcore, void* ws, size_t ws_bytes,
+                                hipStream_t stream);
+
 /* The query front-end of the layer (Sec. 3.2 bag of tricks): a causal depthwise convolution
  * of the hidden states (Trick 4), the query linear of eq. (2), and a LayerNorm of each head's
  * query (Trick 2); with `shared` one query serves both key sets (Trick 5). */

@@ -32,7 +32,9 @@ UMEM_W_RAW, UMEM_W_SOFTMAX = 0, 1
 
 EXPORTED = ("umem_workspace_size", "umem_axis_scores", "umem_select", "umem_score_topk",
             "umem_gather_sum", "umem_project_workspace_size", "umem_project", "umem_forward",
-            "umem_query_workspace_size", "umem_query", "umem_key_norm", "umem_status_string")
+            "umem_query_workspace_size", "umem_query", "umem_key_norm",
+            "umem_gather_backward_workspace_size", "umem_gather_backward",
+            "umem_score_backward_workspace_size", "umem_score_backward", "umem_status_string")
 
 
 class umem_desc(ctypes.Structure):
@@ -76,6 +78,10 @@ def _load() -> ctypes.CDLL:
         "umem_query_workspace_size": [ctypes.POINTER(umem_query_desc), I32, I32, ctypes.POINTER(SZ)],
         "umem_query": [ctypes.POINTER(umem_query_desc), I32, I32, P, P, P, P, P, P, P, P, P, SZ, P],
         "umem_key_norm": [I32, I32, I32, P, P, P, ctypes.c_float, P, P],
+        "umem_gather_backward_workspace_size": [I32, I32, ctypes.POINTER(SZ)],
+        "umem_gather_backward": [I64, I32, I32, P, I32, I32, P, P, P, I32, I32, P, P, P, P, SZ, P],
+        "umem_score_backward_workspace_size": [D, I32, ctypes.POINTER(SZ)],
+        "umem_score_backward": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -190,3 +196,31 @@ def umem_query(qd, B, L, x, x_hist, conv_w, w_q, gamma, beta, q_row, q_col, ws, 
 
 def umem_key_norm(heads, n, dk, keys, gamma, beta, eps, out, stream=None) -> int:
     return _lib.umem_key_norm(heads, n, dk, _p(keys), _p(gamma), _p(beta), eps, _p(out), _s(stream))
+
+
+def umem_gather_backward_workspace_size(T, bag):
+    """Returns (status, bytes)."""
+    out = ctypes.c_size_t(0)
+    st = _lib.umem_gather_backward_workspace_size(T, bag, ctypes.byref(out))
+    return st, out.value
+
+
+def umem_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores,
+                         d_pooled, d_values, dw, ws, ws_bytes, stream=None) -> int:
+    return _lib.umem_gather_backward(n_values, dv, vdtype, _p(values), T, bag, _p(idx), _p(w),
+                                     _p(perm), expand, cores, _p(d_pooled), _p(d_values), _p(dw),
+                                     _p(ws), ws_bytes, _s(stream))
+
+
+def umem_score_backward_workspace_size(desc, T):
+    """Returns (status, bytes)."""
+    out = ctypes.c_size_t(0)
+    st = _lib.umem_score_backward_workspace_size(_d(desc), T, ctypes.byref(out))
+    return st, out.value
+
+
+def umem_score_backward(desc, T, q_row, q_col, k_row, k_col, core, idx, w, dw, dq_row, dq_col,
+                        dk_row, dk_col, dcore, ws, ws_bytes, stream=None) -> int:
+    return _lib.umem_score_backward(_d(desc), T, _p(q_row), _p(q_col), _p(k_row), _p(k_col),
+                                    _p(core), _p(idx), _p(w), _p(dw), _p(dq_row), _p(dq_col),
+                                    _p(dk_row), _p(dk_col), _p(dcore), _p(ws), ws_bytes, _s(stream))

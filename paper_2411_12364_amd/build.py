@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libumem.so")
-SOURCES = ["umem_api.hip", "score.hip", "select.hip", "gather.hip", "project.hip", "query.hip"]
+SOURCES = ["umem_api.hip", "score.hip", "select.hip", "gather.hip", "project.hip", "query.hip", "sort.hip", "backward.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

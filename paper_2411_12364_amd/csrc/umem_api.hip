@@ -348,6 +348,75 @@ UMEM_API umem_status umem_key_norm(int32_t heads, int32_t n, int32_t dk, const f
   return hip_status(launch_key_norm(heads, n, dk, keys, gamma, beta, eps, out, stream));
 }
 
+constexpr int64_t kMaxBackwardEntries = INT64_C(1) << 22;   // pairs the backward sorts at once
+
+UMEM_API umem_status umem_gather_backward_workspace_size(int32_t T, int32_t bag, size_t* bytes) {
+  if (bytes == nullptr) return UMEM_ERR_INVALID_ARG;
+  *bytes = 0;
+  if (T < 0 || bag < 1) return UMEM_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(T) * bag > kMaxBackwardEntries) return UMEM_ERR_UNSUPPORTED;
+  *bytes = gather_backward_workspace_bytes(T, bag);
+  return UMEM_OK;
+}
+
+UMEM_API umem_status umem_gather_backward(int64_t n_values, int32_t dv, int32_t vdtype,
+                                          const void* values, int32_t T, int32_t bag,
+                                          const int32_t* idx, const float* w, const int32_t* perm,
+                                          int32_t expand, int32_t cores, const float* d_pooled,
+                                          float* d_values, float* dw, void* ws, size_t ws_bytes,
+                                          hipStream_t stream) {
+  umem_status st = check_gather(n_values, dv, vdtype, values, T, bag, idx, w, expand, cores, d_values);
+  if (st != UMEM_OK || T == 0) return st;
+  if (!d_pooled || !dw || !aligned(d_pooled, 16) || !aligned(dw, 4)) return UMEM_ERR_INVALID_ARG;
+  if ((expand > 1) != (perm != nullptr) || !aligned(perm, 4)) return UMEM_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(T) * bag > kMaxBackwardEntries) return UMEM_ERR_UNSUPPORTED;
+  const size_t need = gather_backward_workspace_bytes(T, bag);
+  if (ws == nullptr || !aligned(ws, 16) || ws_bytes < need) return UMEM_ERR_WORKSPACE;
+  return hip_status(launch_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm,
+                                           expand, cores, d_pooled, d_values, dw, ws, stream));
+}
+
+UMEM_API umem_status umem_score_backward_workspace_size(const umem_desc* desc, int32_t T,
+                                                        size_t* bytes) {
+  if (bytes == nullptr) return UMEM_ERR_INVALID_ARG;
+  *bytes = 0;
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK) return st;
+  if (static_cast<int64_t>(T) * desc->heads * 2 * desc->topm > kMaxBackwardEntries)
+    return UMEM_ERR_UNSUPPORTED;
+  *bytes = score_backward_workspace_bytes(*desc, T);
+  return UMEM_OK;
+}
+
+UMEM_API umem_status umem_score_backward(const umem_desc* desc, int32_t T, const float* q_row,
+                                         const float* q_col, const float* k_row,
+                                         const float* k_col, const float* core,
+                                         const int32_t* idx, const float* w, const float* dw,
+                                         float* dq_row, float* dq_col, float* dk_row,
+                                         float* dk_col, float* dcore, void* ws, size_t ws_bytes,
+                                         hipStream_t stream) {
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
+  if (st != UMEM_OK) return st;
+  const bool softmax = desc->weight == UMEM_W_SOFTMAX;
+  if (!idx || !dw || (softmax && !w)) return UMEM_ERR_INVALID_ARG;
+  if (!aligned(idx, 4) || !aligned(dw, 4) || !aligned(w, 4)) return UMEM_ERR_INVALID_ARG;
+  if (!dq_row || !dq_col || !dk_row || !dk_col) return UMEM_ERR_INVALID_ARG;
+  if (!aligned(dq_row, 4) || !aligned(dq_col, 4) || !aligned(dk_row, 16) || !aligned(dk_col, 16))
+    return UMEM_ERR_INVALID_ARG;
+  if ((desc->grid == UMEM_GRID_TUCKER) != (dcore != nullptr) || !aligned(dcore, 4))
+    return UMEM_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(T) * desc->heads * 2 * desc->topm > kMaxBackwardEntries)
+    return UMEM_ERR_UNSUPPORTED;
+  const size_t need = score_backward_workspace_bytes(*desc, T);
+  if (ws == nullptr || !aligned(ws, 16) || ws_bytes < need) return UMEM_ERR_WORKSPACE;
+  return hip_status(launch_score_backward(*desc, T, q_row, q_col, k_row, k_col, core, idx, w, dw,
+                                          dq_row, dq_col, dk_row, dk_col, dcore, ws, stream));
+}
+
 UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float* q_row,
                                   const float* q_col, const float* k_row, const float* k_col,
                                   const float* core, const void* values, const int32_t* perm,

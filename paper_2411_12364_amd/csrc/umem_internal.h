@@ -74,6 +74,26 @@ size_t gemm_partial_bytes(int M, int N, int K);
 hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
                      hipStream_t s);
 
+// Stable sort of M (key, value) pairs with keys < 2^bits (sort.hip); the inputs are reordered
+// through ws (sort_workspace_bytes(M) bytes, 4-byte aligned) and the sorted arrays returned
+// (either the inputs or part of ws).
+size_t sort_workspace_bytes(int M);
+hipError_t sort_pairs(uint32_t* keys, uint32_t* vals, int M, int bits, void* ws, hipStream_t s,
+                      uint32_t** keys_sorted, uint32_t** vals_sorted);
+
+// Backward of the gather-sum and of the scores (backward.hip).
+size_t gather_backward_workspace_bytes(int T, int bag);
+hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const void* values, int T,
+                                  int bag, const int32_t* idx, const float* w, const int32_t* perm,
+                                  int expand, int cores, const float* d_pooled, float* d_values,
+                                  float* dw, void* ws, hipStream_t s);
+size_t score_backward_workspace_bytes(const umem_desc& d, int T);
+hipError_t launch_score_backward(const umem_desc& d, int T, const float* q_row, const float* q_col,
+                                 const float* k_row, const float* k_col, const float* core,
+                                 const int32_t* idx, const float* w, const float* dw,
+                                 float* dq_row, float* dq_col, float* dk_row, float* dk_col,
+                                 float* dcore, void* ws, hipStream_t s);
+
 // The query front-end and the key LayerNorm (query.hip).  ws: query_workspace_bytes bytes.
 size_t query_workspace_bytes(const umem_query_desc& qd, int64_t T);
 hipError_t launch_query(const umem_query_desc& qd, int B, int L, const float* x,

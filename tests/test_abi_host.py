@@ -220,3 +220,33 @@ def test_query_workspace_and_entry_validation():
     assert U.umem_key_norm(2, 16, 1100, fake, fake, fake, 1e-5, fake, 0) == U.UMEM_ERR_UNSUPPORTED
     assert U.umem_key_norm(2, 16, 448, fake + 2, fake, fake, 1e-5, fake, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_key_norm(2, 16, 448, fake, fake, fake, -1.0, fake, 0) == U.UMEM_ERR_INVALID_ARG
+
+
+def test_backward_validation():
+    fake = 1 << 20
+    st, n = U.umem_gather_backward_workspace_size(4096, 256)
+    assert st == U.UMEM_OK and n >= 4096 * 256 * 16
+    assert U.umem_gather_backward_workspace_size(0, 64) == (U.UMEM_OK, 0)
+    assert U.umem_gather_backward_workspace_size(1 << 16, 128)[0] == U.UMEM_ERR_UNSUPPORTED
+    g = [100, 512, 1, fake, 4, 64, fake, fake, None, 1, 1]           # as umem_gather_sum
+    assert U.umem_gather_backward(*g, None, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG   # d_pooled
+    assert U.umem_gather_backward(*g, fake, fake, None, fake, n, 0) == U.UMEM_ERR_INVALID_ARG   # dw
+    assert U.umem_gather_backward(*g, fake + 4, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_gather_backward(*g, fake, fake, fake, fake, 16, 0) == U.UMEM_ERR_WORKSPACE
+    g4 = list(g)
+    g4[9] = 4                                                          # expand without perm
+    assert U.umem_gather_backward(*g4, fake, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG
+    d = desc(grid=1, rank=2)
+    st, ns = U.umem_score_backward_workspace_size(d, 32)
+    assert st == U.UMEM_OK and ns > 0
+    a = [d, 32, fake, fake, fake, fake, fake, fake, fake, fake]        # ... core, idx, w, dw
+    assert U.umem_score_backward(*a, fake, fake, fake, fake, None, fake, ns, 0) == U.UMEM_ERR_INVALID_ARG  # dcore
+    assert U.umem_score_backward(*a, fake, fake, fake + 4, fake, fake, fake, ns, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_score_backward(*a, fake, fake, fake, fake, fake, fake, 64, 0) == U.UMEM_ERR_WORKSPACE
+    da = desc()
+    a = [da, 32, fake, fake, fake, fake, None, fake, None, fake]
+    assert U.umem_score_backward(*a, fake, fake, fake, fake, fake, fake, ns, 0) == U.UMEM_ERR_INVALID_ARG  # dcore, additive
+    ds = desc(weight=1)
+    a = [ds, 32, fake, fake, fake, fake, None, fake, None, fake]        # SoftMax needs w
+    assert U.umem_score_backward(*a, fake, fake, fake, fake, None, fake, ns, 0) == U.UMEM_ERR_INVALID_ARG
+    assert U.umem_score_backward_workspace_size(desc(heads=64, topm=32), 1 << 11)[0] == U.UMEM_ERR_UNSUPPORTED

@@ -1,0 +1,205 @@
+"""GPU parity of the backward (value-row and weight gradients; query, key and core gradients)
+through the C ABI, against the backward oracle on the same seeded inputs and the GPU forward's
+own selection."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():     # collected on CPU hosts too; every test here is gpu-marked
+    pytest.skip("no GPU", allow_module_level=True)
+
+import oracle.backward_oracle as B                  # noqa: E402
+import oracle.umem_oracle as O                      # noqa: E402
+import paper_2411_12364_amd as U                    # noqa: E402
+import synth as S                                   # noqa: E402
+from synth import configs as CF                     # noqa: E402
+from synth import device as SD                      # noqa: E402
+from tests import gpu_util as G                     # noqa: E402
+
+RTOL = 1e-5          # fp32 sums of fp32 products against fp64
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def rel(got, ref):
+    ref = np.asarray(ref, np.float64)
+    return float(np.abs(np.asarray(got, np.float64) - ref).max() / max(np.abs(ref).max(), 1e-30))
+
+
+def run_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores, dp, dV):
+    st, nws = U.umem_gather_backward_workspace_size(T, bag)
+    U.check(st)
+    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
+    dw = torch.empty(w.shape, dtype=torch.float32, device="cuda")
+    U.check(U.umem_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores,
+                                   dp, dV, dw, ws, ws.numel()), "umem_gather_backward")
+    return dw
+
+
+@pytest.mark.parametrize("dv,vdtype,expand,bag,T,cores,Np", [
+    (512, CF.BF16, 1, 64, 37, 1, 300),        # many repeated rows
+    (256, CF.F32, 1, 33, 20, 1, 5000),        # few repeats
+    (512, CF.BF16, 4, 96, 25, 2, 200),        # IVE blocks, two cores
+    (4096, CF.BF16, 4, 84, 9, 2, 500),        # 8 KiB rows (eight row chunks)
+    (64, CF.BF16, 1, 40, 50, 4, 60),          # rows narrower than a wave's chunk, four cores
+    (1024, CF.F32, 1, 7, 3, 8, 50000),        # eight cores of fp32 slices
+])
+def test_gather_backward(dv, vdtype, expand, bag, T, cores, Np):
+    rng = np.random.default_rng(dv + bag + T + cores)
+    log(f"[case] gather backward dv={dv} E={expand} bag={bag} T={T} cores={cores} Np={Np}")
+    torch_dt = torch.float32 if vdtype == CF.F32 else torch.bfloat16
+    rows_used = min(Np, 4096)
+    V = torch.randn((Np, dv), dtype=torch.float32, device="cuda").to(torch_dt)
+    idx = rng.integers(0, rows_used * expand, size=(T, bag)).astype(np.int32)
+    perm = None
+    if expand > 1:
+        perm = rng.permutation(Np * expand).astype(np.int32)
+        # map the chosen virtual slots onto rows_used physical rows only, to force repeats
+        perm = (perm % (rows_used * expand)).astype(np.int32) if Np > rows_used else perm
+    w = rng.standard_normal((T, bag) + ((cores,) if cores > 1 else ())).astype(np.float32)
+    dp = rng.standard_normal((T, expand, dv)).astype(np.float32)
+    dV0 = torch.randn((Np, dv), dtype=torch.float32, device="cuda")
+    dV = dV0.clone()
+    dw = run_gather_backward(Np, dv, vdtype, V, T, bag, torch.from_numpy(idx).cuda(),
+                             torch.from_numpy(w).cuda(),
+                             None if perm is None else torch.from_numpy(perm).cuda(), expand, cores,
+                             torch.from_numpy(dp).cuda(), dV)
+    torch.cuda.synchronize()
+    Vh = V.float().cpu().numpy()
+    rows, dV_ref, dw_ref = B.gather_backward(lambda r: Vh[r], idx, w, dp, perm, Np, expand)
+    got = (dV - dV0).cpu().numpy()
+    e_dw = rel(dw.cpu().numpy(), dw_ref)
+    e_dv = rel(got[rows], dV_ref)
+    untouched = np.setdiff1d(np.arange(Np), rows)
+    assert np.array_equal(dV.cpu().numpy()[untouched], dV0.cpu().numpy()[untouched])
+    log(f"[report] gather backward dv={dv} E={expand} cores={cores}: {len(rows)} rows, "
+        f"dw err {e_dw:.2e}, dV err {e_dv:.2e}")
+    assert e_dw <= RTOL and e_dv <= RTOL
+
+
+def test_gather_backward_deterministic():
+    cfg = CF.C5.with_tokens(512)
+    dl = SD.make_layer(cfg)
+    idx, w, _ = G.score_topk(dl, cfg.T, 0)
+    dp = torch.randn((cfg.T, cfg.expand, cfg.dv), dtype=torch.float32, device="cuda")
+    outs = []
+    for _ in range(2):
+        dV = torch.zeros((cfg.n_values, cfg.dv), dtype=torch.float32, device="cuda")
+        dw = run_gather_backward(cfg.n_values, cfg.dv, cfg.vdtype, dl.values, cfg.T, cfg.bag,
+                                 idx.reshape(cfg.T, cfg.bag), w.reshape(cfg.T, cfg.bag), dl.perm,
+                                 cfg.expand, 1, dp, dV)
+        torch.cuda.synchronize()
+        outs.append((dV, dw))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
+def test_gather_backward_tucker_ive_sampled():
+    """The 4M-slot Tucker + IVE layer's 4096-token batch (clustered queries: rows shared by many
+    tokens), on sampled rows: the oracle gets exactly the entries on those rows."""
+    cfg = CF.C5
+    dl = SD.make_layer(cfg)
+    idx, w, _ = G.score_topk(dl, cfg.T, 0)
+    rng = np.random.default_rng(5)
+    dp = torch.from_numpy(rng.standard_normal((cfg.T, cfg.expand, cfg.dv)).astype(np.float32)).cuda()
+    dV = torch.zeros((cfg.n_values, cfg.dv), dtype=torch.float32, device="cuda")
+    idx2, w2 = idx.reshape(cfg.T, cfg.bag), w.reshape(cfg.T, cfg.bag)
+    dw = run_gather_backward(cfg.n_values, cfg.dv, cfg.vdtype, dl.values, cfg.T, cfg.bag, idx2, w2,
+                             dl.perm, cfg.expand, 1, dp, dV)
+    torch.cuda.synchronize()
+    idx_h, w_h, dp_h = G.host(idx2).astype(np.int64), G.host(w2), dp.cpu().numpy()
+    perm = CF.perm(cfg)
+    _, row = O.address_map(idx_h, perm, cfg.n_values, cfg.expand)
+    sample = np.unique(row)[rng.choice(len(np.unique(row)), 24, replace=False)]
+    sel = np.argwhere(np.isin(row, sample))                  # (t, b) entries on sampled rows, in order
+    sub_idx = idx_h[sel[:, 0], sel[:, 1]][:, None]
+    sub_w = w_h[sel[:, 0], sel[:, 1]][:, None]
+    sub_dp = dp_h[sel[:, 0]]
+    vrows = G.value_rows_fn(cfg)
+    rows, dV_ref, dw_ref = B.gather_backward(vrows, sub_idx, sub_w, sub_dp, perm, cfg.n_values, cfg.expand)
+    e_dv = rel(dV[torch.from_numpy(rows).cuda()].cpu().numpy(), dV_ref)
+    e_dw = rel(G.host(dw)[sel[:, 0], sel[:, 1]], dw_ref[:, 0])
+    log(f"[report] tucker-ive-4M gather backward: {len(sel)} entries on 24 sampled rows, "
+        f"dV err {e_dv:.2e}, dw err {e_dw:.2e}")
+    assert e_dv <= RTOL and e_dw <= RTOL
+
+
+# ---------------------------------------------------------------- score backward
+
+SCORE_CASES = [
+    CF.Layer("add-raw", T=24, heads=2, dk=64, n_keys=80, topk=12, topm=20, dv=8, vdtype=CF.F32, seed=51),
+    CF.Layer("add-softmax", T=16, heads=1, dk=32, n_keys=50, topk=8, topm=16, dv=8, vdtype=CF.F32,
+             seed=52, weight=CF.W_SOFTMAX),
+    CF.Layer("tucker", T=20, heads=3, dk=64, n_keys=70, topk=10, topm=24, dv=8, vdtype=CF.F32, seed=53,
+             rank=2, grid=CF.GRID_TUCKER),
+    CF.Layer("tucker-mcs", T=18, heads=2, dk=128, n_keys=64, topk=16, topm=32, dv=8, vdtype=CF.F32,
+             seed=54, rank=2, grid=CF.GRID_TUCKER, cores=2),
+    CF.Layer("tucker-r4-wide", T=256, heads=2, dk=128, n_keys=512, topk=32, topm=64, dv=8,
+             vdtype=CF.F32, seed=55, rank=4, grid=CF.GRID_TUCKER),
+]
+
+
+def run_score_backward(cfg, dl, idx, w, dw, dk_init=None, dc_init=None):
+    d = G.desc_for(cfg)
+    st, nws = U.umem_score_backward_workspace_size(d, cfg.T)
+    U.check(st)
+    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
+    dq_row = torch.empty_like(dl.q_row[0])
+    dq_col = torch.empty_like(dl.q_col[0])
+    dk_row = torch.zeros_like(dl.k_row) if dk_init is None else dk_init[0].clone()
+    dk_col = torch.zeros_like(dl.k_col) if dk_init is None else dk_init[1].clone()
+    dcore = None
+    if cfg.grid == CF.GRID_TUCKER:
+        dcore = torch.zeros_like(dl.core) if dc_init is None else dc_init.clone()
+    U.check(U.umem_score_backward(d, cfg.T, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core,
+                                  idx, w, dw, dq_row, dq_col, dk_row, dk_col, dcore, ws, ws.numel()),
+            "umem_score_backward")
+    return dq_row, dq_col, dk_row, dk_col, dcore
+
+
+@pytest.mark.parametrize("cfg", SCORE_CASES, ids=[c.name for c in SCORE_CASES])
+def test_score_backward(cfg):
+    log(f"[case] score backward {cfg.name}")
+    dl = SD.make_layer(cfg)
+    idx, w, _ = G.score_topk(dl, cfg.T, 0)
+    rng = np.random.default_rng(cfg.seed)
+    dw_h = rng.standard_normal(tuple(w.shape)).astype(np.float32)
+    dk0 = (torch.randn_like(dl.k_row), torch.randn_like(dl.k_col))
+    dc0 = None if dl.core is None else torch.randn_like(dl.core)
+    dq_row, dq_col, dk_row, dk_col, dcore = run_score_backward(
+        cfg, dl, idx, w, torch.from_numpy(dw_h).cuda(), dk0, dc0)
+    torch.cuda.synchronize()
+    qr, qc = CF.queries(cfg)
+    kr, kc = CF.keys(cfg)
+    core = CF.core(cfg)
+    res = B.score_backward(qr, qc, kr, kc, G.host(idx), dw_h, G.host(w), cfg.grid, cfg.weight,
+                           None if cfg.cores > 1 else core, cfg.rank,
+                           core if cfg.cores > 1 else None)
+    errs = dict(dq_row=rel(G.host(dq_row), res["dq_row"]), dq_col=rel(G.host(dq_col), res["dq_col"]),
+                dk_row=rel(G.host(dk_row) - G.host(dk0[0]), res["dK_row"]),
+                dk_col=rel(G.host(dk_col) - G.host(dk0[1]), res["dK_col"]))
+    if dcore is not None:
+        errs["dcore"] = rel(G.host(dcore) - G.host(dc0), res["dC"])
+    log(f"[report] score backward {cfg.name}: {errs}")
+    assert max(errs.values()) <= RTOL, errs
+
+
+def test_score_backward_deterministic():
+    cfg = SCORE_CASES[-1]
+    dl = SD.make_layer(cfg)
+    idx, w, _ = G.score_topk(dl, cfg.T, 0)
+    dw = torch.randn_like(w)
+    a = run_score_backward(cfg, dl, idx, w, dw)
+    b = run_score_backward(cfg, dl, idx, w, dw)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
