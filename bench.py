@@ -10,8 +10,9 @@ Prints one JSON line.  Besides the headline it carries the roofline of the domin
 (the average duration of its launches replayed back to back from a HIP graph, between two HIP
 events on the launch stream), the value-gather bandwidth, a decode batch sweep, the forwards of the 1M-slot prefill layer, of the
 4M-slot Tucker + IVE layer (with one and with two component cores) and of one memory layer of the
-paper's UltraMem-1.6B-x12 model, each with the roofline of every kernel it launches, and the CPU
-oracle's throughput on a bounded sample.  The timed steps are replayed from a captured HIP graph
+paper's UltraMem-1.6B-x12 model, each with the roofline of every kernel it launches and the time
+of its backward (value-row, weight, query, key and core gradients), and the CPU oracle's
+throughput on a bounded sample.  The timed steps are replayed from a captured HIP graph
 (--eager launches them one by one from Python instead).
 """
 from __future__ import annotations
@@ -345,6 +346,7 @@ def workload_report(cfg, steps=50, warmup=5):
                gather_unique_row_bytes=int(uniq),
                gather_unique_GBps=round(uniq / (st["gather_kernel"] * 1e-6) / 1e9, 1),
                gather_logical_GBps=round(g["row_bytes"] / (st["gather_kernel"] * 1e-6) / 1e9, 1))
+    rep["backward"] = backward_report(r)
     fe = front_ends().get(cfg.name)
     if fe is not None:
         rep["front_end"] = front_end_report(fe)
@@ -411,6 +413,54 @@ def front_end_report(fe, launches=200):
                gemm_TFLOPs=round(flops / (us * 1e-6) / 1e12, 2))
     log(f"front end {fe.name}: {rep}")
     return rep
+
+
+def backward_report(r, launches=20):
+    """The backward of one step of runner ``r``'s layer at its forward's selection: the gather
+    backward (value-row and weight gradients) and the score backward (query, key and core
+    gradients), each replayed ``launches`` times from a HIP graph."""
+    torch, U, dl, c = r.torch, r.U, r.dl, r.cfg
+    r.forward(0)
+    T = c.T
+    idx, w = r.idx.reshape(T, c.bag), r.w.reshape((T, c.bag) + tuple(r.w.shape[3:]))
+    dp = torch.randn((T, c.expand, c.dv), dtype=torch.float32, device="cuda")
+    dV = torch.zeros((c.n_values, c.dv), dtype=torch.float32, device="cuda")
+    dw = torch.empty_like(w)
+    st, n1 = U.umem_gather_backward_workspace_size(T, c.bag, c.dv)
+    U.check(st)
+    ws1 = torch.empty(max(n1, 256), dtype=torch.uint8, device="cuda")
+    st, n2 = U.umem_score_backward_workspace_size(r.desc, T)
+    U.check(st)
+    ws2 = torch.empty(max(n2, 256), dtype=torch.uint8, device="cuda")
+    dq_r, dq_c = torch.empty_like(dl.q_row[0]), torch.empty_like(dl.q_col[0])
+    dk_r, dk_c = torch.zeros_like(dl.k_row), torch.zeros_like(dl.k_col)
+    dcore = None if dl.core is None else torch.zeros_like(dl.core)
+
+    def gb():
+        st = U.umem_gather_backward(c.n_values, c.dv, c.vdtype, dl.values, T, c.bag, idx, w, dl.perm,
+                                    c.expand, c.cores, dp, dV, dw, ws1, ws1.numel())
+        if st:
+            U.check(st, "umem_gather_backward")
+
+    def sb():
+        st = U.umem_score_backward(r.desc, T, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core,
+                                   r.idx, r.w, dw.reshape(r.w.shape), dq_r, dq_c, dk_r, dk_c, dcore,
+                                   ws2, ws2.numel())
+        if st:
+            U.check(st, "umem_score_backward")
+    g_us = r._graph_time([gb] * launches) * 1e6
+    s_us = r._graph_time([sb] * launches) * 1e6
+    uniq = r.unique_rows
+    algo = int(uniq * c.dv * (c.vbytes + 8) + T * c.expand * c.dv * 4 + T * c.bag * 4 * (2 + c.cores))
+    achieved = algo / (g_us * 1e-6) / 1e9
+    out = dict(gather_backward_us=round(g_us, 3), score_backward_us=round(s_us, 3),
+               tokens_per_s=round(T / ((g_us + s_us) * 1e-6), 1),
+               gather_backward_roofline=dict(kernel="gather_backward", bound="hbm",
+                                             achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                                             frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
+                                             avg_us=round(g_us, 3), algorithmic_bytes=algo))
+    del dV, ws1, ws2
+    return out
 
 
 def front_ends():

@@ -198,10 +198,11 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
  *   d_values  fp32 [n_values, dv], 16-byte aligned: accumulated into (only the rows the bag
  *             touches change; clear it between steps as the optimiser needs)
  *   dw        fp32 [T, bag] or [T, bag, cores]
- *   ws        16-byte aligned scratch of umem_gather_backward_workspace_size(T, bag) bytes
- * Entries on one row are summed in their bag order by one writer, so the result does not depend
- * on timing.  T * bag <= 2^22 (UMEM_ERR_UNSUPPORTED beyond). */
-UMEM_API umem_status umem_gather_backward_workspace_size(int32_t T, int32_t bag, size_t* bytes);
+ *   ws        16-byte aligned scratch of umem_gather_backward_workspace_size(T, bag, dv) bytes
+ * Entries on one row are summed in a fixed order (in segments of their bag order, then the
+ * segments in order), so the result does not depend on timing.  T * bag <= 2^22
+ * (UMEM_ERR_UNSUPPORTED beyond). */
+UMEM_API umem_status umem_gather_backward_workspace_size(int32_t T, int32_t bag, int32_t dv, size_t* bytes);
 UMEM_API umem_status umem_gather_backward(int64_t n_values, int32_t dv, int32_t vdtype, const void* values,
                                  int32_t T, int32_t bag, const int32_t* idx, const float* w,
                                  const int32_t* perm, int32_t expand, int32_t cores,

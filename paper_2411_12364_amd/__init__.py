@@ -78,7 +78,7 @@ def _load() -> ctypes.CDLL:
         "umem_query_workspace_size": [ctypes.POINTER(umem_query_desc), I32, I32, ctypes.POINTER(SZ)],
         "umem_query": [ctypes.POINTER(umem_query_desc), I32, I32, P, P, P, P, P, P, P, P, P, SZ, P],
         "umem_key_norm": [I32, I32, I32, P, P, P, ctypes.c_float, P, P],
-        "umem_gather_backward_workspace_size": [I32, I32, ctypes.POINTER(SZ)],
+        "umem_gather_backward_workspace_size": [I32, I32, I32, ctypes.POINTER(SZ)],
         "umem_gather_backward": [I64, I32, I32, P, I32, I32, P, P, P, I32, I32, P, P, P, P, SZ, P],
         "umem_score_backward_workspace_size": [D, I32, ctypes.POINTER(SZ)],
         "umem_score_backward": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
@@ -198,10 +198,10 @@ def umem_key_norm(heads, n, dk, keys, gamma, beta, eps, out, stream=None) -> int
     return _lib.umem_key_norm(heads, n, dk, _p(keys), _p(gamma), _p(beta), eps, _p(out), _s(stream))
 
 
-def umem_gather_backward_workspace_size(T, bag):
+def umem_gather_backward_workspace_size(T, bag, dv):
     """Returns (status, bytes)."""
     out = ctypes.c_size_t(0)
-    st = _lib.umem_gather_backward_workspace_size(T, bag, ctypes.byref(out))
+    st = _lib.umem_gather_backward_workspace_size(T, bag, dv, ctypes.byref(out))
     return st, out.value
 
 

@@ -10,14 +10,15 @@
 // adds the accumulator into dV[row].  Every row has one writer and a fixed summation order: the
 // result does not depend on timing, and no atomics are needed.
 //
-// Backward of the scores (eqs. (2)-(4), (10), (16)) with the selection held fixed: one
-// workgroup per (token, head) turns the weight gradients into grid-score gradients (SoftMax
-// Jacobian where eq. (3)'s SoftMax weights), recomputes the selected slots' per-slice scores
-// (Tucker), forms each slot's contribution to dS_row / dS_col and to dC, adds the contributions
-// of slots that share a row (or column) in slot order, and writes dq = sum_i dS[i] K[i].  The key
+// Backward of the scores (eqs. (2)-(4), (10), (16)) with the selection held fixed: one wave
+// per (token, head) turns the weight gradients into grid-score gradients (SoftMax Jacobian where
+// eq. (3)'s SoftMax weights), finds the distinct rows and columns of its slots (ballots over the
+// key bits), recomputes their per-slice scores (Tucker), forms each slot's contribution to
+// dS_row / dS_col and to dC, adds the contributions of slots that share a row (or column) in
+// slot order, and writes dq = sum_i dS[i] K[i].  The key
 // gradients dK[i] += dS[i] q are sums over tokens: each (token, head, axis) emits one entry per
 // distinct key, the entries are stably sorted by key, and one wave per key sums them in order.
-// dC sums its per-token partials in a fixed order (chunks of tokens, then the chunks).
+// dC sums its per-token partials in a fixed order (per thread, then a tree over the threads).
 #include <algorithm>
 
 #include "umem_internal.h"
@@ -73,344 +74,635 @@ struct Chunk<uint16_t> {   // bf16 bit patterns
   }
 };
 
+// The run [i, end) of sorted entries that starts at sorted position i (wave-uniform).
+__device__ __forceinline__ int run_end(const uint32_t* __restrict__ keys, int i, int M, uint32_t key) {
+  const int lane = threadIdx.x & (kWave - 1);
+  for (int base = i + 1; base < M; base += kWave) {
+    const int pos = base + lane;
+    const uint64_t same = __ballot(pos < M && keys[pos] == key);
+    if (same != ~0ull) return base + __builtin_ctzll(~same);
+  }
+  return M;
+}
+
+// The sorted entries are cut into pieces at the starts of runs and at every kSeg-th position, and
+// each piece is one wave's work, so that a row chosen by thousands of tokens does not leave one
+// wave walking them all while a row chosen once still gets a wave of its own.  The piece starts
+// are listed first (counted per chunk, the counts scanned, then written in order), and a fixed
+// grid of waves walks the list.  A piece that is a
+// whole run adds its sum into its row; a piece cut by a segment edge (segment g = positions
+// [g kSeg, (g + 1) kSeg)) stores its partial row: slot 2 g + 1 for the last piece of segment g
+// when it starts its run, slot 2 g for the first piece of segment g when it continues one.  A
+// second pass adds, for each run spanning segments, its head piece and then the first piece of
+// each later segment, in that order.
+constexpr int kSeg = kWave;
+
+// The piece starting at sorted position i, if one does ([i, *pe), with whether it starts and
+// ends its run); false for positions inside a piece.  Wave-uniform.
+__device__ __forceinline__ bool piece_at(const uint32_t* __restrict__ keys, int i, int M,
+                                         uint32_t key, int* pe, bool* run_start, bool* run_end) {
+  const int lane = threadIdx.x & (kWave - 1);
+  *run_start = i == 0 || keys[i - 1] != key;
+  if (!*run_start && i % kSeg != 0) return false;
+  const int seg_end = min(M, (i / kSeg + 1) * kSeg);
+  const int pos = i + 1 + lane;
+  const uint64_t diff = __ballot(pos < seg_end && keys[pos] != key);
+  *pe = diff != 0ull ? i + 1 + __builtin_ctzll(diff) : seg_end;
+  *run_end = *pe == M || keys[*pe] != key;
+  return true;
+}
+
+constexpr int kListWaves = 8192;        // waves of the grids that walk the lists
+constexpr int kInFlight = 4;            // a piece's entries whose loads are issued together
+
+constexpr int kListPer = 16;                           // positions per thread
+constexpr int kListChunk = THREADS * kListPer;          // positions per workgroup
+
+__device__ __forceinline__ bool is_piece_start(const uint32_t* __restrict__ keys, int i, int M,
+                                               uint32_t sentinel) {
+  if (i >= M) return false;
+  const uint32_t k = keys[i];
+  return k != sentinel && (i % kSeg == 0 || keys[i - 1] != k);
+}
+
+// Exclusive prefix of v over the workgroup's threads, in thread order (every thread calls it).
+__device__ __forceinline__ uint32_t block_prefix(uint32_t v, uint32_t* lds, uint32_t* total) {
+  const int tid = threadIdx.x;
+  lds[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < THREADS; off <<= 1) {
+    const uint32_t add = tid >= off ? lds[tid - off] : 0u;
+    __syncthreads();
+    lds[tid] += add;
+    __syncthreads();
+  }
+  const uint32_t incl = lds[tid];
+  *total = lds[THREADS - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ __launch_bounds__(THREADS) void piece_count_kernel(const uint32_t* __restrict__ keys,
+                                                              int M, uint32_t sentinel,
+                                                              uint32_t* __restrict__ offs) {
+  __shared__ uint32_t lds[THREADS];
+  const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
+  uint32_t c = 0;
+  for (int k = 0; k < kListPer; ++k) c += is_piece_start(keys, beg + k, M, sentinel);
+  uint32_t total;
+  block_prefix(c, lds, &total);
+  if (threadIdx.x == 0) offs[blockIdx.x] = total;
+}
+
+// offs: the chunks' exclusive offsets; the last chunk also stores the number of pieces.
+__global__ __launch_bounds__(THREADS) void piece_write_kernel(const uint32_t* __restrict__ keys,
+                                                              int M, uint32_t sentinel,
+                                                              const uint32_t* __restrict__ offs,
+                                                              uint32_t* __restrict__ list,
+                                                              uint32_t* __restrict__ counts) {
+  __shared__ uint32_t lds[THREADS];
+  const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
+  uint32_t c = 0;
+  for (int k = 0; k < kListPer; ++k) c += is_piece_start(keys, beg + k, M, sentinel);
+  uint32_t total;
+  uint32_t at = offs[blockIdx.x] + block_prefix(c, lds, &total);
+  for (int k = 0; k < kListPer; ++k)
+    if (is_piece_start(keys, beg + k, M, sentinel)) list[at++] = static_cast<uint32_t>(beg + k);
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+    counts[0] = offs[blockIdx.x] + total;
+    counts[1] = 0u;                                       // the spanning runs, appended later
+  }
+}
+
+size_t list_workspace_bytes(int M) {
+  const size_t chunks = (static_cast<size_t>(M) + kListChunk - 1) / kListChunk;
+  return (chunks + 1) * sizeof(uint32_t) + scan_workspace_bytes(static_cast<int>(chunks)) + 64;
+}
+
+// The piece starts of the sorted keys into list (in order) and their number into counts[0];
+// counts[1] cleared.  ws: list_workspace_bytes(M).
+hipError_t list_pieces(const uint32_t* keys, int M, uint32_t sentinel, uint32_t* list,
+                       uint32_t* counts, void* ws, hipStream_t s) {
+  const int chunks = (M + kListChunk - 1) / kListChunk;
+  uint32_t* offs = static_cast<uint32_t*>(ws);
+  uint32_t* sums = offs + chunks + 1;
+  hipLaunchKernelGGL(piece_count_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, sentinel, offs);
+  hipError_t e = scan_exclusive(offs, chunks, sums, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(piece_write_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, sentinel, offs,
+                     list, counts);
+  return hipGetLastError();
+}
+
 template <typename Elem>
-__global__ __launch_bounds__(THREADS) void gather_bwd_run_kernel(
+__global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
     const uint32_t* __restrict__ rows, const uint32_t* __restrict__ ents, int M,
     const Elem* __restrict__ values, int dv, const int32_t* __restrict__ idx,
     const float* __restrict__ w, const int32_t* __restrict__ perm, int64_t n_values, int expand,
     int cores, int bag, const float* __restrict__ d_pooled, float* __restrict__ d_values,
-    float* __restrict__ dw) {
+    float* __restrict__ dw, float* __restrict__ partial, const uint32_t* __restrict__ list,
+    uint32_t* __restrict__ counts, uint32_t* __restrict__ heads) {
   constexpr int EPC = Chunk<Elem>::kElems;            // elements per 16-byte piece
   const int lane = threadIdx.x & (kWave - 1);
-  const int i = blockIdx.x * NWAVES + static_cast<int>(threadIdx.x) / kWave;
-  if (i >= M) return;                                 // whole waves: no barrier in this kernel
-  const uint32_t row = rows[i];
-  if (i > 0 && rows[i - 1] == row) return;            // not the first entry of its run
-  int end = i + 1;                                    // the run is [i, end)
-  for (int base = i + 1; base < M; base += kWave) {
-    const int pos = base + lane;
-    const uint64_t same = __ballot(pos < M && rows[pos] == row);
-    if (same != ~0ull) {
-      end = base + __builtin_ctzll(~same);
-      break;
-    }
-    end = min(M, base + kWave);
-  }
+  const uint32_t n_pieces = counts[0];
+  for (uint32_t k = blockIdx.x * NWAVES + threadIdx.x / kWave; k < n_pieces;
+       k += gridDim.x * NWAVES) {                     // wave-uniform: no barrier in this kernel
+  const int ps = static_cast<int>(list[k]);
+  const uint32_t row = rows[ps];
+  int pe;
+  bool run_start, run_end;
+  piece_at(rows, ps, M, row, &pe, &run_start, &run_end);
+  if (run_start && !run_end && lane == 0)            // a run spanning segments: list its head
+    heads[atomicAdd(counts + 1, 1u)] = static_cast<uint32_t>(ps);
+  const int g = ps / kSeg;
   const int slice_w = dv / cores;
+  // the piece's entries, one per lane: entry number and the d_pooled row (token, virtual block)
+  const int n_e = pe - ps;
+  int my_ent = 0, my_prow = 0;
+  if (lane < n_e) {
+    my_ent = static_cast<int>(ents[ps + lane]);
+    const int p = perm != nullptr ? static_cast<int>(perm[idx[my_ent]] / n_values) : 0;
+    my_prow = (my_ent / bag) * expand + p;
+  }
   const Elem* vrow = values + static_cast<size_t>(row) * dv;
-  float* grow = d_values + static_cast<size_t>(row) * dv;
   for (int c0 = 0; c0 < dv; c0 += kWave * EPC) {
     const int col = c0 + lane * EPC;
     const bool active = col < dv;
     const int sl = active ? col / slice_w : 0;        // a piece lies in one column slice
-    float x[EPC];
-    if (active) {
-      Chunk<Elem>::load(vrow + col, x);
-    } else {
+    float x[EPC], acc[EPC];
 #pragma unroll
-      for (int k = 0; k < EPC; ++k) x[k] = 0.0f;
+    for (int k = 0; k < EPC; ++k) {
+      x[k] = 0.0f;
+      acc[k] = 0.0f;
     }
-    float acc[EPC];
+    if (active) Chunk<Elem>::load(vrow + col, x);
+    for (int j0 = 0; j0 < n_e; j0 += kInFlight) {    // wave-uniform
+      int ent[kInFlight];
+      float wt[kInFlight];
+      f32x4 v[kInFlight][EPC / 4];
 #pragma unroll
-    for (int k = 0; k < EPC; ++k) acc[k] = 0.0f;
-    for (int e = i; e < end; ++e) {
-      const int ent = static_cast<int>(ents[e]);
-      const int t = ent / bag;
-      const int p = perm != nullptr ? static_cast<int>(perm[idx[ent]] / n_values) : 0;
-      float g[EPC];
-      float dot = 0.0f;
-      if (active) {
-        const float* src = d_pooled + (static_cast<size_t>(t) * expand + p) * dv + col;
+      for (int u = 0; u < kInFlight; ++u) {          // all loads first
+        const int j = min(j0 + u, n_e - 1);
+        ent[u] = __builtin_amdgcn_readlane(my_ent, j);
+        const int prow = __builtin_amdgcn_readlane(my_prow, j);
+        wt[u] = 0.0f;
+#pragma unroll
+        for (int k = 0; k < EPC / 4; ++k) v[u][k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (active) {
+          wt[u] = w[static_cast<size_t>(ent[u]) * cores + sl];
+          const f32x4* src = reinterpret_cast<const f32x4*>(d_pooled + static_cast<size_t>(prow) * dv + col);
+#pragma unroll
+          for (int k = 0; k < EPC / 4; ++k) v[u][k] = src[k];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kInFlight; ++u) {          // then the entries in order
+        if (j0 + u >= n_e) break;
+        float dot = 0.0f;
 #pragma unroll
         for (int k = 0; k < EPC; k += 4) {
-          const f32x4 v = *reinterpret_cast<const f32x4*>(src + k);
-          g[k] = v.x; g[k + 1] = v.y; g[k + 2] = v.z; g[k + 3] = v.w;
+          const f32x4 vv = v[u][k / 4];
+          dot = fmaf(vv.x, x[k], dot);
+          dot = fmaf(vv.y, x[k + 1], dot);
+          dot = fmaf(vv.z, x[k + 2], dot);
+          dot = fmaf(vv.w, x[k + 3], dot);
+          acc[k] = fmaf(wt[u], vv.x, acc[k]);
+          acc[k + 1] = fmaf(wt[u], vv.y, acc[k + 1]);
+          acc[k + 2] = fmaf(wt[u], vv.z, acc[k + 2]);
+          acc[k + 3] = fmaf(wt[u], vv.w, acc[k + 3]);
         }
-#pragma unroll
-        for (int k = 0; k < EPC; ++k) dot = fmaf(g[k], x[k], dot);
-      } else {
-#pragma unroll
-        for (int k = 0; k < EPC; ++k) g[k] = 0.0f;
-      }
-      const float wt = active ? w[static_cast<size_t>(ent) * cores + sl] : 0.0f;
-#pragma unroll
-      for (int k = 0; k < EPC; ++k) acc[k] = fmaf(wt, g[k], acc[k]);
-      for (int c = 0; c < cores; ++c) {
-        const float s = wave_sum(sl == c ? dot : 0.0f);
-        if (lane == 0) {
-          float* d = dw + static_cast<size_t>(ent) * cores + c;
-          *d = c0 == 0 ? s : *d + s;                  // this wave is the entry's only writer
+        for (int c = 0; c < cores; ++c) {
+          const float sc = wave_sum(sl == c ? dot : 0.0f);
+          if (lane == 0) {
+            float* d = dw + static_cast<size_t>(ent[u]) * cores + c;
+            *d = c0 == 0 ? sc : *d + sc;              // this wave is the entry's only writer
+          }
         }
       }
     }
-    if (active) {
+    if (!active) continue;
+    if (run_start && run_end) {                       // a whole run: add into its row
 #pragma unroll
       for (int k = 0; k < EPC; k += 4) {
-        f32x4* dst = reinterpret_cast<f32x4*>(grow + col + k);
+        f32x4* dst = reinterpret_cast<f32x4*>(d_values + static_cast<size_t>(row) * dv + col + k);
         f32x4 v = *dst;
         v.x += acc[k]; v.y += acc[k + 1]; v.z += acc[k + 2]; v.w += acc[k + 3];
         *dst = v;
       }
+    } else {                                          // cut by a segment edge: its partial row
+      float* dst = partial + (static_cast<size_t>(2) * g + (run_start ? 1 : 0)) * dv + col;
+#pragma unroll
+      for (int k = 0; k < EPC; k += 4)
+        *reinterpret_cast<f32x4*>(dst + k) = f32x4{acc[k], acc[k + 1], acc[k + 2], acc[k + 3]};
     }
+  }
+  }
+}
+
+// One wave per run that spans segments: its partial rows, in segment order, added into the row.
+__global__ __launch_bounds__(THREADS) void seg_join_kernel(const uint32_t* __restrict__ keys, int M,
+                                                           int width, const float* __restrict__ partial,
+                                                           float* __restrict__ out,
+                                                           const uint32_t* __restrict__ heads,
+                                                           const uint32_t* __restrict__ counts,
+                                                           int H, int n, float* __restrict__ out2) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t n_heads = counts[1];
+  for (uint32_t hk = blockIdx.x * NWAVES + threadIdx.x / kWave; hk < n_heads;
+       hk += gridDim.x * NWAVES) {
+  const int i = static_cast<int>(heads[hk]);
+  const uint32_t key = keys[i];
+  const int g0 = i / kSeg;
+  const int end = run_end(keys, i, M, key);
+  const int g1 = (end - 1) / kSeg;
+  // the row of this key: value rows directly, or (out2 given) key rows of the two axes
+  float* dst;
+  if (out2 == nullptr) {
+    dst = out + static_cast<size_t>(key) * width;
+  } else {
+    const int axis = static_cast<int>(key / (static_cast<uint32_t>(H) * n));
+    dst = (axis ? out2 : out) + static_cast<size_t>(key - static_cast<uint32_t>(axis) * H * n) * width;
+  }
+  for (int c = lane * 4; c < width; c += kWave * 4) {
+    f32x4 acc = *reinterpret_cast<const f32x4*>(partial + (static_cast<size_t>(2) * g0 + 1) * width + c);
+    for (int g = g0 + 1; g <= g1; ++g)
+      acc += *reinterpret_cast<const f32x4*>(partial + static_cast<size_t>(2) * g * width + c);
+    f32x4* d = reinterpret_cast<f32x4*>(dst + c);
+    f32x4 v = *d;
+    v += acc;
+    *d = v;
+  }
   }
 }
 
 // ---------------------------------------------------------------- score backward
 
-constexpr int kDcChunk = 256;          // tokens per first-level dC partial sum
-
-struct ScoreBwdShared {
-  int ii[kMaxTopM], jj[kMaxTopM];                  // row, column of each selected slot
-  float dg[kMaxTopM * kMaxCores];                  // grid-score gradient per slot (and core)
-  float srow[kMaxTopM][kMaxRank], scol[kMaxTopM][kMaxRank];   // the slots' per-slice scores
-  float cr[kMaxTopM][kMaxRank], cc[kMaxTopM][kMaxRank];       // a slot's dS_row, dS_col terms
-  int lead_r[kMaxTopM], lead_c[kMaxTopM];          // first slot with the same row / column
-  int dist_r[kMaxTopM], dist_c[kMaxTopM];          // distinct rows / columns, in slot order
-  int pos_r[kMaxTopM], pos_c[kMaxTopM];            // a leader's place in that list
-  float dsr[kMaxTopM][kMaxRank], dsc[kMaxTopM][kMaxRank];     // dS per distinct row / column
-  float core[kMaxCores][kMaxRank * kMaxRank];
-  float red[THREADS];
-  int nr, nc;
+// One wave per (token, head); slot s = g * 64 + lane for the NG groups g of a lane.  The waves
+// of a workgroup share nothing, so the kernel has no workgroup barrier; each wave's own LDS
+// traffic is ordered by wave_sync.
+template <int NG>
+struct ScoreBwdLds {
+  int dist[2][NG * kWave];                     // distinct rows / columns, in slot order
+  float sd[2][NG * kWave][kMaxRank];           // per distinct key: its per-slice score, then its dS
+  float cs[2][NG * kWave][kMaxRank];           // per slot: its dS_row / dS_col term
 };
 
-__global__ __launch_bounds__(THREADS) void score_bwd_kernel(
+template <int NG>
+constexpr int score_bwd_waves() { return NG >= 4 ? 2 : 4; }
+
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The lanes whose key_other (valid_other) equals this lane's key: one ballot per key bit.
+__device__ __forceinline__ uint64_t key_match(uint32_t key, uint32_t key_other, bool valid_other,
+                                              int bits) {
+  uint64_t mask = __ballot(valid_other);
+  for (int b = 0; b < bits; ++b) {
+    const uint64_t ones = __ballot(valid_other && ((key_other >> b) & 1u));
+    mask &= ((key >> b) & 1u) ? ones : ~ones;
+  }
+  return mask;
+}
+
+template <int NG>
+__global__ __launch_bounds__(score_bwd_waves<NG>() * kWave) void score_bwd_kernel(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
     const float* __restrict__ core_all, const int32_t* __restrict__ idx,
-    const float* __restrict__ w, const float* __restrict__ dw, int T, int H, int n, int dk,
-    int rank, int m, int tucker, int softmax, int hc, float* __restrict__ dq_row,
+    const float* __restrict__ w, const float* __restrict__ dw, int T, int H, int n, int key_bits,
+    int dk, int rank, int m, int tucker, int softmax, int hc, float* __restrict__ dq_row,
     float* __restrict__ dq_col, uint32_t* __restrict__ ekeys, uint32_t* __restrict__ evals,
     float* __restrict__ edS, float* __restrict__ dc_part) {
-  __shared__ ScoreBwdShared sh;
-  const int tid = threadIdx.x;
-  const int t = blockIdx.x / H, h = blockIdx.x % H;
-  const size_t th = static_cast<size_t>(t) * H + h;
-  for (int s = tid; s < m; s += THREADS) {
-    const int flat = idx[th * m + s];
-    sh.ii[s] = flat / n;
-    sh.jj[s] = flat % n;
+  constexpr int W = score_bwd_waves<NG>();
+  __shared__ ScoreBwdLds<NG> lds[W];
+  const int lane = threadIdx.x & (kWave - 1);
+  ScoreBwdLds<NG>& sh = lds[threadIdx.x / kWave];
+  const size_t th = static_cast<size_t>(blockIdx.x) * W + threadIdx.x / kWave;
+  if (th >= static_cast<size_t>(T) * H) return;      // wave-uniform
+  const int h = static_cast<int>(th % H);
+  const int R = tucker ? rank : 1;
+  bool valid[NG];
+  uint32_t key[2][NG];                                 // row, column of each slot
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int s = g * kWave + lane;
+    valid[g] = s < m;
+    const uint32_t flat = valid[g] ? static_cast<uint32_t>(idx[th * m + s]) : 0u;
+    key[0][g] = flat / static_cast<uint32_t>(n);
+    key[1][g] = flat % static_cast<uint32_t>(n);
   }
-  if (tucker)
-    for (int x = tid; x < hc * rank * rank; x += THREADS)
-      sh.core[x / (rank * rank)][x % (rank * rank)] =
-          core_all[static_cast<size_t>(h) * hc * rank * rank + x];
-  // ---- weight gradients -> grid-score gradients
+  // ---- weight gradients -> grid-score gradients (SoftMax Jacobian where eq. (3) weights)
+  float dg[NG][kMaxCores];
   if (softmax) {
     float p = 0.0f;
-    for (int s = tid; s < m; s += THREADS) p = fmaf(w[th * m + s], dw[th * m + s], p);
-    sh.red[tid] = p;
-    __syncthreads();
-    for (int off = THREADS / 2; off > 0; off >>= 1) {     // fixed-order tree
-      if (tid < off) sh.red[tid] += sh.red[tid + off];
-      __syncthreads();
+#pragma unroll
+    for (int g = 0; g < NG; ++g)
+      if (valid[g]) p = fmaf(w[th * m + g * kWave + lane], dw[th * m + g * kWave + lane], p);
+    const float wdot = wave_sum(p);                    // identical in every lane
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const size_t x = th * m + g * kWave + lane;
+      dg[g][0] = valid[g] ? w[x] * (dw[x] - wdot) : 0.0f;
     }
-    const float wdot = sh.red[0];
-    for (int s = tid; s < m; s += THREADS) sh.dg[s] = w[th * m + s] * (dw[th * m + s] - wdot);
   } else {
-    for (int x = tid; x < m * hc; x += THREADS) sh.dg[x] = dw[th * m * hc + x];
+#pragma unroll
+    for (int g = 0; g < NG; ++g)
+#pragma unroll
+      for (int c = 0; c < kMaxCores; ++c)
+        dg[g][c] = valid[g] && c < hc ? dw[(th * m + g * kWave + lane) * hc + c] : 0.0f;
   }
-  __syncthreads();
-  // ---- Tucker: the selected slots' per-slice scores, four lanes per (axis, slot) key row
+  // ---- distinct keys per axis: a slot leads its key when no earlier slot holds it; pos is the
+  // number of leaders before the key's leader
+  int first[2][NG], pos[2][NG], nd[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    uint64_t lead[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      int f = -1;
+#pragma unroll
+      for (int g2 = 0; g2 <= g; ++g2) {
+        const uint64_t mm = key_match(key[a][g], key[a][g2], valid[g2], key_bits);
+        if (f < 0 && mm != 0ull) f = g2 * kWave + __builtin_ctzll(mm);
+      }
+      first[a][g] = f;
+      lead[g] = __ballot(valid[g] && f == g * kWave + lane);
+    }
+    int total = 0;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) total += __popcll(lead[g]);
+    nd[a] = total;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int f = valid[g] ? first[a][g] : 0;
+      int p = 0;
+#pragma unroll
+      for (int g2 = 0; g2 < NG; ++g2) {
+        if (g2 < f / kWave) p += __popcll(lead[g2]);
+        if (g2 == f / kWave) p += __popcll(lead[g2] & ((1ull << (f % kWave)) - 1ull));
+      }
+      pos[a][g] = p;
+      if (valid[g] && f == g * kWave + lane) sh.dist[a][p] = static_cast<int>(key[a][g]);
+    }
+  }
+  wave_sync();
+  // ---- Tucker: per-slice scores of the distinct keys, four lanes per key row
+  float sr[NG][kMaxRank] = {}, sc[NG][kMaxRank] = {};
   if (tucker) {
     const int width = dk / rank, n4 = dk >> 2;
-    for (int job = tid; job < 8 * m; job += THREADS) {   // whole quads: 8m is a multiple of 4
-      const int part = job & 3, row = job >> 2;
-      const int axis = row >= m, s = row - (axis ? m : 0);
-      const int key = axis ? sh.jj[s] : sh.ii[s];
-      const float4* kr = reinterpret_cast<const float4*>((axis ? k_col : k_row) + (static_cast<size_t>(h) * n + key) * dk);
-      const float4* qr = reinterpret_cast<const float4*>((axis ? q_col : q_row) + th * dk);
+    const int part = lane & 3;
+    const int f0 = (part * n4) >> 2, f1 = ((part + 1) * n4) >> 2;
+    const int jobs = nd[0] + nd[1];
+    for (int j0 = 0; j0 < jobs; j0 += kWave / 4) {     // wave-uniform trip count
+      const int kk = j0 + lane / 4;
+      const bool ok = kk < jobs;
+      const int a = kk >= nd[0] ? 1 : 0;
+      const int k = kk - (a ? nd[0] : 0);
       float acc[kMaxRank] = {0.0f, 0.0f, 0.0f, 0.0f};
-      const int f1 = ((part + 1) * n4) >> 2;
-      for (int f = (part * n4) >> 2; f < f1; ++f) {
-        const float4 kv = kr[f], qv = qr[f];
-        float d = kv.x * qv.x;
-        d = fmaf(kv.y, qv.y, d);
-        d = fmaf(kv.z, qv.z, d);
-        d = fmaf(kv.w, qv.w, d);
-        const int rho = (4 * f) / width;
+      if (ok) {
+        const float4* kr = reinterpret_cast<const float4*>(
+            (a ? k_col : k_row) + (static_cast<size_t>(h) * n + sh.dist[a][k]) * dk);
+        const float4* qr = reinterpret_cast<const float4*>((a ? q_col : q_row) + th * dk);
+#pragma unroll 4
+        for (int f = f0; f < f1; ++f) {
+          const float4 kv = kr[f], qv = qr[f];
+          float d = kv.x * qv.x;
+          d = fmaf(kv.y, qv.y, d);
+          d = fmaf(kv.z, qv.z, d);
+          d = fmaf(kv.w, qv.w, d);
+          const int rho = (4 * f) / width;
 #pragma unroll
-        for (int r = 0; r < kMaxRank; ++r) acc[r] += rho == r ? d : 0.0f;
+          for (int r = 0; r < kMaxRank; ++r) acc[r] += rho == r ? d : 0.0f;
+        }
       }
 #pragma unroll
-      for (int r = 0; r < kMaxRank; ++r) {
+      for (int r = 0; r < kMaxRank; ++r) {          // quad sums; every lane takes part
         acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0xB1, 0xF, 0xF, false));
         acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0x4E, 0xF, 0xF, false));
       }
-      if (part == 0)
-        for (int r = 0; r < rank; ++r) (axis ? sh.scol : sh.srow)[s][r] = acc[r];
+      if (ok && part == 0)
+#pragma unroll
+        for (int r = 0; r < kMaxRank; ++r) sh.sd[a][k][r] = acc[r];
     }
-    __syncthreads();
+    wave_sync();
+#pragma unroll
+    for (int g = 0; g < NG; ++g)
+#pragma unroll
+      for (int r = 0; r < kMaxRank; ++r) {
+        sr[g][r] = valid[g] ? sh.sd[0][pos[0][g]][r] : 0.0f;
+        sc[g][r] = valid[g] ? sh.sd[1][pos[1][g]][r] : 0.0f;
+      }
   }
-  // ---- each slot's dS terms, and which slot first holds its row / column
-  for (int s = tid; s < m; s += THREADS) {
+  // ---- each slot's dS terms: d score / d s_row = C s_col, d score / d s_col = C^T s_row (eq. (10))
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    if (!valid[g]) continue;
+    const int s = g * kWave + lane;
     if (!tucker) {
-      sh.cr[s][0] = sh.dg[s];
-      sh.cc[s][0] = sh.dg[s];
-    } else {
-      for (int r = 0; r < rank; ++r) {
-        float a = 0.0f, b = 0.0f;
-        for (int c = 0; c < hc; ++c) {
-          float ca = 0.0f, cb = 0.0f;
-          for (int x = 0; x < rank; ++x) {
-            ca = fmaf(sh.core[c][r * rank + x], sh.scol[s][x], ca);   // (C S_col)[r]
-            cb = fmaf(sh.core[c][x * rank + r], sh.srow[s][x], cb);   // (C^T S_row)[r]
-          }
-          a = fmaf(sh.dg[s * hc + c], ca, a);
-          b = fmaf(sh.dg[s * hc + c], cb, b);
+      sh.cs[0][s][0] = dg[g][0];
+      sh.cs[1][s][0] = dg[g][0];
+      continue;
+    }
+    for (int r = 0; r < rank; ++r) {
+      float x0 = 0.0f, x1 = 0.0f;
+#pragma unroll
+      for (int c = 0; c < kMaxCores; ++c) {
+        if (c >= hc) break;
+        const float* C = core_all + (static_cast<size_t>(h) * hc + c) * rank * rank;
+        float ca = 0.0f, cb = 0.0f;
+#pragma unroll
+        for (int x = 0; x < kMaxRank; ++x) {
+          if (x >= rank) break;
+          ca = fmaf(C[r * rank + x], sc[g][x], ca);
+          cb = fmaf(C[x * rank + r], sr[g][x], cb);
         }
-        sh.cr[s][r] = a;
-        sh.cc[s][r] = b;
+        x0 = fmaf(dg[g][c], ca, x0);
+        x1 = fmaf(dg[g][c], cb, x1);
       }
+      sh.cs[0][s][r] = x0;
+      sh.cs[1][s][r] = x1;
     }
-    int lr = s, lc = s;
-    for (int x = s - 1; x >= 0; --x) {
-      if (sh.ii[x] == sh.ii[s]) lr = x;
-      if (sh.jj[x] == sh.jj[s]) lc = x;
-    }
-    sh.lead_r[s] = lr;
-    sh.lead_c[s] = lc;
   }
-  __syncthreads();
-  if (tucker)       // dC partial of this (token, head): slots in order
-    for (int x = tid; x < hc * rank * rank; x += THREADS) {
+  // ---- dC partial of this (token, head): sum over slots of dg s_row s_col^T (a wave sum)
+  if (tucker) {
+    for (int x = 0; x < hc * rank * rank; ++x) {    // wave-uniform
       const int c = x / (rank * rank), r = (x / rank) % rank, z = x % rank;
-      float a = 0.0f;
-      for (int s = 0; s < m; ++s) a = fmaf(sh.dg[s * hc + c], sh.srow[s][r] * sh.scol[s][z], a);
-      dc_part[th * hc * rank * rank + x] = a;
-    }
-  for (int s = tid; s < m; s += THREADS) {
-    if (sh.lead_r[s] == s) {
-      int pos = 0;
-      for (int x = 0; x < s; ++x) pos += sh.lead_r[x] == x;
-      sh.pos_r[s] = pos;
-      sh.dist_r[pos] = sh.ii[s];
-    }
-    if (sh.lead_c[s] == s) {
-      int pos = 0;
-      for (int x = 0; x < s; ++x) pos += sh.lead_c[x] == x;
-      sh.pos_c[s] = pos;
-      sh.dist_c[pos] = sh.jj[s];
-    }
-  }
-  if (tid == 0) {
-    int a = 0, b = 0;
-    for (int s = 0; s < m; ++s) {
-      a += sh.lead_r[s] == s;
-      b += sh.lead_c[s] == s;
-    }
-    sh.nr = a;
-    sh.nc = b;
-  }
-  __syncthreads();
-  // ---- dS per distinct row / column: its slots' terms in slot order
-  for (int s = tid; s < m; s += THREADS) {
-    if (sh.lead_r[s] == s)
-      for (int r = 0; r < rank; ++r) {
-        float a = 0.0f;
-        for (int x = s; x < m; ++x) a += sh.lead_r[x] == s ? sh.cr[x][r] : 0.0f;
-        sh.dsr[sh.pos_r[s]][r] = a;
+      float v = 0.0f;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        float d = 0.0f, a = 0.0f, b = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < kMaxCores; ++cc) d = cc == c ? dg[g][cc] : d;
+#pragma unroll
+        for (int q = 0; q < kMaxRank; ++q) {
+          a = q == r ? sr[g][q] : a;
+          b = q == z ? sc[g][q] : b;
+        }
+        v = fmaf(d, a * b, v);
       }
-    if (sh.lead_c[s] == s)
-      for (int r = 0; r < rank; ++r) {
-        float a = 0.0f;
-        for (int x = s; x < m; ++x) a += sh.lead_c[x] == s ? sh.cc[x][r] : 0.0f;
-        sh.dsc[sh.pos_c[s]][r] = a;
-      }
-  }
-  __syncthreads();
-  // ---- dq = sum over distinct keys of dS K (eq. (2) / (4) transposed)
-  const int width = dk / rank;
-  for (int d = tid; d < 2 * dk; d += THREADS) {
-    const int axis = d >= dk, e = d - (axis ? dk : 0);
-    const int r = e / width;
-    const float* K = axis ? k_col : k_row;
-    const int nk = axis ? sh.nc : sh.nr;
-    float a = 0.0f;
-    for (int k = 0; k < nk; ++k) {
-      const int key = axis ? sh.dist_c[k] : sh.dist_r[k];
-      const float ds = axis ? sh.dsc[k][r] : sh.dsr[k][r];
-      a = fmaf(ds, K[(static_cast<size_t>(h) * n + key) * dk + e], a);
+      v = wave_sum(v);
+      if (lane == 0) dc_part[th * hc * rank * rank + x] = v;
     }
-    (axis ? dq_col : dq_row)[th * dk + e] = a;
   }
-  // ---- key-gradient entries: slot ((t H + h) 2 + axis) m + k for the k-th distinct key
+  wave_sync();
+  // ---- dS per distinct key: its slots' terms in slot order, summed by the leading slot
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const bool leads = valid[g] && first[a][g] == g * kWave + lane;
+      float acc[kMaxRank] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int g2 = g; g2 < NG; ++g2) {
+        uint64_t mm = key_match(key[a][g], key[a][g2], valid[g2], key_bits);
+        if (!leads) continue;
+        while (mm != 0ull) {
+          const int x = g2 * kWave + __builtin_ctzll(mm);
+          mm &= mm - 1ull;
+#pragma unroll
+          for (int r = 0; r < kMaxRank; ++r)
+            if (r < R) acc[r] += sh.cs[a][x][r];
+        }
+      }
+      if (leads)
+#pragma unroll
+        for (int r = 0; r < kMaxRank; ++r) sh.sd[a][pos[a][g]][r] = acc[r];
+    }
+  wave_sync();
+  // ---- dq = sum over distinct keys of dS K (eqs. (2) / (4) transposed)
+  const int width = dk / R;
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const float* Kh = (a ? k_col : k_row) + static_cast<size_t>(h) * n * dk;
+    float* dq = (a ? dq_col : dq_row) + th * dk;
+    const int nk = nd[a];
+    for (int e = lane; e < dk; e += kWave) {
+      const int r = e / width;
+      float acc = 0.0f;
+      int k = 0;
+      for (; k + 8 <= nk; k += 8) {     // eight key loads in flight, the sum still in key order
+        float kv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) kv[u] = Kh[static_cast<size_t>(sh.dist[a][k + u]) * dk + e];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = fmaf(sh.sd[a][k + u][r], kv[u], acc);
+      }
+      for (; k < nk; ++k) acc = fmaf(sh.sd[a][k][r], Kh[static_cast<size_t>(sh.dist[a][k]) * dk + e], acc);
+      dq[e] = acc;
+    }
+  }
+  // ---- key-gradient entries: slot ((t H + h) 2 + axis) m + k for the k-th distinct key; the
+  // rest of the axis' m slots hold the sentinel
   const uint32_t sentinel = static_cast<uint32_t>(2 * H) * n;
-  for (int x = tid; x < 2 * m; x += THREADS) {
-    const int axis = x >= m, k = x - (axis ? m : 0);
-    const size_t slot = (th * 2 + axis) * m + k;
-    const int nk = axis ? sh.nc : sh.nr;
-    evals[slot] = static_cast<uint32_t>(slot);
-    if (k < nk) {
-      const int key = axis ? sh.dist_c[k] : sh.dist_r[k];
-      ekeys[slot] = static_cast<uint32_t>((axis * H + h) * n + key);
-      for (int r = 0; r < rank; ++r) edS[slot * rank + r] = axis ? sh.dsc[k][r] : sh.dsr[k][r];
-    } else {
-      ekeys[slot] = sentinel;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      if (!valid[g]) continue;
+      const int s = g * kWave + lane;
+      const size_t base = (th * 2 + a) * m;
+      if (first[a][g] == s) {
+        const size_t slot = base + pos[a][g];
+        evals[slot] = static_cast<uint32_t>(slot);
+        ekeys[slot] = static_cast<uint32_t>((a * H + h) * n) + key[a][g];
+        for (int r = 0; r < rank; ++r) edS[slot * rank + r] = sh.sd[a][pos[a][g]][r];
+      }
+      if (s >= nd[a]) {
+        evals[base + s] = static_cast<uint32_t>(base + s);
+        ekeys[base + s] = sentinel;
+      }
     }
-  }
 }
 
-// One wave per run of equal keys: dK[key] += sum over the run's entries (in order) of dS q.
-__global__ __launch_bounds__(THREADS) void key_bwd_run_kernel(
+// Key gradients by segments of sorted entries (as the value rows): dK[key] += sum over the
+// entries of its run, in order, of dS[entry][slice] q[t, h, :]; pieces cut by a segment store
+// their partial row for seg_join_kernel.
+__global__ __launch_bounds__(THREADS) void key_bwd_seg_kernel(
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ slots, int M, uint32_t sentinel,
     const float* __restrict__ edS, const float* __restrict__ q_row, const float* __restrict__ q_col,
-    float* __restrict__ dk_row, float* __restrict__ dk_col, int H, int n, int dk, int rank, int m) {
+    float* __restrict__ dk_row, float* __restrict__ dk_col, int H, int n, int dk, int rank, int m,
+    float* __restrict__ partial, const uint32_t* __restrict__ list,
+    uint32_t* __restrict__ counts, uint32_t* __restrict__ heads) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int i = blockIdx.x * NWAVES + static_cast<int>(threadIdx.x) / kWave;
-  if (i >= M) return;
-  const uint32_t key = keys[i];
-  if (key == sentinel || (i > 0 && keys[i - 1] == key)) return;
-  int end = i + 1;
-  for (int base = i + 1; base < M; base += kWave) {
-    const int pos = base + lane;
-    const uint64_t same = __ballot(pos < M && keys[pos] == key);
-    if (same != ~0ull) {
-      end = base + __builtin_ctzll(~same);
-      break;
-    }
-    end = min(M, base + kWave);
-  }
+  const uint32_t n_pieces = counts[0];
+  for (uint32_t pk = blockIdx.x * NWAVES + threadIdx.x / kWave; pk < n_pieces;
+       pk += gridDim.x * NWAVES) {
+  const int ps = static_cast<int>(list[pk]);
+  const uint32_t key = keys[ps];                     // never the sentinel: not listed
+  int pe;
+  bool run_start, run_end;
+  piece_at(keys, ps, M, key, &pe, &run_start, &run_end);
+  if (run_start && !run_end && lane == 0)
+    heads[atomicAdd(counts + 1, 1u)] = static_cast<uint32_t>(ps);
+  const int g = ps / kSeg;
   const int axis = static_cast<int>(key / (static_cast<uint32_t>(H) * n));
   const int rem = static_cast<int>(key - static_cast<uint32_t>(axis) * H * n);
-  const int h = rem / n, kidx = rem % n;
+  const int h = rem / n;
   const float* q = axis ? q_col : q_row;
-  float* dK = (axis ? dk_col : dk_row) + (static_cast<size_t>(h) * n + kidx) * dk;
+  float* dK = (axis ? dk_col : dk_row) + static_cast<size_t>(rem) * dk;
   const int width = dk / rank;
+  const int n_e = pe - ps;
+  const uint32_t my_slot = lane < n_e ? slots[ps + lane] : 0u;   // one entry per lane
   for (int d0 = 0; d0 < dk; d0 += kWave * 4) {
     const int d = d0 + lane * 4;
-    if (d >= dk) continue;                         // no cross-lane operation below
-    const int r = d / width;                       // four consecutive dims lie in one slice
+    const bool active = d < dk;
+    const int r = active ? d / width : 0;             // four consecutive dims lie in one slice
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int e = i; e < end; ++e) {
-      const size_t slot = slots[e];
-      const size_t t = slot / (static_cast<size_t>(2) * H * m);
-      const f32x4 qv = *reinterpret_cast<const f32x4*>(q + (t * H + h) * dk + d);
-      const float ds = edS[slot * rank + r];
-      acc.x = fmaf(ds, qv.x, acc.x);
-      acc.y = fmaf(ds, qv.y, acc.y);
-      acc.z = fmaf(ds, qv.z, acc.z);
-      acc.w = fmaf(ds, qv.w, acc.w);
+    for (int j0 = 0; j0 < n_e; j0 += 2 * kInFlight) {  // wave-uniform
+      f32x4 qv[2 * kInFlight];
+      float ds[2 * kInFlight];
+#pragma unroll
+      for (int u = 0; u < 2 * kInFlight; ++u) {      // all loads first
+        const size_t slot = static_cast<uint32_t>(
+            __builtin_amdgcn_readlane(static_cast<int>(my_slot), min(j0 + u, n_e - 1)));
+        const size_t t = slot / (static_cast<size_t>(2) * H * m);
+        qv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        ds[u] = 0.0f;
+        if (active) {
+          qv[u] = *reinterpret_cast<const f32x4*>(q + (t * H + h) * dk + d);
+          ds[u] = edS[slot * rank + r];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 2 * kInFlight; ++u) {      // then the entries in order
+        if (j0 + u >= n_e) break;
+        acc.x = fmaf(ds[u], qv[u].x, acc.x);
+        acc.y = fmaf(ds[u], qv[u].y, acc.y);
+        acc.z = fmaf(ds[u], qv[u].z, acc.z);
+        acc.w = fmaf(ds[u], qv[u].w, acc.w);
+      }
     }
-    f32x4* dst = reinterpret_cast<f32x4*>(dK + d);
-    f32x4 v = *dst;
-    v += acc;
-    *dst = v;
+    if (!active) continue;
+    if (run_start && run_end) {
+      f32x4* dst = reinterpret_cast<f32x4*>(dK + d);
+      f32x4 v = *dst;
+      v += acc;
+      *dst = v;
+    } else {
+      *reinterpret_cast<f32x4*>(partial + (static_cast<size_t>(2) * g + (run_start ? 1 : 0)) * dk + d) = acc;
+    }
+  }
   }
 }
 
-// out[k][c] = sum over rows j of chunk k (rows k*chunk .. min(R, (k+1)*chunk) - 1, in order) of
-// in[j][c]; with accumulate, out[0][c] += that sum (one chunk only).
-__global__ __launch_bounds__(THREADS) void sum_rows_kernel(const float* __restrict__ in,
-                                                           float* __restrict__ out, int R, int C,
-                                                           int chunk, int accumulate) {
-  const int chunks = (R + chunk - 1) / chunk;
-  for (int x = blockIdx.x * THREADS + threadIdx.x; x < chunks * C; x += gridDim.x * THREADS) {
-    const int k = x / C, c = x % C;
-    float a = 0.0f;
-    for (int j = k * chunk; j < min(R, (k + 1) * chunk); ++j) a += in[static_cast<size_t>(j) * C + c];
-    if (accumulate) out[c] += a;
-    else out[x] = a;
+// out[c] += sum over the R rows of in[.][c]: one workgroup per column, thread i adding rows i,
+// i + 256, ... in order, then a fixed tree over the threads.
+__global__ __launch_bounds__(THREADS) void sum_cols_kernel(const float* __restrict__ in,
+                                                           float* __restrict__ out, int R, int C) {
+  __shared__ float red[THREADS];
+  const int c = blockIdx.x, tid = threadIdx.x;
+  float a = 0.0f;
+  for (int j = tid; j < R; j += THREADS) a += in[static_cast<size_t>(j) * C + c];
+  red[tid] = a;
+  __syncthreads();
+  for (int off = THREADS / 2; off > 0; off >>= 1) {
+    if (tid < off) red[tid] += red[tid + off];
+    __syncthreads();
   }
+  if (tid == 0) out[c] += red[0];
 }
 
 size_t round_up256(size_t x) { return (x + 255) / 256 * 256; }
@@ -423,10 +715,13 @@ int bits_for(int64_t n) {
 
 }  // namespace
 
-size_t gather_backward_workspace_bytes(int T, int bag) {
+size_t gather_backward_workspace_bytes(int T, int bag, int dv) {
   const int M = T * bag;
   if (M == 0) return 0;
-  return 2 * round_up256(static_cast<size_t>(M) * sizeof(uint32_t)) + round_up256(sort_workspace_bytes(M));
+  const size_t nseg = (static_cast<size_t>(M) + kSeg - 1) / kSeg;
+  return 3 * round_up256(static_cast<size_t>(M) * sizeof(uint32_t)) + round_up256(nseg * sizeof(uint32_t)) +
+         256 + round_up256(2 * nseg * dv * sizeof(float)) + round_up256(sort_workspace_bytes(M)) +
+         round_up256(list_workspace_bytes(M));
 }
 
 hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const void* values, int T,
@@ -439,23 +734,40 @@ hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const vo
   char* base = static_cast<char*>(ws);
   uint32_t* keys = reinterpret_cast<uint32_t*>(base);
   uint32_t* vals = reinterpret_cast<uint32_t*>(base + round_up256(static_cast<size_t>(M) * sizeof(uint32_t)));
-  void* sws = base + 2 * round_up256(static_cast<size_t>(M) * sizeof(uint32_t));
+  const size_t nseg = (static_cast<size_t>(M) + kSeg - 1) / kSeg;
+  char* p0 = base + 2 * round_up256(static_cast<size_t>(M) * sizeof(uint32_t));
+  uint32_t* list = reinterpret_cast<uint32_t*>(p0);
+  p0 += round_up256(static_cast<size_t>(M) * sizeof(uint32_t));
+  uint32_t* heads = reinterpret_cast<uint32_t*>(p0);
+  p0 += round_up256(nseg * sizeof(uint32_t));
+  uint32_t* counts = reinterpret_cast<uint32_t*>(p0);
+  p0 += 256;
+  float* partial = reinterpret_cast<float*>(p0);
+  void* sws = p0 + round_up256(2 * nseg * dv * sizeof(float));
+  void* lws = static_cast<char*>(sws) + round_up256(sort_workspace_bytes(M));
   const unsigned kb = static_cast<unsigned>(std::min((M + THREADS - 1) / THREADS, 4096));
   hipLaunchKernelGGL(bwd_keys_kernel, dim3(kb), dim3(THREADS), 0, s, idx,
                      expand > 1 ? perm : nullptr, n_values, M, keys, vals);
   uint32_t *rows_sorted, *ents_sorted;
   hipError_t e = sort_pairs(keys, vals, M, bits_for(n_values), sws, s, &rows_sorted, &ents_sorted);
   if (e != hipSuccess) return e;
-  const dim3 grid((M + NWAVES - 1) / NWAVES);
   const int c = cores > 1 ? cores : 1;
+  const dim3 list_grid(kListWaves / NWAVES);
+  // row indices are below 2^31: the sentinel never occurs
+  e = list_pieces(rows_sorted, M, 0xFFFFFFFFu, list, counts, lws, s);
+  if (e != hipSuccess) return e;
   if (vdtype == UMEM_F32)
-    hipLaunchKernelGGL(gather_bwd_run_kernel<float>, grid, dim3(THREADS), 0, s, rows_sorted,
+    hipLaunchKernelGGL(gather_bwd_seg_kernel<float>, list_grid, dim3(THREADS), 0, s, rows_sorted,
                        ents_sorted, M, static_cast<const float*>(values), dv, idx, w,
-                       expand > 1 ? perm : nullptr, n_values, expand, c, bag, d_pooled, d_values, dw);
+                       expand > 1 ? perm : nullptr, n_values, expand, c, bag, d_pooled, d_values, dw,
+                       partial, list, counts, heads);
   else
-    hipLaunchKernelGGL(gather_bwd_run_kernel<uint16_t>, grid, dim3(THREADS), 0, s, rows_sorted,
+    hipLaunchKernelGGL(gather_bwd_seg_kernel<uint16_t>, list_grid, dim3(THREADS), 0, s, rows_sorted,
                        ents_sorted, M, static_cast<const uint16_t*>(values), dv, idx, w,
-                       expand > 1 ? perm : nullptr, n_values, expand, c, bag, d_pooled, d_values, dw);
+                       expand > 1 ? perm : nullptr, n_values, expand, c, bag, d_pooled, d_values, dw,
+                       partial, list, counts, heads);
+  hipLaunchKernelGGL(seg_join_kernel, list_grid, dim3(THREADS), 0, s, rows_sorted, M, dv, partial,
+                     d_values, heads, counts, 0, 0, nullptr);
   return hipGetLastError();
 }
 
@@ -465,11 +777,11 @@ size_t score_backward_workspace_bytes(const umem_desc& d, int T) {
   const int Mk = static_cast<int>(th * 2 * d.topm);
   const int hc = d.cores > 1 ? d.cores : 1;
   const size_t dc = d.grid == UMEM_GRID_TUCKER ? static_cast<size_t>(hc) * d.rank * d.rank : 0;
-  const size_t chunks = (static_cast<size_t>(T) + kDcChunk - 1) / kDcChunk;
-  return 2 * round_up256(static_cast<size_t>(Mk) * sizeof(uint32_t)) +
-         round_up256(static_cast<size_t>(Mk) * d.rank * sizeof(float)) +
-         round_up256(th * dc * sizeof(float)) + round_up256(chunks * d.heads * dc * sizeof(float)) +
-         round_up256(sort_workspace_bytes(Mk));
+  const size_t nseg = (static_cast<size_t>(Mk) + kSeg - 1) / kSeg;
+  return 3 * round_up256(static_cast<size_t>(Mk) * sizeof(uint32_t)) + round_up256(nseg * sizeof(uint32_t)) +
+         256 + round_up256(static_cast<size_t>(Mk) * d.rank * sizeof(float)) +
+         round_up256(2 * nseg * d.dk * sizeof(float)) + round_up256(list_workspace_bytes(Mk)) +
+         round_up256(th * dc * sizeof(float)) + round_up256(sort_workspace_bytes(Mk));
 }
 
 hipError_t launch_score_backward(const umem_desc& d, int T, const float* q_row, const float* q_col,
@@ -492,33 +804,47 @@ hipError_t launch_score_backward(const umem_desc& d, int T, const float* q_row, 
   base += round_up256(static_cast<size_t>(Mk) * sizeof(uint32_t));
   float* edS = reinterpret_cast<float*>(base);
   base += round_up256(static_cast<size_t>(Mk) * r * sizeof(float));
+  const size_t nseg = (static_cast<size_t>(Mk) + kSeg - 1) / kSeg;
+  float* kpart = reinterpret_cast<float*>(base);
+  base += round_up256(2 * nseg * d.dk * sizeof(float));
+  uint32_t* list = reinterpret_cast<uint32_t*>(base);
+  base += round_up256(static_cast<size_t>(Mk) * sizeof(uint32_t));
+  uint32_t* heads = reinterpret_cast<uint32_t*>(base);
+  base += round_up256(nseg * sizeof(uint32_t));
+  uint32_t* counts = reinterpret_cast<uint32_t*>(base);
+  base += 256;
+  void* lws = base;
+  base += round_up256(list_workspace_bytes(Mk));
   float* dc_part = reinterpret_cast<float*>(base);
   base += round_up256(th * dc * sizeof(float));
-  float* dc_chunks = reinterpret_cast<float*>(base);
-  const size_t chunks = (static_cast<size_t>(T) + kDcChunk - 1) / kDcChunk;
-  base += round_up256(chunks * H * dc * sizeof(float));
   void* sws = base;
-  hipLaunchKernelGGL(score_bwd_kernel, dim3(static_cast<unsigned>(th)), dim3(THREADS), 0, s, q_row,
-                     q_col, k_row, k_col, core, idx, w, dw, T, H, d.n_keys, d.dk, r, m,
-                     tucker ? 1 : 0, d.weight == UMEM_W_SOFTMAX ? 1 : 0, hc, dq_row, dq_col, ekeys,
-                     evals, edS, dc_part);
+  const int key_bits = bits_for(d.n_keys);
+  const int sm = d.weight == UMEM_W_SOFTMAX ? 1 : 0;
+#define UMEM_SCORE_BWD(NG)                                                                       \
+  hipLaunchKernelGGL(score_bwd_kernel<NG>,                                                      \
+                     dim3(static_cast<unsigned>((th + score_bwd_waves<NG>() - 1) / score_bwd_waves<NG>())), \
+                     dim3(score_bwd_waves<NG>() * kWave), 0, s, q_row, q_col, k_row, k_col, core, \
+                     idx, w, dw, T, H, d.n_keys, key_bits, d.dk, r, m, tucker ? 1 : 0, sm, hc,   \
+                     dq_row, dq_col, ekeys, evals, edS, dc_part)
+  if (m <= kWave) UMEM_SCORE_BWD(1);
+  else if (m <= 2 * kWave) UMEM_SCORE_BWD(2);
+  else UMEM_SCORE_BWD(4);
+#undef UMEM_SCORE_BWD
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const uint32_t sentinel = static_cast<uint32_t>(2 * H) * d.n_keys;
   uint32_t *ks, *vs;
   e = sort_pairs(ekeys, evals, Mk, bits_for(static_cast<int64_t>(sentinel) + 1), sws, s, &ks, &vs);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(key_bwd_run_kernel, dim3((Mk + NWAVES - 1) / NWAVES), dim3(THREADS), 0, s, ks,
-                     vs, Mk, sentinel, edS, q_row, q_col, dk_row, dk_col, H, d.n_keys, d.dk, r, m);
-  if (tucker) {
-    // dC: per-token partials [T][H dc] -> chunks of kDcChunk tokens -> the chunks, added to dcore
-    const int C = H * dc;
-    const unsigned b1 = static_cast<unsigned>(std::min<size_t>((chunks * C + THREADS - 1) / THREADS, 1024));
-    hipLaunchKernelGGL(sum_rows_kernel, dim3(b1), dim3(THREADS), 0, s, dc_part, dc_chunks, T, C,
-                       kDcChunk, 0);
-    hipLaunchKernelGGL(sum_rows_kernel, dim3((C + THREADS - 1) / THREADS), dim3(THREADS), 0, s,
-                       dc_chunks, dcore, static_cast<int>(chunks), C, static_cast<int>(chunks), 1);
-  }
+  const dim3 list_grid(kListWaves / NWAVES);
+  e = list_pieces(ks, Mk, sentinel, list, counts, lws, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(key_bwd_seg_kernel, list_grid, dim3(THREADS), 0, s, ks, vs, Mk, sentinel, edS,
+                     q_row, q_col, dk_row, dk_col, H, d.n_keys, d.dk, r, m, kpart, list, counts, heads);
+  hipLaunchKernelGGL(seg_join_kernel, list_grid, dim3(THREADS), 0, s, ks, Mk, d.dk, kpart, dk_row,
+                     heads, counts, H, d.n_keys, dk_col);
+  if (tucker)   // dC: the per-token partials [T][H dc], summed over tokens into dcore
+    hipLaunchKernelGGL(sum_cols_kernel, dim3(H * dc), dim3(THREADS), 0, s, dc_part, dcore, T, H * dc);
   return hipGetLastError();
 }
 

@@ -5,11 +5,13 @@
 //
 // Per pass, over tiles of 4096 pairs (256 threads x 16 steps):
 //  * sort_hist_kernel: the tile's digit histogram (LDS atomics), stored digit-major [256][tiles];
-//  * sort_scan_kernel: one workgroup turns the 256 * tiles counts into exclusive offsets (digit
-//    by digit, tile by tile: the order the stable pass writes in);
-//  * sort_scatter_kernel: the tile again, 256 consecutive pairs per step; a pair's place is its
-//    digit's running offset in this tile + the count of equal digits in earlier waves of this
-//    step + its rank among equal digits in its own wave (eight ballots match the digit).
+//  * scan_exclusive turns the 256 * tiles counts into exclusive offsets (digit by digit, tile by
+//    tile: the order the stable pass writes in): chunk sums, then each chunk rescanned from the
+//    sum of the chunks before it;
+//  * sort_scatter_kernel: the tile again (all of its pairs loaded up front), 256 consecutive
+//    pairs per step; a pair's place is its digit's running offset in this tile + the count of
+//    equal digits in earlier waves of this step + its rank among equal digits in its own wave
+//    (eight ballots match the digit).
 #include <utility>
 
 #include "umem_internal.h"
@@ -21,7 +23,6 @@ constexpr int kThreads = 256;
 constexpr int kSteps = 16;
 constexpr int kTile = kThreads * kSteps;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kScanThreads = 1024;
 
 __device__ __forceinline__ uint64_t lanes_below() {
   const unsigned lane = threadIdx.x & (kWave - 1);
@@ -44,27 +45,65 @@ __global__ __launch_bounds__(kThreads) void sort_hist_kernel(const uint32_t* __r
   hist[static_cast<size_t>(threadIdx.x) * tiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
-// Exclusive scan of n counts in place, one workgroup: each thread sums a contiguous chunk, the
-// chunk sums are scanned in LDS, and each thread rewrites its chunk with running offsets.
-__global__ __launch_bounds__(kScanThreads) void sort_scan_kernel(uint32_t* __restrict__ v, int n) {
-  __shared__ uint32_t part[kScanThreads];
-  const int per = (n + kScanThreads - 1) / kScanThreads;
-  const int beg = threadIdx.x * per, end = min(n, beg + per);
-  uint32_t s = 0;
-  for (int i = beg; i < end; ++i) s += v[i];
-  part[threadIdx.x] = s;
+// ---------------------------------------------------------------- exclusive scan
+// Over chunks of kScanChunk counts: each chunk's sum (scan_sums_kernel, skipped for one chunk),
+// then each chunk rescanned from the sum of the chunk sums before it (scan_apply_kernel).  Thread
+// t of a chunk owns its 16 consecutive counts.  Integer sums: exact in any order.
+
+constexpr int kScanPer = 16;
+constexpr int kScanChunk = kThreads * kScanPer;
+
+// Exclusive prefix of v over the workgroup's threads (every thread calls it), and the total.
+__device__ __forceinline__ uint32_t block_exclusive(uint32_t v, uint32_t* lds, uint32_t* total) {
+  const int tid = threadIdx.x;
+  lds[tid] = v;
   __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {      // Hillis-Steele inclusive scan
-    const uint32_t add = threadIdx.x >= off ? part[threadIdx.x - off] : 0u;
+  for (int off = 1; off < kThreads; off <<= 1) {          // Hillis-Steele inclusive scan
+    const uint32_t add = tid >= off ? lds[tid - off] : 0u;
     __syncthreads();
-    part[threadIdx.x] += add;
+    lds[tid] += add;
     __syncthreads();
   }
-  uint32_t run = part[threadIdx.x] - s;                    // exclusive
-  for (int i = beg; i < end; ++i) {
-    const uint32_t c = v[i];
-    v[i] = run;
-    run += c;
+  const uint32_t incl = lds[tid];
+  *total = lds[kThreads - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ __launch_bounds__(kThreads) void scan_sums_kernel(const uint32_t* __restrict__ v, int n,
+                                                             uint32_t* __restrict__ sums) {
+  __shared__ uint32_t lds[kThreads];
+  const int beg = blockIdx.x * kScanChunk + threadIdx.x * kScanPer;
+  uint32_t a = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; ++k) a += beg + k < n ? v[beg + k] : 0u;
+  uint32_t total;
+  block_exclusive(a, lds, &total);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+// sums: the chunk sums (read only by chunks after the first; nb <= 256 * 16).
+__global__ __launch_bounds__(kThreads) void scan_apply_kernel(uint32_t* __restrict__ v, int n,
+                                                              const uint32_t* __restrict__ sums) {
+  __shared__ uint32_t lds[kThreads];
+  uint32_t before = 0;
+  for (int j = threadIdx.x; j < static_cast<int>(blockIdx.x); j += kThreads) before += sums[j];
+  uint32_t offset;
+  block_exclusive(before, lds, &offset);                  // offset: all threads' parts summed
+  const int beg = blockIdx.x * kScanChunk + threadIdx.x * kScanPer;
+  uint32_t loc[kScanPer];
+  uint32_t a = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; ++k) {
+    loc[k] = beg + k < n ? v[beg + k] : 0u;
+    a += loc[k];
+  }
+  uint32_t total;
+  uint32_t run = offset + block_exclusive(a, lds, &total);
+#pragma unroll
+  for (int k = 0; k < kScanPer; ++k) {
+    if (beg + k < n) v[beg + k] = run;
+    run += loc[k];
   }
 }
 
@@ -78,14 +117,22 @@ __global__ __launch_bounds__(kThreads) void sort_scatter_kernel(
   const int wave = tid / kWave;
   base[tid] = offs[static_cast<size_t>(tid) * tiles + blockIdx.x];
   const int tile0 = blockIdx.x * kTile;
+  uint32_t kin[kSteps], vin[kSteps];
+#pragma unroll
+  for (int q = 0; q < kSteps; ++q) {
+    const int pos = tile0 + q * kThreads + tid;
+    kin[q] = pos < M ? keys_in[pos] : 0u;
+    vin[q] = pos < M ? vals_in[pos] : 0u;
+  }
+#pragma unroll
   for (int q = 0; q < kSteps; ++q) {
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) wcnt[w][tid] = 0;
     __syncthreads();
     const int pos = tile0 + q * kThreads + tid;
     const bool valid = pos < M;
-    const uint32_t key = valid ? keys_in[pos] : 0u;
-    const uint32_t val = valid ? vals_in[pos] : 0u;
+    const uint32_t key = kin[q];
+    const uint32_t val = vin[q];
     const uint32_t digit = (key >> shift) & 255u;
     uint64_t peers = __ballot(valid);
 #pragma unroll
@@ -114,9 +161,23 @@ __global__ __launch_bounds__(kThreads) void sort_scatter_kernel(
 
 }  // namespace
 
+size_t scan_workspace_bytes(int n) {
+  return (static_cast<size_t>(n) / kScanChunk + 2) * sizeof(uint32_t);
+}
+
+hipError_t scan_exclusive(uint32_t* v, int n, uint32_t* sums, hipStream_t s) {
+  const int nb = (n + kScanChunk - 1) / kScanChunk;
+  if (nb > kScanChunk) return hipErrorInvalidValue;
+  if (nb == 0) return hipSuccess;
+  if (nb > 1) hipLaunchKernelGGL(scan_sums_kernel, dim3(nb), dim3(kThreads), 0, s, v, n, sums);
+  hipLaunchKernelGGL(scan_apply_kernel, dim3(nb), dim3(kThreads), 0, s, v, n, sums);
+  return hipGetLastError();
+}
+
 size_t sort_workspace_bytes(int M) {
   const size_t tiles = (static_cast<size_t>(M) + kTile - 1) / kTile;
-  return 2 * static_cast<size_t>(M) * sizeof(uint32_t) + 256 * tiles * sizeof(uint32_t) + 256;
+  return 2 * static_cast<size_t>(M) * sizeof(uint32_t) + 256 * tiles * sizeof(uint32_t) +
+         scan_workspace_bytes(static_cast<int>(256 * tiles)) + 256;
 }
 
 hipError_t sort_pairs(uint32_t* keys, uint32_t* vals, int M, int bits, void* ws, hipStream_t s,
@@ -124,13 +185,15 @@ hipError_t sort_pairs(uint32_t* keys, uint32_t* vals, int M, int bits, void* ws,
   uint32_t* k2 = static_cast<uint32_t*>(ws);
   uint32_t* v2 = k2 + M;
   uint32_t* hist = v2 + M;
+  uint32_t* sums = hist + 256 * static_cast<size_t>((M + kTile - 1) / kTile);
   uint32_t *ka = keys, *va = vals, *kb = k2, *vb = v2;
   const int tiles = (M + kTile - 1) / kTile;
   const int passes = (M <= 1 || bits <= 0) ? 0 : (bits + 7) / 8;
   for (int pass = 0; pass < passes; ++pass) {
     const int shift = 8 * pass;
     hipLaunchKernelGGL(sort_hist_kernel, dim3(tiles), dim3(kThreads), 0, s, ka, M, shift, hist, tiles);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, hist, 256 * tiles);
+    hipError_t e = scan_exclusive(hist, 256 * tiles, sums, s);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(tiles), dim3(kThreads), 0, s, ka, va, kb, vb, M,
                        shift, hist, tiles);
     std::swap(ka, kb);

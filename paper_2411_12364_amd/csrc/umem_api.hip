@@ -350,12 +350,13 @@ UMEM_API umem_status umem_key_norm(int32_t heads, int32_t n, int32_t dk, const f
 
 constexpr int64_t kMaxBackwardEntries = INT64_C(1) << 22;   // pairs the backward sorts at once
 
-UMEM_API umem_status umem_gather_backward_workspace_size(int32_t T, int32_t bag, size_t* bytes) {
+UMEM_API umem_status umem_gather_backward_workspace_size(int32_t T, int32_t bag, int32_t dv,
+                                                         size_t* bytes) {
   if (bytes == nullptr) return UMEM_ERR_INVALID_ARG;
   *bytes = 0;
-  if (T < 0 || bag < 1) return UMEM_ERR_INVALID_ARG;
+  if (T < 0 || bag < 1 || dv < 1) return UMEM_ERR_INVALID_ARG;
   if (static_cast<int64_t>(T) * bag > kMaxBackwardEntries) return UMEM_ERR_UNSUPPORTED;
-  *bytes = gather_backward_workspace_bytes(T, bag);
+  *bytes = gather_backward_workspace_bytes(T, bag, dv);
   return UMEM_OK;
 }
 
@@ -370,7 +371,7 @@ UMEM_API umem_status umem_gather_backward(int64_t n_values, int32_t dv, int32_t 
   if (!d_pooled || !dw || !aligned(d_pooled, 16) || !aligned(dw, 4)) return UMEM_ERR_INVALID_ARG;
   if ((expand > 1) != (perm != nullptr) || !aligned(perm, 4)) return UMEM_ERR_INVALID_ARG;
   if (static_cast<int64_t>(T) * bag > kMaxBackwardEntries) return UMEM_ERR_UNSUPPORTED;
-  const size_t need = gather_backward_workspace_bytes(T, bag);
+  const size_t need = gather_backward_workspace_bytes(T, bag, dv);
   if (ws == nullptr || !aligned(ws, 16) || ws_bytes < need) return UMEM_ERR_WORKSPACE;
   return hip_status(launch_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm,
                                            expand, cores, d_pooled, d_values, dw, ws, stream));

@@ -78,11 +78,15 @@ hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, 
 // through ws (sort_workspace_bytes(M) bytes, 4-byte aligned) and the sorted arrays returned
 // (either the inputs or part of ws).
 size_t sort_workspace_bytes(int M);
+// Exclusive prefix sums of v[0, n) in place (n <= 2^24); sums: scan_workspace_bytes(n) bytes of
+// scratch for the per-chunk sums.
+size_t scan_workspace_bytes(int n);
+hipError_t scan_exclusive(uint32_t* v, int n, uint32_t* sums, hipStream_t s);
 hipError_t sort_pairs(uint32_t* keys, uint32_t* vals, int M, int bits, void* ws, hipStream_t s,
                       uint32_t** keys_sorted, uint32_t** vals_sorted);
 
 // Backward of the gather-sum and of the scores (backward.hip).
-size_t gather_backward_workspace_bytes(int T, int bag);
+size_t gather_backward_workspace_bytes(int T, int bag, int dv);
 hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const void* values, int T,
                                   int bag, const int32_t* idx, const float* w, const int32_t* perm,
                                   int expand, int cores, const float* d_pooled, float* d_values,

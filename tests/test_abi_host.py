@@ -224,10 +224,10 @@ def test_query_workspace_and_entry_validation():
 
 def test_backward_validation():
     fake = 1 << 20
-    st, n = U.umem_gather_backward_workspace_size(4096, 256)
+    st, n = U.umem_gather_backward_workspace_size(4096, 256, 512)
     assert st == U.UMEM_OK and n >= 4096 * 256 * 16
-    assert U.umem_gather_backward_workspace_size(0, 64) == (U.UMEM_OK, 0)
-    assert U.umem_gather_backward_workspace_size(1 << 16, 128)[0] == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_gather_backward_workspace_size(0, 64, 512) == (U.UMEM_OK, 0)
+    assert U.umem_gather_backward_workspace_size(1 << 16, 128, 512)[0] == U.UMEM_ERR_UNSUPPORTED
     g = [100, 512, 1, fake, 4, 64, fake, fake, None, 1, 1]           # as umem_gather_sum
     assert U.umem_gather_backward(*g, None, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG   # d_pooled
     assert U.umem_gather_backward(*g, fake, fake, None, fake, n, 0) == U.UMEM_ERR_INVALID_ARG   # dw

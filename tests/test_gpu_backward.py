@@ -37,7 +37,7 @@ def rel(got, ref):
 
 
 def run_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores, dp, dV):
-    st, nws = U.umem_gather_backward_workspace_size(T, bag)
+    st, nws = U.umem_gather_backward_workspace_size(T, bag, dv)
     U.check(st)
     ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
     dw = torch.empty(w.shape, dtype=torch.float32, device="cuda")
@@ -143,6 +143,14 @@ SCORE_CASES = [
              rank=2, grid=CF.GRID_TUCKER),
     CF.Layer("tucker-mcs", T=18, heads=2, dk=128, n_keys=64, topk=16, topm=32, dv=8, vdtype=CF.F32,
              seed=54, rank=2, grid=CF.GRID_TUCKER, cores=2),
+    # more than 64 slots per (token, head): two and four slots per lane; one slot
+    CF.Layer("tucker-m100", T=40, heads=2, dk=64, n_keys=96, topk=16, topm=100, dv=8, vdtype=CF.F32,
+             seed=56, rank=2, grid=CF.GRID_TUCKER),
+    CF.Layer("add-softmax-m200", T=12, heads=1, dk=32, n_keys=120, topk=20, topm=200, dv=8,
+             vdtype=CF.F32, seed=57, weight=CF.W_SOFTMAX),
+    CF.Layer("tucker-mcs-m256", T=10, heads=2, dk=64, n_keys=64, topk=16, topm=256, dv=8,
+             vdtype=CF.F32, seed=58, rank=2, grid=CF.GRID_TUCKER, cores=2),
+    CF.Layer("add-m1", T=9, heads=3, dk=16, n_keys=30, topk=2, topm=1, dv=8, vdtype=CF.F32, seed=59),
     CF.Layer("tucker-r4-wide", T=256, heads=2, dk=128, n_keys=512, topk=32, topm=64, dv=8,
              vdtype=CF.F32, seed=55, rank=4, grid=CF.GRID_TUCKER),
 ]
