@@ -53,6 +53,9 @@ def run_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expa
     (4096, CF.BF16, 4, 84, 9, 2, 500),        # 8 KiB rows (eight row chunks)
     (64, CF.BF16, 1, 40, 50, 4, 60),          # rows narrower than a wave's chunk, four cores
     (1024, CF.F32, 1, 7, 3, 8, 50000),        # eight cores of fp32 slices
+    # d_pooled beyond one XCD's L2 (4 MB)
+    (256, CF.F32, 1, 16, 4200, 1, 500),
+    (512, CF.BF16, 4, 32, 600, 2, 300),       # IVE blocks, two cores
 ])
 def test_gather_backward(dv, vdtype, expand, bag, T, cores, Np):
     rng = np.random.default_rng(dv + bag + T + cores)
