@@ -376,7 +376,7 @@ def front_end_report(fe, launches=200):
     ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
     dev = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
     x, hist, cw = dev(inp["x"]), dev(inp["hist"]), dev(inp["conv_w"])
-    wq, g, b = dev(inp["w_q"].view(np.int16)), dev(inp["gamma"]), dev(inp["beta"])
+    wq, g, b = dev(CF.output_major(inp["w_q"]).view(np.int16)), dev(inp["gamma"]), dev(inp["beta"])
     q_row = torch.empty((fe.T, fe.heads, fe.dk), dtype=torch.float32, device="cuda")
     q_col = None if fe.shared else torch.empty_like(q_row)
 

@@ -163,13 +163,16 @@ UMEM_API umem_status umem_project_workspace_size(int32_t T, int32_t expand, int3
 
 /* a8: y = sum_p pooled[:, p, :] W_p (eq. (15)), then y W_out (Trick 6).  bf16 operands (the
  * fp32 pooled sums and the intermediate are rounded to bf16, nearest even), fp32 accumulation.
- *   pooled  fp32 [T, E, dv]; w_proj bf16 bits [E, dv, dv_virt]; w_out bf16 bits [dv_virt, d_out]
- *           or NULL; out fp32 [T, d_out] (or [T, dv_virt] without w_out).  With w_proj NULL
- *           (dv_virt 0, expand 1) the output linear alone: out = pooled [T, dv] by w_out [dv, d_out]
+ * The weights are stored output-major, as a linear layer's weight ([out features, in features]):
+ *   pooled  fp32 [T, E, dv]
+ *   w_proj  bf16 bits [dv_virt, E * dv]: element (j, p * dv + c) is W_p[c][j]
+ *   w_out   bf16 bits [d_out, dv_virt] (element (o, j) is W_out[j][o]), or NULL
+ *   out     fp32 [T, d_out] (or [T, dv_virt] without w_out).  With w_proj NULL (dv_virt 0,
+ *           expand 1) the output linear alone: out = pooled [T, dv] by w_out [d_out, dv]^T
  *   ws      16-byte aligned scratch of umem_project_workspace_size(...) bytes (NULL if 0)
  * The result does not depend on timing (split reductions add their partials in a fixed order).
- * UMEM_ERR_UNSUPPORTED unless pooled, w_proj and w_out are 16-byte aligned, expand * dv is a
- * multiple of 4 and dv_virt, d_out are multiples of 8. */
+ * UMEM_ERR_UNSUPPORTED unless pooled, w_proj and w_out are 16-byte aligned, expand * dv,
+ * dv_virt and d_out are multiples of 8, and each weight is below 2 GiB. */
 UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
                          const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
                          float* out, void* ws, size_t ws_bytes, hipStream_t stream);
@@ -245,8 +248,8 @@ typedef struct umem_query_desc {
   float eps;        /* LayerNorm epsilon */
 } umem_query_desc;
 /* Requirements (UMEM_ERR_INVALID_ARG otherwise): every count >= 1, shared 0 or 1, eps >= 0.
- * Limits (UMEM_ERR_UNSUPPORTED beyond them): d_model % 4 == 0; conv_k <= 8; dk <= 1024;
- *   (shared ? 1 : 2) * heads * dk a multiple of 8. */
+ * Limits (UMEM_ERR_UNSUPPORTED beyond them): d_model % 8 == 0; conv_k <= 8; dk <= 1024;
+ *   (shared ? 1 : 2) * heads * dk a multiple of 8; the query weight below 2 GiB. */
 
 /* Scratch bytes umem_query needs for B sequences of L tokens. */
 UMEM_API umem_status umem_query_workspace_size(const umem_query_desc* qd, int32_t B, int32_t L,
@@ -257,9 +260,10 @@ UMEM_API umem_status umem_query_workspace_size(const umem_query_desc* qd, int32_
  *   x_hist  fp32 [B, conv_k - 1, d_model], 16-byte aligned: the hidden states before each
  *           sequence's first token here (oldest first), or NULL for zeros (a sequence start)
  *   conv_w  fp32 [conv_k, d_model], 16-byte aligned (no bias)
- *   w_q     bf16 bits [d_model, A * heads * dk], 16-byte aligned, A = 1 if shared else 2: the
- *           row queries of the H heads, then (A = 2) the column queries; the convolved rows are
- *           rounded to bf16 (nearest even) for this product, fp32 accumulation
+ *   w_q     bf16 bits [A * heads * dk, d_model] (output-major, as a linear layer's weight),
+ *           16-byte aligned, A = 1 if shared else 2: the row queries of the H heads, then (A = 2)
+ *           the column queries; the convolved rows are rounded to bf16 (nearest even) for this
+ *           product, fp32 accumulation.  d_model a multiple of 8, w_q below 2 GiB
  *   gamma, beta  fp32 [A, heads, dk]: the LayerNorm of each (axis, head)
  *   q_row   fp32 [T, heads, dk]; q_col the same, or NULL when shared (pass q_row for both
  *           key sets to the scoring then)

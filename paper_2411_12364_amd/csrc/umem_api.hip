@@ -56,6 +56,10 @@ umem_status check_desc(const umem_desc* d) {
   if (d->expand > kMaxExpand) return UMEM_ERR_UNSUPPORTED;
   if (!gather_row_supported(d->dv, d->vdtype)) return UMEM_ERR_UNSUPPORTED;
   if (d->dv_virt % 8 != 0 || d->d_out % 8 != 0) return UMEM_ERR_UNSUPPORTED;   // 16-byte weight rows
+  if (d->dv_virt > 0 && ((static_cast<int64_t>(d->expand) * d->dv) % 8 != 0 ||
+                         !gemm_weight_supported(d->dv_virt, static_cast<int64_t>(d->expand) * d->dv) ||
+                         !gemm_weight_supported(d->d_out, d->dv_virt)))
+    return UMEM_ERR_UNSUPPORTED;
   return UMEM_OK;
 }
 
@@ -138,8 +142,11 @@ umem_status check_project_shape(int32_t expand, int32_t dv, int32_t dv_virt, int
   if (expand < 1 || dv < 1 || dv_virt < 0 || d_out < 0) return UMEM_ERR_INVALID_ARG;
   if (has_proj != (dv_virt > 0) || has_out != (d_out > 0)) return UMEM_ERR_INVALID_ARG;
   if (!has_proj && (expand != 1 || d_out == 0)) return UMEM_ERR_INVALID_ARG;
-  // the GEMMs read 16-byte pieces: 4 fp32 of a pooled row, 8 bf16 of a weight row
-  if ((static_cast<int64_t>(expand) * dv) % 4 != 0 || dv_virt % 8 != 0 || d_out % 8 != 0)
+  // the GEMMs read 16-byte pieces of rows of K: 4 fp32 of a pooled row, 8 bf16 of a weight row
+  const int64_t k1 = static_cast<int64_t>(expand) * dv;
+  if (k1 % 8 != 0 || dv_virt % 8 != 0 || d_out % 8 != 0) return UMEM_ERR_UNSUPPORTED;
+  if (has_proj ? !gemm_weight_supported(dv_virt, k1) || (has_out && !gemm_weight_supported(d_out, dv_virt))
+               : !gemm_weight_supported(d_out, dv))
     return UMEM_ERR_UNSUPPORTED;
   return UMEM_OK;
 }
@@ -291,7 +298,8 @@ umem_status check_query_desc(const umem_query_desc* qd) {
   if ((qd->shared != 0 && qd->shared != 1) || !(qd->eps >= 0.0f) || qd->eps == INFINITY)
     return UMEM_ERR_INVALID_ARG;
   const int64_t nq = static_cast<int64_t>(qd->shared ? 1 : 2) * qd->heads * qd->dk;
-  if (qd->d_model % 4 != 0 || qd->conv_k > 8 || qd->dk > 1024 || nq % 8 != 0 || nq > (1 << 24))
+  if (qd->d_model % 8 != 0 || qd->conv_k > 8 || qd->dk > 1024 || nq % 8 != 0 || nq > (1 << 24) ||
+      !gemm_weight_supported(nq, qd->d_model))
     return UMEM_ERR_UNSUPPORTED;
   return UMEM_OK;
 }

@@ -67,10 +67,12 @@ hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* value
 inline int n_cores(const umem_desc& d) { return d.cores > 1 ? d.cores : 1; }
 bool cores_supported(int dv, int vdtype, int cores);
 
-// C [M, N] = bf16(A [M, K]) B [K, N] on MFMA with fp32 accumulation (A fp32, B bf16 bits, all
-// 16-byte aligned, K % 4 == 0, N % 8 == 0); part: gemm_partial_bytes(M, N, K) bytes of scratch
-// for the split-K partial sums (unused when that is 0).
+// C [M, N] = bf16(A [M, K]) B[N, K]^T on MFMA with fp32 accumulation (A fp32, B bf16 bits stored
+// output-major like a linear layer's weight, all 16-byte aligned, K % 8 == 0, N % 4 == 0);
+// part: gemm_partial_bytes(M, N, K) bytes of scratch for the split-K partial sums (unused when
+// that is 0).  gemm_weight_supported: B's bytes within the loads' 32-bit range.
 size_t gemm_partial_bytes(int M, int N, int K);
+inline bool gemm_weight_supported(int64_t N, int64_t K) { return N * K * 2 < (INT64_C(1) << 31); }
 hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
                      hipStream_t s);
 

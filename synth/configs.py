@@ -218,6 +218,12 @@ def value_table_host(cfg: Layer) -> np.ndarray:
     return x if cfg.vdtype == F32 else S.f32_to_bf16_bits(x).reshape(x.shape)
 
 
+def output_major(w: np.ndarray) -> np.ndarray:
+    """A weight drawn as [..., in, out] (the paper's W in x W) in the output-major layout of a linear
+    layer's weight, [out, in] with the leading axes folded into in: the layout the GPU takes."""
+    return np.ascontiguousarray(w.reshape(-1, w.shape[-1]).T)
+
+
 def projections(cfg: Layer):
     """IVE projectors W_p as bf16 bits [E, Dv, D'v] and output linear bf16 bits [D'v, d_out]."""
     if cfg.dv_virt == 0:

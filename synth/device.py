@@ -72,8 +72,8 @@ class DeviceLayer:
     core: Optional[torch.Tensor]     # [H, r, r] fp32
     values: torch.Tensor             # [N_p, Dv] fp32 or bf16
     perm: Optional[torch.Tensor]     # [E * N_p] int32
-    w_proj: Optional[torch.Tensor]   # [E, Dv, D'v] bf16 bits (int16)
-    w_out: Optional[torch.Tensor]    # [D'v, d_out] bf16 bits (int16)
+    w_proj: Optional[torch.Tensor]   # [D'v, E * Dv] bf16 bits (int16), output-major
+    w_out: Optional[torch.Tensor]    # [d_out, D'v] bf16 bits (int16), output-major
 
     @property
     def batches(self) -> int:
@@ -98,7 +98,8 @@ def make_layer(cfg: CF.Layer, batches: int = 1, values: Optional[torch.Tensor] =
     return DeviceLayer(cfg, q_row, q_col, _cuda(kr), _cuda(kc),
                        None if core is None else _cuda(core), values,
                        None if perm is None else _cuda(perm),
-                       None if wp is None else _cuda(wp), None if wo is None else _cuda(wo))
+                       None if wp is None else _cuda(CF.output_major(wp)),
+                       None if wo is None else _cuda(CF.output_major(wo)))
 
 
 def value_bytes(cfg: CF.Layer) -> int:

@@ -143,6 +143,9 @@ def test_entry_points_reject_before_launch():
     assert U.umem_project(8, 4, 512, 516, 2048, fake, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
     assert U.umem_project(8, 4, 512, 512, 2044, fake, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
     assert U.umem_project(8, 1, 6, 0, 64, fake, None, fake, fake, None, 0, 0) == U.UMEM_ERR_UNSUPPORTED
+    assert U.umem_project(8, 3, 4, 8, 64, fake, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED  # K = 12
+    # weights within the loads' 32-bit byte range: [8192, 4 * 65536] bf16 is 4 GiB
+    assert U.umem_project_workspace_size(8, 4, 65536, 8192, 0)[0] == U.UMEM_ERR_UNSUPPORTED
     assert U.umem_project(8, 4, 512, 512, 2048, fake, fake + 8, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
     assert U.umem_project(8, 4, 512, 512, 2048, fake + 4, fake, fake, fake, fake, 1 << 20, 0) == U.UMEM_ERR_UNSUPPORTED
     # forward: perm required iff expand > 1, projection weights iff D'v / d_out
@@ -186,6 +189,8 @@ def qdesc(**kw):
     (dict(eps=-1.0), U.UMEM_ERR_INVALID_ARG),
     (dict(eps=float("nan")), U.UMEM_ERR_INVALID_ARG),
     (dict(d_model=2046), U.UMEM_ERR_UNSUPPORTED),          # 16-byte pieces of a hidden row
+    (dict(d_model=2052), U.UMEM_ERR_UNSUPPORTED),          # 16-byte pieces of a weight row (bf16)
+    (dict(d_model=1 << 20, heads=8, dk=256, shared=0), U.UMEM_ERR_UNSUPPORTED),   # a 8 GiB weight
     (dict(conv_k=9), U.UMEM_ERR_UNSUPPORTED),
     (dict(dk=1028), U.UMEM_ERR_UNSUPPORTED),
     (dict(heads=1, dk=4), U.UMEM_ERR_UNSUPPORTED),         # 4 query outputs: not whole 16-byte pieces

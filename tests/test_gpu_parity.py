@@ -311,7 +311,8 @@ def test_project_standalone(T, E, dv, dvv, dout):
     st, nws = U.umem_project_workspace_size(T, E, dv, dvv, dout)
     U.check(st)
     ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
-    dev = lambda a: None if a is None else torch.from_numpy(a.view(np.int16)).cuda()
+    # the GPU takes the weights output-major ([out, in]), as a linear layer stores them
+    dev = lambda a: None if a is None else torch.from_numpy(CF.output_major(a).view(np.int16)).cuda()
     U.check(U.umem_project(T, E, dv, dvv, dout, torch.from_numpy(pooled).cuda(), dev(wp), dev(wo), out,
                            ws, ws.numel()))
     torch.cuda.synchronize()

@@ -53,7 +53,7 @@ def run_query(fe, inp=None):
     log(f"[case] query front-end {fe.name}: B={fe.B} L={fe.L} d={fe.d_model} K_c={fe.conv_k} "
         f"H={fe.heads} Dk={fe.dk} shared={fe.shared}")
     U.check(U.umem_query(qd, fe.B, fe.L, dev(inp["x"]), dev(inp["hist"]), dev(inp["conv_w"]),
-                         dev(inp["w_q"].view(np.int16)), dev(inp["gamma"]), dev(inp["beta"]),
+                         dev(CF.output_major(inp["w_q"]).view(np.int16)), dev(inp["gamma"]), dev(inp["beta"]),
                          q_row, q_col, ws, ws.numel()), "umem_query")
     torch.cuda.synchronize()
     return inp, q_row, (q_row if fe.shared else q_col), ws
