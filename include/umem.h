@@ -102,8 +102,10 @@ UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_
  *   core          fp32 [H, r, r]   Tucker cores (NULL for UMEM_GRID_ADD); [H, h, r, r] component
  *                                  cores with multi-core scoring (their sum is the core)
  *   sel           fp32 [2, T, H, n] out: [0] row scores, [1] column scores
- *   ws            scratch for the singular vectors, Tucker grid only (2 KiB, 256-byte aligned;
- *                 a workspace sized by umem_workspace_size suffices); may be NULL otherwise */
+ *   ws            256-byte aligned scratch: the singular vectors (Tucker grid, 2 KiB), then for
+ *                 T > 64 tokens the bf16 planes of the many-token kernel (2 * 3 * (T + n_keys) *
+ *                 heads * dk * 2 bytes where dk % 32 == 0 and n_keys % 4 == 0); a workspace sized
+ *                 by umem_workspace_size suffices; may be NULL where neither is needed */
 UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const float* q_row,
                                       const float* q_col, const float* k_row, const float* k_col,
                                       const float* core, float* sel, void* ws, size_t ws_bytes,

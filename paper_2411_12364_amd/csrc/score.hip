@@ -20,6 +20,8 @@
 //    streamed through LDS in chunks of DC dims.
 // With a rank-r core each slice's partial scores are multiplied by their factor (u or t) before
 // they are summed; for the additive grid the factor is 1.
+#include <algorithm>
+
 #include "umem_internal.h"
 
 namespace umem {
@@ -375,6 +377,201 @@ __global__ __launch_bounds__(THREADS) void axis_scores_wide(
   }
 }
 
+// ---------------------------------------------------------------- scores on bf16 matrix cores
+// For many tokens the scores are one GEMM per (head, axis): with the slice factors folded into
+// the query (sum_rho f_rho sum_{d in rho} q_d K_d = sum_d (f_rho(d) q_d) K_d), S = Q' K^T with
+// both operands rows of dk.  fp32 MFMA runs at 1/16 of the bf16 rate, so the GEMM is done on
+// bf16 MFMA in fp32 precision: each fp32 x is split exactly into three bf16 parts x = x1 + x2 + x3
+// (x1 = bf16(x), x2 = bf16(x - x1), x3 = x - x1 - x2; each part holds the next 8 bits of the
+// significand), and q . k = sum of the six products q_i k_j with i + j <= 4 (the three dropped
+// ones are below 2^-24 of the leading term).  Each product of two bf16 is exact in fp32 and the
+// MFMA accumulates in fp32, so the scores carry fp32-level rounding, at 6/16 of the fp32 MFMA
+// time.
+//
+// split_planes_kernel writes the three planes of Q' and K in the workspace, per (axis, plane,
+// head) a [rows, dk] block; axis_scores_x6 is a 128 x 128 tile of (tokens x keys) per
+// workgroup, four waves of 64 x 64 (4 x 4 v_mfma_f32_16x16x32_bf16 tiles x 6 products), dk in
+// steps of 32 through LDS with the next slice prefetched into registers, and the scores leave
+// through LDS as whole 128-byte lines (nontemporal).
+constexpr int XT = 128, XN = 128, XK = 32;
+constexpr int XLD = XK + 8;                   // LDS pitch in bf16 (80 B: fragment reads conflict-free)
+constexpr int XLDC = 64 + 4;                  // LDS pitch of the epilogue's fp32 rows
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// The three bf16 parts of x, most significant first, into element e of p[0], p[1], p[2].
+__device__ __forceinline__ void split3(float x, bf16x4* p, int e) {
+  const __bf16 a = static_cast<__bf16>(x);
+  const float r1 = x - static_cast<float>(a);        // exact
+  const __bf16 b = static_cast<__bf16>(r1);
+  p[0][e] = a;
+  p[1][e] = b;
+  p[2][e] = static_cast<__bf16>(r1 - static_cast<float>(b));   // exact: at most 8 bits left
+}
+
+// Queries (both axes, scaled by their slice factors) then keys, four dims per thread.  Planes:
+// Qp[axis][p][h][t][dk] (T rows per head), Kp[axis][p][h][i][dk].
+__global__ __launch_bounds__(THREADS) void split_planes_kernel(
+    const float* __restrict__ q_row, const float* __restrict__ q_col,
+    const float* __restrict__ k_row, const float* __restrict__ k_col,
+    const float* __restrict__ factors, int T, int H, int n, int dk, int width,
+    uint16_t* __restrict__ Qp, uint16_t* __restrict__ Kp) {
+  const int d4n = dk / 4;
+  const size_t nq = static_cast<size_t>(2) * T * H * d4n, nk = static_cast<size_t>(2) * H * n * d4n;
+  for (size_t x = static_cast<size_t>(blockIdx.x) * THREADS + threadIdx.x; x < nq + nk;
+       x += static_cast<size_t>(gridDim.x) * THREADS) {
+    const bool query = x < nq;
+    const size_t y = query ? x : x - nq;
+    const int d4 = static_cast<int>(y % d4n);
+    const size_t r = y / d4n;                          // (axis, t, h) or (axis, h, i)
+    int axis, h;
+    size_t src_row, dst_row, rows;
+    if (query) {
+      h = static_cast<int>(r % H);
+      const size_t at = r / H;
+      axis = static_cast<int>(at / T);
+      const size_t t = at % T;
+      src_row = t * H + h;
+      dst_row = static_cast<size_t>(h) * T + t;
+      rows = static_cast<size_t>(H) * T;
+    } else {
+      axis = static_cast<int>(r / (static_cast<size_t>(H) * n));
+      src_row = r % (static_cast<size_t>(H) * n);
+      h = static_cast<int>(src_row / n);
+      dst_row = src_row;
+      rows = static_cast<size_t>(H) * n;
+    }
+    const float* src = query ? (axis ? q_col : q_row) : (axis ? k_col : k_row);
+    float4 v = *reinterpret_cast<const float4*>(src + src_row * dk + 4 * d4);
+    if (query && factors != nullptr) {
+      const float f = factors[(h * 2 + axis) * kMaxRank + (4 * d4) / width];
+      v.x *= f; v.y *= f; v.z *= f; v.w *= f;
+    }
+    bf16x4 p[3];
+    split3(v.x, p, 0);
+    split3(v.y, p, 1);
+    split3(v.z, p, 2);
+    split3(v.w, p, 3);
+    uint16_t* dst = query ? Qp : Kp;
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl)
+      *reinterpret_cast<bf16x4*>(dst + ((static_cast<size_t>(axis) * 3 + pl) * rows + dst_row) * dk + 4 * d4) = p[pl];
+  }
+}
+
+// One 16-byte piece per thread and plane-row chunk: piece f of 3 * 128 * 4 (plane f / 512, row
+// (f % 512) / 4, dims 8 (f % 4) ..), six per thread per operand.
+struct XSlice {
+  u32x4 a[6], b[6];
+};
+
+__device__ __forceinline__ void x6_fetch(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Kb,
+                                         size_t qplane, size_t kplane, int T, int n, int dk,
+                                         int t0, int i0, int k0, int tid, XSlice& sl) {
+#pragma unroll
+  for (int j = 0; j < 6; ++j) {
+    const int f = tid + THREADS * j;
+    const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
+    const int t = t0 + row, i = i0 + row;
+    sl.a[j] = t < T ? *reinterpret_cast<const u32x4*>(Qa + pl * qplane + static_cast<size_t>(t) * dk + k0 + 8 * ch)
+                    : u32x4{0u, 0u, 0u, 0u};
+    sl.b[j] = i < n ? *reinterpret_cast<const u32x4*>(Kb + pl * kplane + static_cast<size_t>(i) * dk + k0 + 8 * ch)
+                    : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+__global__ __launch_bounds__(THREADS) void axis_scores_x6(
+    const uint16_t* __restrict__ Qp, const uint16_t* __restrict__ Kp, float* __restrict__ sel,
+    int T, int H, int n, int dk, float4* __restrict__ zero, int zero_n4) {
+  clear_with_grid(zero, zero_n4);
+  __shared__ __align__(16) uint16_t smem[2 * 3 * XT * XLD];   // [A | B][plane][row][k]
+  uint16_t* As = smem;
+  uint16_t* Bs = smem + 3 * XT * XLD;
+  const int axis = blockIdx.z & 1, h = blockIdx.z >> 1;
+  const int i0 = blockIdx.x * XN, t0 = blockIdx.y * XT;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;              // 64 tokens x 64 keys of the tile
+  const size_t qplane = static_cast<size_t>(H) * T * dk, kplane = static_cast<size_t>(H) * n * dk;
+  const uint16_t* Qa = Qp + static_cast<size_t>(axis) * 3 * qplane + static_cast<size_t>(h) * T * dk;
+  const uint16_t* Kb = Kp + static_cast<size_t>(axis) * 3 * kplane + static_cast<size_t>(h) * n * dk;
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  XSlice sl;
+  x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, 0, tid, sl);
+  for (int k0 = 0; k0 < dk; k0 += XK) {
+#pragma unroll
+    for (int j = 0; j < 6; ++j) {
+      const int f = tid + THREADS * j;
+      const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
+      *reinterpret_cast<u32x4*>(As + (pl * XT + row) * XLD + 8 * ch) = sl.a[j];
+      *reinterpret_cast<u32x4*>(Bs + (pl * XN + row) * XLD + 8 * ch) = sl.b[j];
+    }
+    __syncthreads();
+    if (k0 + XK < dk) x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + XK, tid, sl);
+    // lane: row (token or key) lane % 16 of a 16-block, dims 8 (lane / 16) ... + 7
+    bf16x8 af[3][4], bfr[3][4];
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        af[pl][a] = *reinterpret_cast<const bf16x8*>(As + (pl * XT + wm * 64 + a * 16 + (lane & 15)) * XLD + 8 * (lane >> 4));
+        bfr[pl][a] = *reinterpret_cast<const bf16x8*>(Bs + (pl * XN + wn * 64 + a * 16 + (lane & 15)) * XLD + 8 * (lane >> 4));
+      }
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        // the six products of significance 2^-16 and above, smaller ones first
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[2][a], bfr[0][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[1][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[2][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[0][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[1][b], acc[a][b], 0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[0][b], acc[a][b], 0, 0, 0);
+      }
+    __syncthreads();
+  }
+  // D layout: lane holds tokens 4 (lane / 16) + r of key lane % 16.  Each wave's 64 x 64 block
+  // leaves in two halves of 32 tokens through LDS (free after the last barrier), as 16-byte
+  // pieces: every token's 64 keys are 256 contiguous bytes of sel.
+  float* Cs = reinterpret_cast<float*>(smem) + wave * 32 * XLDC;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+#pragma unroll
+    for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          Cs[(a2 * 16 + 4 * (lane >> 4) + r) * XLDC + b * 16 + (lane & 15)] = acc[half * 2 + a2][b][r];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int row = (lane >> 4) + 4 * it, c4 = (lane & 15) * 4;
+      const int t = t0 + wm * 64 + half * 32 + row, key = i0 + wn * 64 + c4;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(Cs + row * XLDC + c4);
+      if (t < T && key < n)      // n % 4 == 0: the piece is whole
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n + key));
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+static_assert(4 * 32 * XLDC * 4 <= 2 * 3 * XT * XLD * 2, "epilogue staging fits the tiles' LDS");
+
+bool scores_use_x6(const umem_desc& d, int T) {
+  return T > 64 && d.dk % XK == 0 && d.n_keys % 4 == 0 && (d.dk / d.rank) % 4 == 0;
+}
+
 }  // namespace
 
 // One thread per head; with multi-core scoring the head's component cores are summed first
@@ -395,9 +592,15 @@ hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, h
   return hipGetLastError();
 }
 
+size_t score_planes_bytes(const umem_desc& d, int T) {
+  if (!scores_use_x6(d, T)) return 0;
+  return static_cast<size_t>(2) * 3 * (static_cast<size_t>(T) + d.n_keys) * d.heads * d.dk * sizeof(uint16_t);
+}
+
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
                               const float* k_row, const float* k_col, const float* factors,
-                              float* sel, float* zero_out, size_t zero_floats, hipStream_t s) {
+                              float* sel, float* zero_out, size_t zero_floats, void* planes,
+                              hipStream_t s) {
   float4* zero = reinterpret_cast<float4*>(zero_out);
   const int zero_n4 = zero_out ? static_cast<int>(zero_floats / 4) : 0;
   clear_stale_error();
@@ -425,6 +628,19 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
     else if (d.dk == 128) UMEM_WIDE(4);
     else UMEM_WIDE(8);
 #undef UMEM_WIDE
+    return hipGetLastError();
+  }
+  // (the x6 kernel stores 16-byte pieces of sel)
+  if (scores_use_x6(d, T) && planes != nullptr && reinterpret_cast<uintptr_t>(sel) % 16 == 0) {
+    uint16_t* Qp = static_cast<uint16_t*>(planes);
+    uint16_t* Kp = Qp + static_cast<size_t>(2) * 3 * T * d.heads * d.dk;
+    const size_t items = static_cast<size_t>(2) * (static_cast<size_t>(T) + d.n_keys) * d.heads * d.dk / 4;
+    const unsigned blocks = static_cast<unsigned>(std::min<size_t>((items + THREADS - 1) / THREADS, 8192));
+    hipLaunchKernelGGL(split_planes_kernel, dim3(blocks), dim3(THREADS), 0, s, q_row, q_col, k_row,
+                       k_col, c, T, d.heads, d.n_keys, d.dk, d.dk / d.rank, Qp, Kp);
+    dim3 grid((d.n_keys + XN - 1) / XN, (T + XT - 1) / XT, d.heads * 2);
+    hipLaunchKernelGGL(axis_scores_x6, grid, dim3(THREADS), 0, s, Qp, Kp, sel, T, d.heads, d.n_keys,
+                       d.dk, zero, zero_n4);
     return hipGetLastError();
   }
   // the key widths of the paper's UltraMem models (Kdim 256, 384, 448) and smaller powers of two

@@ -4,6 +4,8 @@
 
 #include <cmath>
 
+#include <algorithm>
+
 #include "umem_internal.h"
 
 using namespace umem;
@@ -83,7 +85,8 @@ struct Layout {
 };
 
 // Workspace: [rank-1 factors (Tucker)] [selection scores] [idx] [w] [pooled] [projection
-// scratch: the intermediate and split-K partials]
+// scratch: the intermediate and split-K partials; before the projection, the scoring's bf16
+// planes of queries and keys, dead once the scores are written]
 Layout layout(const umem_desc* d, int32_t T) {
   Layout L{};
   const size_t th = static_cast<size_t>(T) * d->heads;
@@ -100,8 +103,9 @@ Layout layout(const umem_desc* d, int32_t T) {
   if (d->dv_virt > 0 || d->d_out > 0)
     off += round_up(static_cast<size_t>(T) * d->expand * d->dv * sizeof(float));
   L.proj = off;
-  if (d->dv_virt > 0 || d->d_out > 0)
-    off += round_up(project_workspace_bytes(T, d->expand, d->dv, d->dv_virt, d->d_out));
+  const size_t proj = (d->dv_virt > 0 || d->d_out > 0)
+                          ? project_workspace_bytes(T, d->expand, d->dv, d->dv_virt, d->d_out) : 0;
+  off += round_up(std::max(proj, score_planes_bytes(*d, T)));
   L.total = off;
   return L;
 }
@@ -194,13 +198,18 @@ UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const fl
   if (st == UMEM_OK) st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
   if (st == UMEM_OK && (sel == nullptr || !aligned(sel, 4))) st = UMEM_ERR_INVALID_ARG;
   const bool tucker = desc->grid == UMEM_GRID_TUCKER;
-  if (st == UMEM_OK && tucker && (ws == nullptr || !aligned(ws, kAlign) || ws_bytes < kFactorBytes))
+  // [factors (Tucker)] [bf16 planes of the many-token path]
+  const size_t planes_at = tucker ? round_up(kFactorBytes) : 0;
+  const size_t planes = score_planes_bytes(*desc, T);
+  const size_t need = planes > 0 ? planes_at + planes : (tucker ? kFactorBytes : 0);
+  if (st == UMEM_OK && need > 0 && (ws == nullptr || !aligned(ws, kAlign) || ws_bytes < need))
     st = UMEM_ERR_WORKSPACE;
   if (st != UMEM_OK) return st;
   float* factors = tucker ? static_cast<float*>(ws) : nullptr;
   hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
   if (e == hipSuccess)
-    e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, factors, sel, nullptr, 0, stream);
+    e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, factors, sel, nullptr, 0,
+                           planes > 0 ? static_cast<char*>(ws) + planes_at : nullptr, stream);
   return hip_status(e);
 }
 
@@ -246,7 +255,7 @@ UMEM_API umem_status umem_score_topk(const umem_desc* desc, int32_t T, const flo
   hipError_t e = tucker ? launch_rank1(*desc, core, factors, stream) : hipSuccess;
   if (e == hipSuccess)
     e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, tucker ? factors : nullptr, sel,
-                           nullptr, 0, stream);
+                           nullptr, 0, static_cast<char*>(ws) + L.proj, stream);
   if (e == hipSuccess)
     e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, axis_idx, nullptr,
                       nullptr, stream);
@@ -465,7 +474,8 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
   const bool fused = !project && select_pools(*desc) && T <= kMaxPoolTokens;
   if (e == hipSuccess)
     e = launch_axis_scores(*desc, T, q_row, q_col, k_row, k_col, tucker ? factors : nullptr, sel,
-                           fused ? out : nullptr, static_cast<size_t>(T) * desc->dv, stream);
+                           fused ? out : nullptr, static_cast<size_t>(T) * desc->dv,
+                           base + L.proj, stream);
   if (e == hipSuccess)
     e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, nullptr,
                       fused ? values : nullptr, fused ? out : nullptr, stream);

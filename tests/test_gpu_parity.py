@@ -160,8 +160,11 @@ def test_exact_ties_lower_index(kw):
     dict(T=100, heads=1, dk=256, n_keys=130, rank=2, grid=CF.GRID_TUCKER),    # tiled MFMA
     dict(T=70, heads=3, dk=64, n_keys=200),                                   # tiled MFMA
     dict(T=5, heads=2, dk=12, n_keys=33, rank=3, grid=CF.GRID_TUCKER),        # vector ALU
+    # many tokens on bf16 planes: ragged token and key tiles, three dk steps; dk = 448
+    dict(T=200, heads=3, dk=96, n_keys=300, rank=2, grid=CF.GRID_TUCKER),
+    dict(T=130, heads=1, dk=448, n_keys=260),
 ], ids=["split", "split-tucker2", "split-tucker4", "split-dk256", "tiled-tucker2", "tiled",
-        "valu-tucker3"])
+        "valu-tucker3", "planes-tucker2", "planes-dk448"])
 def test_axis_scores_kernels(kw):
     cfg = small("scores", topk=4, topm=4, **kw)
     log(f"[case] axis scores {kw}")
