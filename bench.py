@@ -361,6 +361,8 @@ def workload_report(cfg, steps=50, warmup=5):
                gather_unique_GBps=round(uniq / (st["gather_kernel"] * 1e-6) / 1e9, 1),
                gather_logical_GBps=round(g["row_bytes"] / (st["gather_kernel"] * 1e-6) / 1e9, 1))
     rep["backward"] = backward_report(r)
+    if cfg.name in overlap_stand_ins():
+        rep["overlap"] = overlap_report(r, *overlap_stand_ins()[cfg.name])
     fe = front_ends().get(cfg.name)
     if fe is not None:
         rep["front_end"] = front_end_report(fe)
@@ -475,6 +477,82 @@ def backward_report(r, launches=20):
                                              avg_us=round(g_us, 3), algorithmic_bytes=algo))
     del dV, ws1, ws2
     return out
+
+
+def overlap_stand_ins():
+    """Layer name -> (hidden width, MLP width, transformer layers spanned) of the dense work the
+    memory layer can run beside: in UltraMem-1.6B each memory layer takes layer 3's output and
+    adds into layer 7's (insertion 3:7/8:12/...), so it spans four layers of hidden 2048, MLP
+    8192."""
+    from synth import configs as CF
+    return {CF.C6.name: (2048, 8192, 4)}
+
+
+def overlap_report(r, d_model, d_ff, layers, launches=10):
+    """The memory layer beside the dense layers (the skip-layer structure of Sec. 3.2 and the
+    asynchronous execution of the appendix): ``launches`` forwards of runner ``r``'s layer on one
+    stream and ``launches`` passes of a stand-in for the dense layers it spans on another, each
+    replayed from its own HIP graph, timed alone and concurrently.  The stand-in is the bf16
+    GEMMs of ``layers`` transformer layers over the layer's tokens (QKV and output projections,
+    MLP up and down; random weights, distinct per layer); attention's own softmax and cache reads
+    are left out."""
+    torch, c = r.torch, r.cfg
+    x = torch.randn((c.T, d_model), dtype=torch.bfloat16, device="cuda")
+    ws = [(torch.randn((d_model, 3 * d_model), dtype=torch.bfloat16, device="cuda") / d_model ** 0.5,
+           torch.randn((d_model, d_model), dtype=torch.bfloat16, device="cuda") / d_model ** 0.5,
+           torch.randn((d_model, d_ff), dtype=torch.bfloat16, device="cuda") / d_model ** 0.5,
+           torch.randn((d_ff, d_model), dtype=torch.bfloat16, device="cuda") / d_ff ** 0.5)
+          for _ in range(layers)]
+
+    def dense():
+        for wqkv, wo, w1, w2 in ws:
+            torch.mm(x, wqkv)
+            torch.mm(x, wo)
+            torch.mm(torch.mm(x, w1), w2)
+
+    def capture(fns):
+        for f in fns[:2]:
+            f()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for f in fns:
+                f()
+        return g
+    g_mem = capture([lambda b=b: r.forward(b % r.R) for b in range(launches)])
+    g_dense = capture([dense] * launches)
+    s_mem, s_dense = torch.cuda.Stream(), torch.cuda.Stream()     # default priority
+
+    def timed(which):
+        main = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        done = []
+        e0.record(main)
+        for g, s in which:
+            s.wait_event(e0)
+            with torch.cuda.stream(s):
+                g.replay()
+            ev = torch.cuda.Event()
+            ev.record(s)
+            done.append(ev)
+        for ev in done:
+            main.wait_event(ev)
+        e1.record(main)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / launches
+    for _ in range(2):
+        timed([(g_mem, s_mem), (g_dense, s_dense)])
+    mem_us = timed([(g_mem, s_mem)])
+    dense_us = timed([(g_dense, s_dense)])
+    both_us = timed([(g_mem, s_mem), (g_dense, s_dense)])
+    dense_flops = layers * 2 * c.T * (4 * d_model * d_model + 2 * d_model * d_ff)
+    del g_mem, g_dense, ws
+    return dict(dense_stand_in=(f"bf16 GEMMs of {layers} transformer layers (hidden {d_model}, MLP "
+                                f"{d_ff}) over {c.T} tokens"),
+                memory_layer_us=round(mem_us, 2), dense_us=round(dense_us, 2),
+                dense_TFLOPs=round(dense_flops / (dense_us * 1e-6) / 1e12, 1),
+                sequential_us=round(mem_us + dense_us, 2), concurrent_us=round(both_us, 2),
+                memory_layer_hidden_frac=round((mem_us + dense_us - both_us) / mem_us, 3))
 
 
 def front_ends():
