@@ -306,7 +306,7 @@ class Runner:
 
 def scores_on_planes(cfg, T):
     """Whether the scoring of T tokens takes the bf16-plane kernel (the library's own rule)."""
-    return T > 64 and cfg.dk % 32 == 0 and cfg.n_keys % 4 == 0 and (cfg.dk // cfg.rank) % 4 == 0
+    return T > 64 and cfg.dk % 32 == 0 and cfg.n_keys % 4 == 0 and (cfg.dk // cfg.rank) % 8 == 0
 
 
 def roofline_for(cfg, T, name, avg_us, workload, fused):

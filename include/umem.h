@@ -104,7 +104,8 @@ UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_
  *   sel           fp32 [2, T, H, n] out: [0] row scores, [1] column scores
  *   ws            256-byte aligned scratch: the singular vectors (Tucker grid, 2 KiB), then for
  *                 T > 64 tokens the bf16 planes of the many-token kernel (2 * 3 * (T + n_keys) *
- *                 heads * dk * 2 bytes where dk % 32 == 0 and n_keys % 4 == 0); a workspace sized
+ *                 heads * dk * 2 bytes where dk % 32 == 0, (dk / rank) % 8 == 0 and n_keys % 4 ==
+ *                 0); a workspace sized
  *                 by umem_workspace_size suffices; may be NULL where neither is needed */
 UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const float* q_row,
                                       const float* q_col, const float* k_row, const float* k_col,

@@ -398,34 +398,24 @@ constexpr int XLD = XK + 8;                   // LDS pitch in bf16 (80 B: fragme
 constexpr int XLDC = 64 + 4;                  // LDS pitch of the epilogue's fp32 rows
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// The three bf16 parts of x, most significant first, into element e of p[0], p[1], p[2].
-__device__ __forceinline__ void split3(float x, bf16x4* p, int e) {
-  const __bf16 a = static_cast<__bf16>(x);
-  const float r1 = x - static_cast<float>(a);        // exact
-  const __bf16 b = static_cast<__bf16>(r1);
-  p[0][e] = a;
-  p[1][e] = b;
-  p[2][e] = static_cast<__bf16>(r1 - static_cast<float>(b));   // exact: at most 8 bits left
-}
-
-// Queries (both axes, scaled by their slice factors) then keys, four dims per thread.  Planes:
-// Qp[axis][p][h][t][dk] (T rows per head), Kp[axis][p][h][i][dk].
+// Queries (both axes, scaled by their slice factors) then keys, eight dims per thread (two
+// 16-byte loads, one 16-byte store per plane).  Planes: Qp[axis][p][h][t][dk] (T rows per head),
+// Kp[axis][p][h][i][dk].
 __global__ __launch_bounds__(THREADS) void split_planes_kernel(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
     const float* __restrict__ factors, int T, int H, int n, int dk, int width,
     uint16_t* __restrict__ Qp, uint16_t* __restrict__ Kp) {
-  const int d4n = dk / 4;
-  const size_t nq = static_cast<size_t>(2) * T * H * d4n, nk = static_cast<size_t>(2) * H * n * d4n;
+  const int d8n = dk / 8;
+  const size_t nq = static_cast<size_t>(2) * T * H * d8n, nk = static_cast<size_t>(2) * H * n * d8n;
   for (size_t x = static_cast<size_t>(blockIdx.x) * THREADS + threadIdx.x; x < nq + nk;
        x += static_cast<size_t>(gridDim.x) * THREADS) {
     const bool query = x < nq;
     const size_t y = query ? x : x - nq;
-    const int d4 = static_cast<int>(y % d4n);
-    const size_t r = y / d4n;                          // (axis, t, h) or (axis, h, i)
+    const int d8 = static_cast<int>(y % d8n);
+    const size_t r = y / d8n;                          // (axis, t, h) or (axis, h, i)
     int axis, h;
     size_t src_row, dst_row, rows;
     if (query) {
@@ -443,21 +433,29 @@ __global__ __launch_bounds__(THREADS) void split_planes_kernel(
       dst_row = src_row;
       rows = static_cast<size_t>(H) * n;
     }
-    const float* src = query ? (axis ? q_col : q_row) : (axis ? k_col : k_row);
-    float4 v = *reinterpret_cast<const float4*>(src + src_row * dk + 4 * d4);
+    const float* src = (query ? (axis ? q_col : q_row) : (axis ? k_col : k_row)) + src_row * dk + 8 * d8;
+    const float4 v0 = *reinterpret_cast<const float4*>(src);
+    const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
+    float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
     if (query && factors != nullptr) {
-      const float f = factors[(h * 2 + axis) * kMaxRank + (4 * d4) / width];
-      v.x *= f; v.y *= f; v.z *= f; v.w *= f;
+      const float f = factors[(h * 2 + axis) * kMaxRank + (8 * d8) / width];   // width % 8 == 0
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] *= f;
     }
-    bf16x4 p[3];
-    split3(v.x, p, 0);
-    split3(v.y, p, 1);
-    split3(v.z, p, 2);
-    split3(v.w, p, 3);
+    bf16x8 p[3];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const __bf16 a = static_cast<__bf16>(v[e]);
+      const float r1 = v[e] - static_cast<float>(a);            // exact
+      const __bf16 b = static_cast<__bf16>(r1);
+      p[0][e] = a;
+      p[1][e] = b;
+      p[2][e] = static_cast<__bf16>(r1 - static_cast<float>(b));   // exact: at most 8 bits left
+    }
     uint16_t* dst = query ? Qp : Kp;
 #pragma unroll
     for (int pl = 0; pl < 3; ++pl)
-      *reinterpret_cast<bf16x4*>(dst + ((static_cast<size_t>(axis) * 3 + pl) * rows + dst_row) * dk + 4 * d4) = p[pl];
+      *reinterpret_cast<bf16x8*>(dst + ((static_cast<size_t>(axis) * 3 + pl) * rows + dst_row) * dk + 8 * d8) = p[pl];
   }
 }
 
@@ -569,7 +567,7 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
 static_assert(4 * 32 * XLDC * 4 <= 2 * 3 * XT * XLD * 2, "epilogue staging fits the tiles' LDS");
 
 bool scores_use_x6(const umem_desc& d, int T) {
-  return T > 64 && d.dk % XK == 0 && d.n_keys % 4 == 0 && (d.dk / d.rank) % 4 == 0;
+  return T > 64 && d.dk % XK == 0 && d.n_keys % 4 == 0 && (d.dk / d.rank) % 8 == 0;
 }
 
 }  // namespace
@@ -634,7 +632,7 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
   if (scores_use_x6(d, T) && planes != nullptr && reinterpret_cast<uintptr_t>(sel) % 16 == 0) {
     uint16_t* Qp = static_cast<uint16_t*>(planes);
     uint16_t* Kp = Qp + static_cast<size_t>(2) * 3 * T * d.heads * d.dk;
-    const size_t items = static_cast<size_t>(2) * (static_cast<size_t>(T) + d.n_keys) * d.heads * d.dk / 4;
+    const size_t items = static_cast<size_t>(2) * (static_cast<size_t>(T) + d.n_keys) * d.heads * d.dk / 8;
     const unsigned blocks = static_cast<unsigned>(std::min<size_t>((items + THREADS - 1) / THREADS, 8192));
     hipLaunchKernelGGL(split_planes_kernel, dim3(blocks), dim3(THREADS), 0, s, q_row, q_col, k_row,
                        k_col, c, T, d.heads, d.n_keys, d.dk, d.dk / d.rank, Qp, Kp);
