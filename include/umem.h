@@ -175,7 +175,8 @@ UMEM_API umem_status umem_project_workspace_size(int32_t T, int32_t expand, int3
  *   ws      16-byte aligned scratch of umem_project_workspace_size(...) bytes (NULL if 0)
  * The result does not depend on timing (split reductions add their partials in a fixed order).
  * UMEM_ERR_UNSUPPORTED unless pooled, w_proj and w_out are 16-byte aligned, expand * dv,
- * dv_virt and d_out are multiples of 8, and each weight is below 2 GiB. */
+ * dv_virt and d_out are multiples of 8, each weight is below 2 GiB and each GEMM's inner
+ * dimension (expand * dv, dv_virt) is at most 2^20. */
 UMEM_API umem_status umem_project(int32_t T, int32_t expand, int32_t dv, int32_t dv_virt, int32_t d_out,
                          const float* pooled, const uint16_t* w_proj, const uint16_t* w_out,
                          float* out, void* ws, size_t ws_bytes, hipStream_t stream);
@@ -252,7 +253,7 @@ typedef struct umem_query_desc {
 } umem_query_desc;
 /* Requirements (UMEM_ERR_INVALID_ARG otherwise): every count >= 1, shared 0 or 1, eps >= 0.
  * Limits (UMEM_ERR_UNSUPPORTED beyond them): d_model % 8 == 0; conv_k <= 8; dk <= 1024;
- *   (shared ? 1 : 2) * heads * dk a multiple of 8; the query weight below 2 GiB. */
+ *   (shared ? 1 : 2) * heads * dk a multiple of 8; the query weight below 2 GiB; d_model <= 2^20. */
 
 /* Scratch bytes umem_query needs for B sequences of L tokens. */
 UMEM_API umem_status umem_query_workspace_size(const umem_query_desc* qd, int32_t B, int32_t L,

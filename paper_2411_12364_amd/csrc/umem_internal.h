@@ -74,9 +74,12 @@ bool cores_supported(int dv, int vdtype, int cores);
 // C [M, N] = bf16(A [M, K]) B[N, K]^T on MFMA with fp32 accumulation (A fp32, B bf16 bits stored
 // output-major like a linear layer's weight, all 16-byte aligned, K % 8 == 0, N % 4 == 0);
 // part: gemm_partial_bytes(M, N, K) bytes of scratch for the split-K partial sums (unused when
-// that is 0).  gemm_weight_supported: B's bytes within the loads' 32-bit range.
+// that is 0).  gemm_weight_supported: B's bytes within the loads' 32-bit range, and K small
+// enough that a band of 128 rows of A does too (A is launched in bands below 2 GiB).
 size_t gemm_partial_bytes(int M, int N, int K);
-inline bool gemm_weight_supported(int64_t N, int64_t K) { return N * K * 2 < (INT64_C(1) << 31); }
+inline bool gemm_weight_supported(int64_t N, int64_t K) {
+  return N * K * 2 < (INT64_C(1) << 31) && K <= (INT64_C(1) << 20);
+}
 hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
                      hipStream_t s);
 

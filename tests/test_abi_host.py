@@ -191,6 +191,7 @@ def qdesc(**kw):
     (dict(d_model=2046), U.UMEM_ERR_UNSUPPORTED),          # 16-byte pieces of a hidden row
     (dict(d_model=2052), U.UMEM_ERR_UNSUPPORTED),          # 16-byte pieces of a weight row (bf16)
     (dict(d_model=1 << 20, heads=8, dk=256, shared=0), U.UMEM_ERR_UNSUPPORTED),   # a 8 GiB weight
+    (dict(d_model=1 << 21, heads=1, dk=4, shared=0), U.UMEM_ERR_UNSUPPORTED),     # K beyond 2^20
     (dict(conv_k=9), U.UMEM_ERR_UNSUPPORTED),
     (dict(dk=1028), U.UMEM_ERR_UNSUPPORTED),
     (dict(heads=1, dk=4), U.UMEM_ERR_UNSUPPORTED),         # 4 query outputs: not whole 16-byte pieces
