@@ -214,3 +214,57 @@ def test_score_backward_deterministic():
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+def test_backward_graph_replay_matches_eager():
+    """Both backward entry points captured in a HIP graph (with the clearing of their accumulated
+    outputs by fill kernels), replayed several times with eager work in between, give the eager
+    results bit for bit: their piece counters and lists are rebuilt by kernels on every call."""
+    cfg = SCORE_CASES[-1]                  # Tucker r = 4, 64 slots, rows shared by many tokens
+    dl = SD.make_layer(cfg)
+    idx, w, _ = G.score_topk(dl, cfg.T, 0)
+    torch.cuda.synchronize()
+    T, bag = cfg.T, cfg.heads * cfg.topm
+    desc = G.desc_for(cfg)
+    dp = torch.randn((T, cfg.expand, cfg.dv), dtype=torch.float32, device="cuda")
+    dwin = torch.randn_like(w)
+    st, n1 = U.umem_gather_backward_workspace_size(T, bag, cfg.dv)
+    U.check(st)
+    st, n2 = U.umem_score_backward_workspace_size(desc, T)
+    U.check(st)
+    ws1 = torch.empty(max(n1, 256), dtype=torch.uint8, device="cuda")
+    ws2 = torch.empty(max(n2, 256), dtype=torch.uint8, device="cuda")
+    dV = torch.empty((cfg.n_values, cfg.dv), dtype=torch.float32, device="cuda")
+    dw = torch.empty((T, bag), dtype=torch.float32, device="cuda")
+    dq_r, dq_c = torch.empty_like(dl.q_row[0]), torch.empty_like(dl.q_col[0])
+    dk_r, dk_c = torch.empty_like(dl.k_row), torch.empty_like(dl.k_col)
+    dc = torch.empty_like(dl.core)
+    outs = (dV, dw, dq_r, dq_c, dk_r, dk_c, dc)
+
+    def step():
+        for t in (dV, dk_r, dk_c, dc):          # accumulated outputs start from zero
+            t.zero_()
+        U.check(U.umem_gather_backward(cfg.n_values, cfg.dv, cfg.vdtype, dl.values, T, bag,
+                                       idx.reshape(T, bag), w.reshape(T, bag), dl.perm, cfg.expand,
+                                       cfg.cores, dp, dV, dw, ws1, ws1.numel()), "umem_gather_backward")
+        U.check(U.umem_score_backward(desc, T, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core,
+                                      idx, w, dwin, dq_r, dq_c, dk_r, dk_c, dc, ws2, ws2.numel()),
+                "umem_score_backward")
+
+    step()
+    torch.cuda.synchronize()
+    want = [t.clone() for t in outs]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(4):
+        for t in outs:
+            t.fill_(-1.0)
+        ws1.fill_(0xAB)                      # stale counters and lists from any earlier call
+        ws2.fill_(0xCD)
+        g.replay()
+        torch.cuda.synchronize()
+        for got, ref in zip(outs, want):
+            assert torch.equal(got, ref), rep
+        step()                               # eager work between replays
+        torch.cuda.synchronize()
