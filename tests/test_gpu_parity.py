@@ -400,6 +400,44 @@ def test_hip_graph_replay_matches_eager():
         torch.cuda.synchronize()
 
 
+def test_graph_replay_projected_layer_stale_workspace():
+    """A Tucker + IVE layer with projection at 130 tokens (scoring on bf16 planes, the expanded
+    gather, the projection with a split K) captured in a HIP graph and replayed with a
+    garbage-filled workspace and eager work between replays gives the eager results bit for
+    bit: nothing reads the workspace before writing it."""
+    cfg = small("graph-ive", T=130, heads=2, dk=64, n_keys=96, topk=16, topm=24, dv=512,
+                vdtype=CF.BF16, rank=2, grid=CF.GRID_TUCKER, expand=4, dv_virt=64, d_out=128)
+    dl = SD.make_layer(cfg)
+    desc = G.desc_for(cfg)
+    T = cfg.T
+    ws = G.workspace(desc, T)
+    out = torch.empty((T, cfg.d_out), dtype=torch.float32, device="cuda")
+    idx = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.float32, device="cuda")
+
+    def step():
+        U.check(U.umem_forward(desc, T, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core,
+                               dl.values, dl.perm, dl.w_proj, dl.w_out, out, idx, w, ws, ws.numel()),
+                "umem_forward")
+
+    step()
+    torch.cuda.synchronize()
+    want = (out.clone(), idx.clone(), w.clone())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(4):
+        out.fill_(-1.0)
+        w.fill_(-1.0)
+        idx.fill_(-1)
+        ws.fill_(0x5A)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, want[0]) and torch.equal(idx, want[1]) and torch.equal(w, want[2]), rep
+        step()
+        torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("kw", [
     dict(T=3, heads=2, n_keys=2048, topk=32, topm=32, dv=8, vdtype=CF.BF16),        # float4 loads
     dict(T=2, heads=1, n_keys=1001, topk=20, topm=50, dv=8, vdtype=CF.BF16),        # scalar loads
