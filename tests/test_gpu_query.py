@@ -103,6 +103,43 @@ def test_query_deterministic():
     assert torch.equal(a, b)
 
 
+def test_query_graph_replay_stale_workspace():
+    """The 1.6B-x12 front-end (convolution, split-K query linear, LayerNorm) captured in a HIP
+    graph and replayed over a garbage-filled workspace, with eager work between replays, gives
+    the eager queries bit for bit."""
+    fe = CF.FE6
+    inp = CF.front_end_inputs(fe)
+    qd = qdesc(fe)
+    st, nws = U.umem_query_workspace_size(qd, fe.B, fe.L)
+    U.check(st)
+    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
+    dev = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    x, hist, cw = dev(inp["x"]), dev(inp["hist"]), dev(inp["conv_w"])
+    wq = dev(CF.output_major(inp["w_q"]).view(np.int16))
+    g_, b_ = dev(inp["gamma"]), dev(inp["beta"])
+    q_row = torch.empty((fe.T, fe.heads, fe.dk), dtype=torch.float32, device="cuda")
+    q_col = None if fe.shared else torch.empty_like(q_row)
+
+    def step():
+        U.check(U.umem_query(qd, fe.B, fe.L, x, hist, cw, wq, g_, b_, q_row, q_col, ws, ws.numel()),
+                "umem_query")
+
+    step()
+    torch.cuda.synchronize()
+    want = q_row.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(4):
+        q_row.fill_(-1.0)
+        ws.fill_(0x3C)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(q_row, want), rep
+        step()
+        torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("H,n,dk", [(2, 300, 64), (4, 2048, 128), (2, 1792, 448), (1, 5, 1000)])
 def test_key_norm(H, n, dk):
     cfg = CF.Layer("keys", T=1, heads=H, dk=dk, n_keys=n, topk=1, topm=1, dv=8, vdtype=CF.F32, seed=40 + dk)
