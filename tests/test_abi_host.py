@@ -108,6 +108,14 @@ def test_entry_points_reject_before_launch():
     tucker = desc(grid=1, rank=2)
     assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, fake, fake, None, 0, 0) == U.UMEM_ERR_WORKSPACE
+    # more than 64 tokens: the bf16 planes of the scoring need their scratch after the factors
+    planes = 2 * 3 * (100 + 4480) * 2 * 128 * 2
+    st, nfull = U.umem_workspace_size(tucker, 100)
+    assert st == U.UMEM_OK and nfull >= 2048 + planes
+    assert U.umem_axis_scores(tucker, 100, fake, fake, fake, fake, fake, fake, fake, 2048, 0) == U.UMEM_ERR_WORKSPACE
+    assert U.umem_axis_scores(tucker, 100, fake, fake, fake, fake, fake, fake, fake, 2048 + planes - 1, 0) == U.UMEM_ERR_WORKSPACE
+    additive = desc()
+    assert U.umem_axis_scores(additive, 100, fake, fake, fake, fake, None, fake, None, 0, 0) == U.UMEM_ERR_WORKSPACE
     assert U.umem_select(d, 8, None, None, None, None, None, None, fake, fake, None, None, None, 0) == U.UMEM_ERR_INVALID_ARG
     # select with pooling: values and pooled together, aligned, and only where the layer allows
     assert U.umem_select(d, 8, fake, None, None, None, None, None, fake, fake, None, None, fake, 0) == U.UMEM_ERR_INVALID_ARG
