@@ -236,6 +236,13 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
       acc[k] = 0.0f;
     }
     if (active) Chunk<Elem>::load(vrow + col, x);
+    // a whole run adds into its gradient row: read that row now, under the entries' loads
+    const bool whole = run_start && run_end;
+    f32x4 old[EPC / 4];
+#pragma unroll
+    for (int k = 0; k < EPC / 4; ++k)
+      old[k] = (active && whole) ? *reinterpret_cast<const f32x4*>(d_values + static_cast<size_t>(row) * dv + col + 4 * k)
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j0 = 0; j0 < n_e; j0 += kInFlight) {    // wave-uniform
       int ent[kInFlight];
       float wt[kInFlight];
@@ -281,13 +288,12 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
       }
     }
     if (!active) continue;
-    if (run_start && run_end) {                       // a whole run: add into its row
+    if (whole) {                                      // a whole run: add into its row
 #pragma unroll
       for (int k = 0; k < EPC; k += 4) {
-        f32x4* dst = reinterpret_cast<f32x4*>(d_values + static_cast<size_t>(row) * dv + col + k);
-        f32x4 v = *dst;
+        f32x4 v = old[k / 4];
         v.x += acc[k]; v.y += acc[k + 1]; v.z += acc[k + 2]; v.w += acc[k + 3];
-        *dst = v;
+        *reinterpret_cast<f32x4*>(d_values + static_cast<size_t>(row) * dv + col + k) = v;
       }
     } else {                                          // cut by a segment edge: its partial row
       float* dst = partial + (static_cast<size_t>(2) * g + (run_start ? 1 : 0)) * dv + col;
@@ -651,6 +657,9 @@ __global__ __launch_bounds__(THREADS) void key_bwd_seg_kernel(
     const bool active = d < dk;
     const int r = active ? d / width : 0;             // four consecutive dims lie in one slice
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    // a whole run adds into its key's gradient row: read it now, under the entries' loads
+    const f32x4 old = (active && run_start && run_end) ? *reinterpret_cast<const f32x4*>(dK + d)
+                                                       : f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j0 = 0; j0 < n_e; j0 += 2 * kInFlight) {  // wave-uniform
       f32x4 qv[2 * kInFlight];
       float ds[2 * kInFlight];
@@ -677,10 +686,7 @@ __global__ __launch_bounds__(THREADS) void key_bwd_seg_kernel(
     }
     if (!active) continue;
     if (run_start && run_end) {
-      f32x4* dst = reinterpret_cast<f32x4*>(dK + d);
-      f32x4 v = *dst;
-      v += acc;
-      *dst = v;
+      *reinterpret_cast<f32x4*>(dK + d) = old + acc;
     } else {
       *reinterpret_cast<f32x4*>(partial + (static_cast<size_t>(2) * g + (run_start ? 1 : 0)) * dk + d) = acc;
     }
