@@ -144,6 +144,20 @@ __device__ __forceinline__ int group_sum(int r, int lp) {
   return r;
 }
 
+// The same for floats (IEEE addition commutes, so every lane of a group gets the same bits).
+__device__ __forceinline__ float group_sum_f(float x, int lp) {
+  int r = __builtin_bit_cast(int, x);
+#define UMEM_FSTEP(CTRL) \
+  r = __builtin_bit_cast(int, __builtin_bit_cast(float, r) + \
+                         __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, r, CTRL, 0xF, 0xF, false)))
+  if (lp >= 1) UMEM_FSTEP(0xB1);
+  if (lp >= 2) UMEM_FSTEP(0x4E);
+  if (lp >= 3) UMEM_FSTEP(0x141);
+  if (lp >= 4) UMEM_FSTEP(0x140);
+#undef UMEM_FSTEP
+  return __builtin_bit_cast(float, r);
+}
+
 // Exclusive offset of each thread's count within waves [w0, w0 + nw), and their total.
 // Called by every thread of the workgroup (it holds two barriers).
 __device__ __forceinline__ int2 group_offsets(int cnt, int w0, int nw, SelectShared& sh) {
@@ -550,6 +564,14 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
   }
   if (tid < 2) sh.ax_cnt[tid] = 0;
   if (tid == 0) sh.grid_cnt = 0;
+  // Tucker: the token's two query rows (2 dk / 4 <= THREADS 16-byte pieces), loaded now, staged
+  // in LDS for the exact per-slice scores once the axes are done with it
+  const int n4 = dk >> 2;
+  f32x4 q_piece = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (tucker && tid < 2 * n4) {
+    const int ax = tid >= n4;
+    q_piece = reinterpret_cast<const f32x4*>((ax ? q_col : q_row) + (static_cast<size_t>(t) * H + h) * dk)[tid - (ax ? n4 : 0)];
+  }
   select_axes<NV, VEC, MODE>(sel, T, H, t, h, n, k, m, !tucker, reinterpret_cast<uint64_t*>(dyn), sh);
   if (axis_out != nullptr)
     for (int a = tid; a < 2 * k; a += THREADS)
@@ -595,46 +617,48 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     __syncthreads();
     S = sh.grid_cnt;
   } else {
-    // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32.  Four
-    // lanes (a quad) per (axis, key) row, each a quarter of its dk elements in 16-byte pieces
-    // (four in flight at a time); the quad's partial sums are added with DPP.
+    // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32.  G = 4, 8
+    // or 16 lanes per (axis, key) row, as many as 2k rows leave in the workgroup (one pass); lane
+    // p of a group takes the row's 16-byte pieces p, p + G, ... (the group reads contiguous
+    // 16G-byte runs), eight loads in flight before any is used; the group's partial sums per
+    // slice are added with DPP.
     {
+      const f32x4* qs = reinterpret_cast<const f32x4*>(dyn);          // [2][n4] query pieces
+      if (tid < 2 * n4) reinterpret_cast<f32x4*>(dyn)[tid] = q_piece;
+      __syncthreads();
+      constexpr int kPieces = 8;
       const int width = dk / rank;
-      const int n4 = dk >> 2;                           // 16-byte pieces per row
-      for (int job = tid; job < 8 * k; job += THREADS) {   // whole quads: 8k is a multiple of 4
-        const int part = job & 3, row = job >> 2;
+      const int lg = 2 * k <= 32 ? 4 : (2 * k <= 64 ? 3 : 2);
+      const int G = 1 << lg;
+      for (int job = tid; job < (2 * k) << lg; job += THREADS) {   // whole groups: G | THREADS
+        const int part = job & (G - 1), row = job >> lg;
         const int axis = row >= k, a = row - (axis ? k : 0);
-        const float4* kr = reinterpret_cast<const float4*>(
+        const f32x4* kr = reinterpret_cast<const f32x4*>(
             (axis ? k_col : k_row) + (static_cast<size_t>(h) * n + sh.ax_idx[axis][a]) * dk);
-        const float4* qr = reinterpret_cast<const float4*>(
-            (axis ? q_col : q_row) + (static_cast<size_t>(t) * H + h) * dk);
-        const int f1 = ((part + 1) * n4) >> 2;
+        const f32x4* qr = qs + axis * n4;
         float acc[kMaxRank] = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (int f0 = (part * n4) >> 2; f0 < f1; f0 += 4) {
-          float4 kv[4], qv[4];
+        for (int f0 = part; f0 < n4; f0 += kPieces * G) {
+          f32x4 kv[kPieces];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (f0 + i < f1) {
-              kv[i] = kr[f0 + i];
-              qv[i] = qr[f0 + i];
-            }
+          for (int i = 0; i < kPieces; ++i)
+            if (f0 + i * G < n4) kv[i] = kr[f0 + i * G];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (f0 + i < f1) {
-              float d = kv[i].x * qv[i].x;
-              d = fmaf(kv[i].y, qv[i].y, d);
-              d = fmaf(kv[i].z, qv[i].z, d);
-              d = fmaf(kv[i].w, qv[i].w, d);
-              const int rho = (4 * (f0 + i)) / width;   // a piece never straddles two slices
+          for (int i = 0; i < kPieces; ++i) {
+            const int f = f0 + i * G;
+            if (f < n4) {
+              const f32x4 qv = qr[f];
+              float d = kv[i].x * qv.x;
+              d = fmaf(kv[i].y, qv.y, d);
+              d = fmaf(kv[i].z, qv.z, d);
+              d = fmaf(kv[i].w, qv.w, d);
+              const int rho = (4 * f) / width;                  // a piece never straddles two slices
 #pragma unroll
               for (int r = 0; r < kMaxRank; ++r) acc[r] += rho == r ? d : 0.0f;
             }
+          }
         }
 #pragma unroll
-        for (int r = 0; r < kMaxRank; ++r) {
-          acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0xB1, 0xF, 0xF, false));
-          acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0x4E, 0xF, 0xF, false));
-        }
+        for (int r = 0; r < kMaxRank; ++r) acc[r] = group_sum_f(acc[r], lg);
         if (part == 0)
           for (int r = 0; r < rank; ++r) sh.s_ex[axis][r][a] = acc[r];
       }
