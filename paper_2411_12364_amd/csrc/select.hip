@@ -618,49 +618,45 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
     S = sh.grid_cnt;
   } else {
     // ---- a4 (Tucker): exact per-slice scores of the selected keys (eq. (4)), in fp32.  G = 4, 8
-    // or 16 lanes per (axis, key) row, as many as 2k rows leave in the workgroup (one pass); lane
-    // p of a group takes the row's 16-byte pieces p, p + G, ... (the group reads contiguous
-    // 16G-byte runs), eight loads in flight before any is used; the group's partial sums per
-    // slice are added with DPP.
+    // or 16 lanes per (axis, key) row, as many as 2k rows leave in the workgroup (one pass), and
+    // L = G / 4, G / 2 or G lanes per slice of the row (rank 3 or 4, 2, 1): lane sub of a slice
+    // takes its 16-byte pieces sub, sub + L, ... (the L lanes read contiguous 16L-byte runs),
+    // eight loads in flight before any is used, and the L partial sums meet through DPP.
     {
       const f32x4* qs = reinterpret_cast<const f32x4*>(dyn);          // [2][n4] query pieces
       if (tid < 2 * n4) reinterpret_cast<f32x4*>(dyn)[tid] = q_piece;
       __syncthreads();
       constexpr int kPieces = 8;
-      const int width = dk / rank;
+      const int wp = n4 / rank;                                        // pieces per slice
       const int lg = 2 * k <= 32 ? 4 : (2 * k <= 64 ? 3 : 2);
-      const int G = 1 << lg;
+      const int ls = rank == 1 ? lg : (rank == 2 ? lg - 1 : lg - 2);
       for (int job = tid; job < (2 * k) << lg; job += THREADS) {   // whole groups: G | THREADS
-        const int part = job & (G - 1), row = job >> lg;
+        const int part = job & ((1 << lg) - 1), row = job >> lg;
         const int axis = row >= k, a = row - (axis ? k : 0);
+        const int rho = part >> ls, sub = part & ((1 << ls) - 1);
+        const int cnt = rho < rank ? (wp - sub + (1 << ls) - 1) >> ls : 0;
+        const int first = rho * wp + sub;
         const f32x4* kr = reinterpret_cast<const f32x4*>(
-            (axis ? k_col : k_row) + (static_cast<size_t>(h) * n + sh.ax_idx[axis][a]) * dk);
-        const f32x4* qr = qs + axis * n4;
-        float acc[kMaxRank] = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (int f0 = part; f0 < n4; f0 += kPieces * G) {
+            (axis ? k_col : k_row) + (static_cast<size_t>(h) * n + sh.ax_idx[axis][a]) * dk) + first;
+        const f32x4* qr = qs + axis * n4 + first;
+        float acc = 0.0f;
+        for (int i0 = 0; i0 < cnt; i0 += kPieces) {
           f32x4 kv[kPieces];
 #pragma unroll
           for (int i = 0; i < kPieces; ++i)
-            if (f0 + i * G < n4) kv[i] = kr[f0 + i * G];
+            if (i0 + i < cnt) kv[i] = kr[(i0 + i) << ls];
 #pragma unroll
-          for (int i = 0; i < kPieces; ++i) {
-            const int f = f0 + i * G;
-            if (f < n4) {
-              const f32x4 qv = qr[f];
-              float d = kv[i].x * qv.x;
-              d = fmaf(kv[i].y, qv.y, d);
-              d = fmaf(kv[i].z, qv.z, d);
-              d = fmaf(kv[i].w, qv.w, d);
-              const int rho = (4 * f) / width;                  // a piece never straddles two slices
-#pragma unroll
-              for (int r = 0; r < kMaxRank; ++r) acc[r] += rho == r ? d : 0.0f;
+          for (int i = 0; i < kPieces; ++i)
+            if (i0 + i < cnt) {
+              const f32x4 qv = qr[(i0 + i) << ls];
+              acc = fmaf(kv[i].x, qv.x, acc);
+              acc = fmaf(kv[i].y, qv.y, acc);
+              acc = fmaf(kv[i].z, qv.z, acc);
+              acc = fmaf(kv[i].w, qv.w, acc);
             }
-          }
         }
-#pragma unroll
-        for (int r = 0; r < kMaxRank; ++r) acc[r] = group_sum_f(acc[r], lg);
-        if (part == 0)
-          for (int r = 0; r < rank; ++r) sh.s_ex[axis][r][a] = acc[r];
+        acc = group_sum_f(acc, ls);
+        if (rho < rank && sub == 0) sh.s_ex[axis][rho][a] = acc;
       }
     }
     __syncthreads();
