@@ -687,7 +687,9 @@ __global__ __launch_bounds__(THREADS) void select_kernel(
       k32[j] = 0u;
       if (on && a < k) {
         double gv = 0.0;
-        for (int rho = 0; rho < rank; ++rho) gv += static_cast<double>(sh.s_ex[0][rho][a]) * pc[rho];
+#pragma unroll
+        for (int rho = 0; rho < kMaxRank; ++rho)            // pc[] indexed at compile time
+          if (rho < rank) gv += static_cast<double>(sh.s_ex[0][rho][a]) * pc[rho];
         k64[j] = order_key64(gv);
         k32[j] = order_key(static_cast<float>(gv));
         mx = max(mx, k32[j]);
