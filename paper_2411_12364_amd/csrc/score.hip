@@ -394,7 +394,7 @@ __global__ __launch_bounds__(THREADS) void axis_scores_wide(
 // steps of 32 through LDS with the next slice prefetched into registers, and the scores leave
 // through LDS as whole 128-byte lines (nontemporal).
 constexpr int XT = 128, XN = 128, XK = 32;
-constexpr int XLD = XK + 8;                   // LDS pitch in bf16 (80 B: fragment reads conflict-free)
+constexpr int XLD = XK;                       // LDS pitch in bf16 (64-byte rows, chunks swizzled)
 constexpr int XLDC = 64 + 4;                  // LDS pitch of the epilogue's fp32 rows
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -465,6 +465,14 @@ struct XSlice {
   u32x4 a[6], b[6];
 };
 
+// Where 16-byte chunk ch of tile row `row` sits in LDS: the chunk index is XORed with row bits
+// 1..3, so that the eight (or sixteen) lanes an LDS cycle serves, rows r..r+7 of one chunk when
+// fragments are read and rows r, r+1 (r..r+3) of all four chunks when tiles are staged, fall on
+// distinct banks with 32 (or 64) banks of 4 bytes.
+__device__ __forceinline__ int x6_pos(int row, int ch) {
+  return row * XLD + 8 * (ch ^ (((row >> 1) ^ (row >> 3)) & 3));
+}
+
 __device__ __forceinline__ void x6_fetch(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Kb,
                                          size_t qplane, size_t kplane, int T, int n, int dk,
                                          int t0, int i0, int k0, int tid, XSlice& sl) {
@@ -487,8 +495,16 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
   __shared__ __align__(16) uint16_t smem[2 * 3 * XT * XLD];   // [A | B][plane][row][k]
   uint16_t* As = smem;
   uint16_t* Bs = smem + 3 * XT * XLD;
-  const int axis = blockIdx.z & 1, h = blockIdx.z >> 1;
-  const int i0 = blockIdx.x * XN, t0 = blockIdx.y * XT;
+  // Tiles in (key tile, token tile, head/axis) order, dealt to the eight XCDs in contiguous runs
+  // (workgroups go to XCDs round-robin): each XCD walks its own token tiles against every key tile
+  // of a head and axis, so both operands' planes are reused from its L2.
+  const int nx = (n + XN - 1) / XN, ny = (T + XT - 1) / XT;
+  const int ntiles = nx * ny * 2 * H;
+  const int L = blockIdx.x, xcd = L & 7, per = ntiles >> 3, extra = ntiles & 7;
+  const int u = xcd * per + min(xcd, extra) + (L >> 3);
+  const int tz = u / (nx * ny), txy = u - tz * (nx * ny);
+  const int axis = tz & 1, h = tz >> 1;
+  const int i0 = (txy % nx) * XN, t0 = (txy / nx) * XT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;              // 64 tokens x 64 keys of the tile
   const size_t qplane = static_cast<size_t>(H) * T * dk, kplane = static_cast<size_t>(H) * n * dk;
@@ -507,8 +523,8 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
     for (int j = 0; j < 6; ++j) {
       const int f = tid + THREADS * j;
       const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
-      *reinterpret_cast<u32x4*>(As + (pl * XT + row) * XLD + 8 * ch) = sl.a[j];
-      *reinterpret_cast<u32x4*>(Bs + (pl * XN + row) * XLD + 8 * ch) = sl.b[j];
+      *reinterpret_cast<u32x4*>(As + pl * XT * XLD + x6_pos(row, ch)) = sl.a[j];
+      *reinterpret_cast<u32x4*>(Bs + pl * XN * XLD + x6_pos(row, ch)) = sl.b[j];
     }
     __syncthreads();
     if (k0 + XK < dk) x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + XK, tid, sl);
@@ -518,8 +534,8 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
     for (int pl = 0; pl < 3; ++pl)
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        af[pl][a] = *reinterpret_cast<const bf16x8*>(As + (pl * XT + wm * 64 + a * 16 + (lane & 15)) * XLD + 8 * (lane >> 4));
-        bfr[pl][a] = *reinterpret_cast<const bf16x8*>(Bs + (pl * XN + wn * 64 + a * 16 + (lane & 15)) * XLD + 8 * (lane >> 4));
+        af[pl][a] = *reinterpret_cast<const bf16x8*>(As + pl * XT * XLD + x6_pos(wm * 64 + a * 16 + (lane & 15), lane >> 4));
+        bfr[pl][a] = *reinterpret_cast<const bf16x8*>(Bs + pl * XN * XLD + x6_pos(wn * 64 + a * 16 + (lane & 15), lane >> 4));
       }
 #pragma unroll
     for (int a = 0; a < 4; ++a)
@@ -636,7 +652,7 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
     const unsigned blocks = static_cast<unsigned>(std::min<size_t>((items + THREADS - 1) / THREADS, 8192));
     hipLaunchKernelGGL(split_planes_kernel, dim3(blocks), dim3(THREADS), 0, s, q_row, q_col, k_row,
                        k_col, c, T, d.heads, d.n_keys, d.dk, d.dk / d.rank, Qp, Kp);
-    dim3 grid((d.n_keys + XN - 1) / XN, (T + XT - 1) / XT, d.heads * 2);
+    const dim3 grid(((d.n_keys + XN - 1) / XN) * ((T + XT - 1) / XT) * d.heads * 2);
     hipLaunchKernelGGL(axis_scores_x6, grid, dim3(THREADS), 0, s, Qp, Kp, sel, T, d.heads, d.n_keys,
                        d.dk, zero, zero_n4);
     return hipGetLastError();
