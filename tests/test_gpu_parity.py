@@ -126,6 +126,20 @@ def test_edge_shapes(kw):
     run_and_check(small("edge", **kw))
 
 
+# The Tucker grid's exact per-slice scores (eq. (4)) split each key row over G = 16, 8 or 4 lanes
+# (by 2k) and those over the slices (G, G/2 or G/4 lanes per slice for rank 1, 2, 3-4); these
+# cases take every split, the idle lanes of rank 3, a slice of 7 pieces over 2 lanes, and rows
+# of 112 pieces that need four batches of loads.
+@pytest.mark.parametrize("kw", [
+    dict(T=6, heads=2, dk=64, n_keys=120, rank=1, topk=12, topm=20),
+    dict(T=5, heads=1, dk=84, n_keys=90, rank=3, topk=30, topm=40),
+    dict(T=4, heads=2, dk=128, n_keys=100, rank=4, topk=50, topm=64),
+    dict(T=3, heads=1, dk=448, n_keys=80, rank=2, topk=64, topm=64),
+], ids=["rank1-G16", "rank3-G8", "rank4-G4", "dk448-G4"])
+def test_tucker_exact_slice_splits(kw):
+    run_and_check(small("tucker-slices", grid=CF.GRID_TUCKER, seed=17, **kw))
+
+
 def _tie_layer(cfg):
     """Integer-valued queries and keys (0, +-1, +-2): many exact ties in fp32 and fp64 alike."""
     dl = SD.make_layer(cfg)
