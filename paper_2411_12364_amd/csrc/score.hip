@@ -473,18 +473,24 @@ __device__ __forceinline__ int x6_pos(int row, int ch) {
   return row * XLD + 8 * (ch ^ (((row >> 1) ^ (row >> 3)) & 3));
 }
 
+// The tile's next K-slice (32 dims) of the three planes of Q' (tokens t0..) and K (keys i0..) into
+// registers.  Buffer loads over one (axis, plane, head) block each: rows past T (or n) fall
+// outside the block's range and read as zeros, and the addresses are 32-bit lane offsets on
+// scalar bases (no 64-bit address per load to keep live).
 __device__ __forceinline__ void x6_fetch(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Kb,
                                          size_t qplane, size_t kplane, int T, int n, int dk,
                                          int t0, int i0, int k0, int tid, XSlice& sl) {
+  static_assert(THREADS == 256, "a thread's six pieces: planes j / 2, rows tid / 4 + 64 (j % 2)");
+  const uint32_t qbytes = static_cast<uint32_t>(T) * dk * 2u, kbytes = static_cast<uint32_t>(n) * dk * 2u;
 #pragma unroll
   for (int j = 0; j < 6; ++j) {
-    const int f = tid + THREADS * j;
-    const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
-    const int t = t0 + row, i = i0 + row;
-    sl.a[j] = t < T ? *reinterpret_cast<const u32x4*>(Qa + pl * qplane + static_cast<size_t>(t) * dk + k0 + 8 * ch)
-                    : u32x4{0u, 0u, 0u, 0u};
-    sl.b[j] = i < n ? *reinterpret_cast<const u32x4*>(Kb + pl * kplane + static_cast<size_t>(i) * dk + k0 + 8 * ch)
-                    : u32x4{0u, 0u, 0u, 0u};
+    const int pl = j >> 1, row = (tid >> 2) + 64 * (j & 1), col = k0 + 8 * (tid & 3);
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(Qa + pl * qplane), static_cast<short>(0), static_cast<int>(qbytes), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(Kb + pl * kplane), static_cast<short>(0), static_cast<int>(kbytes), 0x00020000);
+    sl.a[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, static_cast<uint32_t>((t0 + row) * dk + col) * 2u, 0, 0);
+    sl.b[j] = __builtin_amdgcn_raw_buffer_load_b128(rb, static_cast<uint32_t>((i0 + row) * dk + col) * 2u, 0, 0);
   }
 }
 
@@ -497,87 +503,114 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
   uint16_t* Bs = smem + 3 * XT * XLD;
   // Tiles in (key tile, token tile, head/axis) order, dealt to the eight XCDs in contiguous runs
   // (workgroups go to XCDs round-robin): each XCD walks its own token tiles against every key tile
-  // of a head and axis, so both operands' planes are reused from its L2.
+  // of a head and axis, so both operands' planes are reused from its L2.  The grid is persistent
+  // (8 gx workgroups, gx per XCD): workgroup s of an XCD takes the XCD's tiles s, s + gx, ..., and
+  // the last K-step of a tile fetches the first slice of the next one, under the MFMAs and the
+  // epilogue.
   const int nx = (n + XN - 1) / XN, ny = (T + XT - 1) / XT;
   const int ntiles = nx * ny * 2 * H;
-  const int L = blockIdx.x, xcd = L & 7, per = ntiles >> 3, extra = ntiles & 7;
-  const int u = xcd * per + min(xcd, extra) + (L >> 3);
-  const int tz = u / (nx * ny), txy = u - tz * (nx * ny);
-  const int axis = tz & 1, h = tz >> 1;
-  const int i0 = (txy % nx) * XN, t0 = (txy / nx) * XT;
+  const int xcd = blockIdx.x & 7, gx = gridDim.x >> 3, per = ntiles >> 3, extra = ntiles & 7;
+  const int first = xcd * per + min(xcd, extra), cnt = per + (xcd < extra ? 1 : 0);
+  int jt = blockIdx.x >> 3;                              // this workgroup's tiles: jt, jt + gx, ...
+  if (jt >= cnt) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;              // 64 tokens x 64 keys of the tile
   const size_t qplane = static_cast<size_t>(H) * T * dk, kplane = static_cast<size_t>(H) * n * dk;
-  const uint16_t* Qa = Qp + static_cast<size_t>(axis) * 3 * qplane + static_cast<size_t>(h) * T * dk;
-  const uint16_t* Kb = Kp + static_cast<size_t>(axis) * 3 * kplane + static_cast<size_t>(h) * n * dk;
-
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto coords = [&](int u, int& axis, int& h, int& i0, int& t0, const uint16_t*& Qa, const uint16_t*& Kb) {
+    const int tz = u / (nx * ny), txy = u - tz * (nx * ny);
+    axis = tz & 1;
+    h = tz >> 1;
+    i0 = (txy % nx) * XN;
+    t0 = (txy / nx) * XT;
+    Qa = Qp + static_cast<size_t>(axis) * 3 * qplane + static_cast<size_t>(h) * T * dk;
+    Kb = Kp + static_cast<size_t>(axis) * 3 * kplane + static_cast<size_t>(h) * n * dk;
+  };
+  int axis, h, i0, t0;
+  const uint16_t *Qa, *Kb;
+  coords(first + jt, axis, h, i0, t0, Qa, Kb);
   XSlice sl;
   x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, 0, tid, sl);
-  for (int k0 = 0; k0 < dk; k0 += XK) {
-#pragma unroll
-    for (int j = 0; j < 6; ++j) {
-      const int f = tid + THREADS * j;
-      const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
-      *reinterpret_cast<u32x4*>(As + pl * XT * XLD + x6_pos(row, ch)) = sl.a[j];
-      *reinterpret_cast<u32x4*>(Bs + pl * XN * XLD + x6_pos(row, ch)) = sl.b[j];
-    }
-    __syncthreads();
-    if (k0 + XK < dk) x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + XK, tid, sl);
-    // lane: row (token or key) lane % 16 of a 16-block, dims 8 (lane / 16) ... + 7
-    bf16x8 af[3][4], bfr[3][4];
-#pragma unroll
-    for (int pl = 0; pl < 3; ++pl)
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        af[pl][a] = *reinterpret_cast<const bf16x8*>(As + pl * XT * XLD + x6_pos(wm * 64 + a * 16 + (lane & 15), lane >> 4));
-        bfr[pl][a] = *reinterpret_cast<const bf16x8*>(Bs + pl * XN * XLD + x6_pos(wn * 64 + a * 16 + (lane & 15), lane >> 4));
-      }
+  while (true) {
+    const bool has_next = jt + gx < cnt;
+    int naxis = 0, nh = 0, ni0 = 0, nt0 = 0;
+    const uint16_t *nQa = Qa, *nKb = Kb;
+    if (has_next) coords(first + jt + gx, naxis, nh, ni0, nt0, nQa, nKb);
+    f32x4 acc[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        // the six products of significance 2^-16 and above, smaller ones first
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[2][a], bfr[0][b], acc[a][b], 0, 0, 0);
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[1][b], acc[a][b], 0, 0, 0);
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[2][b], acc[a][b], 0, 0, 0);
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[0][b], acc[a][b], 0, 0, 0);
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[1][b], acc[a][b], 0, 0, 0);
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[0][b], acc[a][b], 0, 0, 0);
+      for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < dk; k0 += XK) {
+#pragma unroll
+      for (int j = 0; j < 6; ++j) {
+        const int f = tid + THREADS * j;
+        const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
+        *reinterpret_cast<u32x4*>(As + pl * XT * XLD + x6_pos(row, ch)) = sl.a[j];
+        *reinterpret_cast<u32x4*>(Bs + pl * XN * XLD + x6_pos(row, ch)) = sl.b[j];
       }
-    __syncthreads();
-  }
-  // D layout: lane holds tokens 4 (lane / 16) + r of key lane % 16.  Each wave's 64 x 64 block
-  // leaves in two halves of 32 tokens through LDS (free after the last barrier), as 16-byte
-  // pieces: every token's 64 keys are 256 contiguous bytes of sel.
-  float* Cs = reinterpret_cast<float*>(smem) + wave * 32 * XLDC;
+      __syncthreads();
+      if (k0 + XK < dk) x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + XK, tid, sl);
+      else if (has_next) x6_fetch(nQa, nKb, qplane, kplane, T, n, dk, nt0, ni0, 0, tid, sl);
+      // lane: row (token or key) lane % 16 of a 16-block, dims 8 (lane / 16) ... + 7
+      bf16x8 af[3][4], bfr[3][4];
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
+      for (int pl = 0; pl < 3; ++pl)
 #pragma unroll
-    for (int a2 = 0; a2 < 2; ++a2)
+        for (int a = 0; a < 4; ++a) {
+          af[pl][a] = *reinterpret_cast<const bf16x8*>(As + pl * XT * XLD + x6_pos(wm * 64 + a * 16 + (lane & 15), lane >> 4));
+          bfr[pl][a] = *reinterpret_cast<const bf16x8*>(Bs + pl * XN * XLD + x6_pos(wn * 64 + a * 16 + (lane & 15), lane >> 4));
+        }
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
+      for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          Cs[(a2 * 16 + 4 * (lane >> 4) + r) * XLDC + b * 16 + (lane & 15)] = acc[half * 2 + a2][b][r];
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-    for (int it = 0; it < 8; ++it) {
-      const int row = (lane >> 4) + 4 * it, c4 = (lane & 15) * 4;
-      const int t = t0 + wm * 64 + half * 32 + row, key = i0 + wn * 64 + c4;
-      const f32x4 v = *reinterpret_cast<const f32x4*>(Cs + row * XLDC + c4);
-      if (t < T && key < n)      // n % 4 == 0: the piece is whole
-        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n + key));
+        for (int b = 0; b < 4; ++b) {
+          // the six products of significance 2^-16 and above, smaller ones first
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[2][a], bfr[0][b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[1][b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[2][b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[0][b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[1][b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[0][b], acc[a][b], 0, 0, 0);
+        }
+      __syncthreads();
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // D layout: lane holds tokens 4 (lane / 16) + r of key lane % 16.  Each wave's 64 x 64 block
+    // leaves in two halves of 32 tokens through LDS (free after the last barrier), as 16-byte
+    // pieces: every token's 64 keys are 256 contiguous bytes of sel.
+    float* Cs = reinterpret_cast<float*>(smem) + wave * 32 * XLDC;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+#pragma unroll
+      for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            Cs[(a2 * 16 + 4 * (lane >> 4) + r) * XLDC + b * 16 + (lane & 15)] = acc[half * 2 + a2][b][r];
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        const int row = (lane >> 4) + 4 * it, c4 = (lane & 15) * 4;
+        const int t = t0 + wm * 64 + half * 32 + row, key = i0 + wn * 64 + c4;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(Cs + row * XLDC + c4);
+        if (t < T && key < n)      // n % 4 == 0: the piece is whole
+          __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n + key));
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    if (!has_next) break;
+    jt += gx;
+    axis = naxis;
+    h = nh;
+    i0 = ni0;
+    t0 = nt0;
+    Qa = nQa;
+    Kb = nKb;
+    __syncthreads();          // the epilogue's LDS rows are free before the next tile is staged
   }
 }
 static_assert(4 * 32 * XLDC * 4 <= 2 * 3 * XT * XLD * 2, "epilogue staging fits the tiles' LDS");
@@ -652,7 +685,9 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
     const unsigned blocks = static_cast<unsigned>(std::min<size_t>((items + THREADS - 1) / THREADS, 8192));
     hipLaunchKernelGGL(split_planes_kernel, dim3(blocks), dim3(THREADS), 0, s, q_row, q_col, k_row,
                        k_col, c, T, d.heads, d.n_keys, d.dk, d.dk / d.rank, Qp, Kp);
-    const dim3 grid(((d.n_keys + XN - 1) / XN) * ((T + XT - 1) / XT) * d.heads * 2);
+    // a persistent grid of 8 gx workgroups (two per CU, as registers allow), gx per XCD
+    const long long ntiles = static_cast<long long>((d.n_keys + XN - 1) / XN) * ((T + XT - 1) / XT) * d.heads * 2;
+    const dim3 grid(static_cast<unsigned>(8 * std::min<long long>((ntiles + 7) / 8, 64)));
     hipLaunchKernelGGL(axis_scores_x6, grid, dim3(THREADS), 0, s, Qp, Kp, sel, T, d.heads, d.n_keys,
                        d.dk, zero, zero_n4);
     return hipGetLastError();
