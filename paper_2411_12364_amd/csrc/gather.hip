@@ -1,9 +1,11 @@
 // a6 + a7: score-weighted gather-sum of value rows (embedding bag), eq. (1) and eq. (15).
 //
 // One workgroup of four waves per token; each wave pools a contiguous quarter of the bag.  A
-// value row is read once, with 16-byte nontemporal loads (the rows are not reused), L lanes per
-// row and CPL 16-byte chunks per lane (row bytes = 16 * L * CPL); a wave keeps U rows in
-// flight.  Accumulation is fp32 in registers; the sub-rows of a wave are combined with
+// value row is read with 16-byte loads, L lanes per row and CPL 16-byte chunks per lane (row
+// bytes = 16 * L * CPL); a wave keeps U rows in flight.  The loads are nontemporal unless the
+// launch reads at least a quarter as many rows as the table holds: then rows repeat (more than
+// one read in nine even if slots were drawn uniformly, far more with clustered queries) and are
+// worth keeping in L2 and the MALL.  Accumulation is fp32 in registers; the sub-rows of a wave are combined with
 // shuffles, and the four waves' partial rows in LDS behind one barrier, always in wave order
 // (the result does not depend on timing).  Pooled rows are written with nontemporal stores:
 // they are not read again here, and the read stream suffers less from them.  With implicit
@@ -60,7 +62,7 @@ struct ElemTraits<uint16_t> {   // bf16 bit patterns
 // `slot(j)` gives entry j's position in idx / w (after the block partition, if any).  With
 // multi-core scoring (cores > 1) entry s has cores weights, w_of[s * cores + i], and a lane's
 // 16-byte chunk takes the weight of the column slice it lies in.
-template <typename Elem, int L, int CPL, typename Slot>
+template <typename Elem, int L, int CPL, bool KEEP, typename Slot>
 __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int dv, int cnt,
                                           const Slot& slot, const int32_t* __restrict__ rows_of,
                                           const float* __restrict__ w_of, int cores, float* red,
@@ -98,7 +100,10 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
           wt[u][c] = w_of[static_cast<size_t>(s) * cores + slice[c]];
-          raw[u][c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + (cl + L * c) * EPC));
+          const u32x4* p = reinterpret_cast<const u32x4*>(src + (cl + L * c) * EPC);
+          // (a compile-time choice: a run-time select of the two loads is merged into a plain one)
+          if constexpr (KEEP) raw[u][c] = *p;
+          else raw[u][c] = __builtin_nontemporal_load(p);
         }
       } else {
 #pragma unroll
@@ -170,7 +175,7 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
 // Without expansion the bag is read straight from idx / w (for rows of 64 lanes a wave's row
 // index is uniform and lives in scalar registers).  With expansion the bag is first mapped
 // through perm and stably partitioned by virtual block in LDS.
-template <typename Elem, int L, int CPL>
+template <typename Elem, int L, int CPL, bool KEEP>
 __global__ __launch_bounds__(THREADS) void gather_kernel(
     const Elem* __restrict__ values, int64_t n_values, int dv, int bag,
     const int32_t* __restrict__ idx, const float* __restrict__ w, const int32_t* __restrict__ perm,
@@ -180,8 +185,8 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
   const int32_t* __restrict__ idx_t = idx + static_cast<size_t>(t) * bag;
   const float* __restrict__ w_t = w + static_cast<size_t>(t) * bag * cores;
   if (expand == 1) {
-    pool_rows<Elem, L, CPL>(values, dv, bag, [](int j) { return j; }, idx_t, w_t, cores, red,
-                            out + static_cast<size_t>(t) * dv);
+    pool_rows<Elem, L, CPL, KEEP>(values, dv, bag, [](int j) { return j; }, idx_t, w_t, cores, red,
+                                  out + static_cast<size_t>(t) * dv);
     return;
   }
   int32_t* rows = reinterpret_cast<int32_t*>(red + (dv <= 2048 ? NWAVES : 2) * dv);   // [bag]
@@ -216,8 +221,8 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
   __syncthreads();
   for (int p = 0; p < expand; ++p) {
     const int beg = bstart[p];
-    pool_rows<Elem, L, CPL>(values, dv, bcount[p], [=](int j) { return order[beg + j]; }, rows,
-                            w_t, cores, red, out + (static_cast<size_t>(t) * expand + p) * dv);
+    pool_rows<Elem, L, CPL, KEEP>(values, dv, bcount[p], [=](int j) { return order[beg + j]; }, rows,
+                                  w_t, cores, red, out + (static_cast<size_t>(t) * expand + p) * dv);
     __syncthreads();
   }
 }
@@ -328,13 +333,18 @@ hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int
   // thousands of tokens without expansion (or multi-core weights): a wave per token
   const bool per_wave = expand == 1 && cores == 1 && T >= kWaveTokensMin;
   const dim3 grid(per_wave ? (T + NWAVES - 1) / NWAVES : T);
+  // temporal row loads when rows will repeat: T * bag row reads against n_values rows
+  const bool keep = 4 * static_cast<int64_t>(T) * bag >= n_values;
 #define UMEM_GATHER(LL, CC)                                                                      \
   if (per_wave)                                                                                  \
     hipLaunchKernelGGL((gather_wave_kernel<Elem, LL, CC>), grid, block, 0, s, values, dv, T, bag, \
                        idx, w, out);                                                             \
+  else if (keep)                                                                                 \
+    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC, true>), grid, block, lds, s, values, n_values, \
+                       dv, bag, idx, w, perm, expand, cores, out);                               \
   else                                                                                           \
-    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC>), grid, block, lds, s, values, n_values, dv,   \
-                       bag, idx, w, perm, expand, cores, out)
+    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC, false>), grid, block, lds, s, values,          \
+                       n_values, dv, bag, idx, w, perm, expand, cores, out)
   switch (chunks) {
     case 1: UMEM_GATHER(1, 1); break;
     case 2: UMEM_GATHER(2, 1); break;
