@@ -309,7 +309,8 @@ __global__ __launch_bounds__(THREADS) void axis_scores_split(
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = t0 + mt * 16 + 4 * g + r;
-        if (t < T && key < n) sel[((static_cast<size_t>(axis) * T + t) * H + h) * n + key] = o[r];
+        if (t < T && key < n)
+          __builtin_nontemporal_store(o[r], sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n + key);
       }
     }
   }
@@ -373,7 +374,10 @@ __global__ __launch_bounds__(THREADS) void axis_scores_wide(
     const int j = 4 * wave + jj;
     const float o = ((part[0][j][lane] + part[1][j][lane]) + part[2][j][lane]) + part[3][j][lane];
     const int t = blockIdx.y * 32 + 8 * wave + 4 * hh + jj;
-    if (t < T && key < n) sel[((static_cast<size_t>(axis) * T + t) * H + h) * n + key] = o;
+    // nontemporal: the selection reads the scores from other XCDs, so this XCD's L2 has no use
+    // for them (measured: decode-20M step 16.53 -> 16.29 us)
+    if (t < T && key < n)
+      __builtin_nontemporal_store(o, sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n + key);
   }
 }
 
