@@ -300,18 +300,19 @@ __device__ void select_axes(const float* __restrict__ sel, int T, int H, int t, 
   uint32_t key[NE];
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
-    // the many-token variants read the scores nontemporally (they stream through once; the keys
-    // the Tucker grid reads back should stay in L2)
+    // the scores are read nontemporally: they stream through once (the keys the Tucker grid
+    // reads back should stay in L2), and they were written from other XCDs (measured at decode:
+    // 10.32 -> 10.06 us against plain loads)
     if (VEC == 4) {
       const f32x4* p = reinterpret_cast<const f32x4*>(src + min(1024 * j + 4 * g, n - 4));
-      const f32x4 v = MODE == kModePool ? *p : __builtin_nontemporal_load(p);
+      const f32x4 v = __builtin_nontemporal_load(p);
       key[4 * j + 0] = order_key(v.x);
       key[4 * j + 1] = order_key(v.y);
       key[4 * j + 2] = order_key(v.z);
       key[4 * j + 3] = order_key(v.w);
     } else {
       const float* p = src + min(GROUP * j + g, n - 1);
-      key[j] = order_key(MODE == kModePool ? *p : __builtin_nontemporal_load(p));
+      key[j] = order_key(__builtin_nontemporal_load(p));
     }
   }
   if (tables && tid < kWave) additive_tables(k, m, sh);
