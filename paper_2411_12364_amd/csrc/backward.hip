@@ -455,43 +455,52 @@ __global__ __launch_bounds__(score_bwd_waves<NG>() * kWave) void score_bwd_kerne
     }
   }
   wave_sync();
-  // ---- Tucker: per-slice scores of the distinct keys, four lanes per key row
+  // ---- Tucker: per-slice scores of the distinct keys, four lanes per key row.  The quad is
+  // split into one group per slice (4, 2 or 1 lanes for rank 1, 2, 3-4; rank 3 leaves a lane
+  // idle); a lane strides its slice's 16-byte pieces by the group width, eight loads in flight,
+  // and the group's partial sums meet through DPP in a fixed order.
   float sr[NG][kMaxRank] = {}, sc[NG][kMaxRank] = {};
   if (tucker) {
-    const int width = dk / rank, n4 = dk >> 2;
+    constexpr int kPieces = 8;
+    const int n4 = dk >> 2, wp = n4 / rank;                   // pieces per row, per slice
     const int part = lane & 3;
-    const int f0 = (part * n4) >> 2, f1 = ((part + 1) * n4) >> 2;
+    const int ls = rank == 1 ? 2 : (rank == 2 ? 1 : 0);       // log2 lanes per slice
+    const int rho = part >> ls, sub = part & ((1 << ls) - 1);
+    const int cnt = rho < rank ? (wp - sub + (1 << ls) - 1) >> ls : 0;
+    const int first = rho * wp + sub;
     const int jobs = nd[0] + nd[1];
     for (int j0 = 0; j0 < jobs; j0 += kWave / 4) {     // wave-uniform trip count
       const int kk = j0 + lane / 4;
-      const bool ok = kk < jobs;
+      const bool ok = kk < jobs;                       // uniform across each quad
       const int a = kk >= nd[0] ? 1 : 0;
       const int k = kk - (a ? nd[0] : 0);
-      float acc[kMaxRank] = {0.0f, 0.0f, 0.0f, 0.0f};
+      float acc = 0.0f;
       if (ok) {
         const float4* kr = reinterpret_cast<const float4*>(
-            (a ? k_col : k_row) + (static_cast<size_t>(h) * n + sh.dist[a][k]) * dk);
-        const float4* qr = reinterpret_cast<const float4*>((a ? q_col : q_row) + th * dk);
-#pragma unroll 4
-        for (int f = f0; f < f1; ++f) {
-          const float4 kv = kr[f], qv = qr[f];
-          float d = kv.x * qv.x;
-          d = fmaf(kv.y, qv.y, d);
-          d = fmaf(kv.z, qv.z, d);
-          d = fmaf(kv.w, qv.w, d);
-          const int rho = (4 * f) / width;
+            (a ? k_col : k_row) + (static_cast<size_t>(h) * n + sh.dist[a][k]) * dk) + first;
+        const float4* qr = reinterpret_cast<const float4*>((a ? q_col : q_row) + th * dk) + first;
+        for (int i0 = 0; i0 < cnt; i0 += kPieces) {
+          float4 kv[kPieces];
 #pragma unroll
-          for (int r = 0; r < kMaxRank; ++r) acc[r] += rho == r ? d : 0.0f;
+          for (int i = 0; i < kPieces; ++i)
+            if (i0 + i < cnt) kv[i] = kr[(i0 + i) << ls];
+#pragma unroll
+          for (int i = 0; i < kPieces; ++i)
+            if (i0 + i < cnt) {
+              const float4 qv = qr[(i0 + i) << ls];
+              acc = fmaf(kv[i].x, qv.x, acc);
+              acc = fmaf(kv[i].y, qv.y, acc);
+              acc = fmaf(kv[i].z, qv.z, acc);
+              acc = fmaf(kv[i].w, qv.w, acc);
+            }
         }
       }
-#pragma unroll
-      for (int r = 0; r < kMaxRank; ++r) {          // quad sums; every lane takes part
-        acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0xB1, 0xF, 0xF, false));
-        acc[r] += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc[r]), 0x4E, 0xF, 0xF, false));
-      }
+      // the slice group's sum (every lane takes part)
+      if (ls >= 1) acc += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc), 0xB1, 0xF, 0xF, false));
+      if (ls >= 2) acc += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, acc), 0x4E, 0xF, 0xF, false));
+      if (ok && rho < rank && sub == 0) sh.sd[a][k][rho] = acc;
       if (ok && part == 0)
-#pragma unroll
-        for (int r = 0; r < kMaxRank; ++r) sh.sd[a][k][r] = acc[r];
+        for (int r = rank; r < kMaxRank; ++r) sh.sd[a][k][r] = 0.0f;
     }
     wave_sync();
 #pragma unroll

@@ -156,6 +156,12 @@ SCORE_CASES = [
     CF.Layer("add-m1", T=9, heads=3, dk=16, n_keys=30, topk=2, topm=1, dv=8, vdtype=CF.F32, seed=59),
     CF.Layer("tucker-r4-wide", T=256, heads=2, dk=128, n_keys=512, topk=32, topm=64, dv=8,
              vdtype=CF.F32, seed=55, rank=4, grid=CF.GRID_TUCKER),
+    # the per-slice recompute's other lane splits: four lanes on one slice; rank 3 (one idle lane,
+    # 7-piece slices)
+    CF.Layer("tucker-r1", T=14, heads=2, dk=64, n_keys=60, topk=12, topm=30, dv=8, vdtype=CF.F32,
+             seed=60, rank=1, grid=CF.GRID_TUCKER),
+    CF.Layer("tucker-r3", T=11, heads=1, dk=84, n_keys=70, topk=14, topm=40, dv=8, vdtype=CF.F32,
+             seed=61, rank=3, grid=CF.GRID_TUCKER),
 ]
 
 
