@@ -168,7 +168,9 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
       r.z += x.z;
       r.w += x.w;
     }
-    __builtin_nontemporal_store(f32x4{r.x, r.y, r.z, r.w}, reinterpret_cast<f32x4*>(dst + col));
+    // (where rows repeat, the pooled rows also stay cached for the projection that reads them next)
+    if constexpr (KEEP) *reinterpret_cast<f32x4*>(dst + col) = f32x4{r.x, r.y, r.z, r.w};
+    else __builtin_nontemporal_store(f32x4{r.x, r.y, r.z, r.w}, reinterpret_cast<f32x4*>(dst + col));
   }
 }
 
