@@ -7,8 +7,9 @@
 // one read in nine even if slots were drawn uniformly, far more with clustered queries) and are
 // worth keeping in L2 and the MALL.  Accumulation is fp32 in registers; the sub-rows of a wave are combined with
 // shuffles, and the four waves' partial rows in LDS behind one barrier, always in wave order
-// (the result does not depend on timing).  Pooled rows are written with nontemporal stores:
-// they are not read again here, and the read stream suffers less from them.  With implicit
+// (the result does not depend on timing).  Pooled rows are written with nontemporal stores
+// (they are not read again here, and the read stream suffers less from them), except where the
+// row loads are temporal: then the projection reading them next finds them cached.  With implicit
 // value expansion the bag is first mapped through the shuffle and split by virtual block p (a
 // stable partition), and each block's rows are pooled into out[t, p, :].  From 2048 tokens on
 // (without expansion) a wave per token does the same work without LDS or barriers.
