@@ -7,9 +7,8 @@
 // one read in nine even if slots were drawn uniformly, far more with clustered queries) and are
 // worth keeping in L2 and the MALL.  Accumulation is fp32 in registers; the sub-rows of a wave are combined with
 // shuffles, and the four waves' partial rows in LDS behind one barrier, always in wave order
-// (the result does not depend on timing).  Pooled rows are written with nontemporal stores
-// (they are not read again here, and the read stream suffers less from them), except where the
-// row loads are temporal: then the projection reading them next finds them cached.  With implicit
+// (the result does not depend on timing).  Pooled rows are written with plain stores: with
+// implicit value expansion the projection reads them next and finds them cached.  With implicit
 // value expansion the bag is first mapped through the shuffle and split by virtual block p (a
 // stable partition), and each block's rows are pooled into out[t, p, :].  From 2048 tokens on
 // (without expansion) a wave per token does the same work without LDS or barriers.
@@ -169,9 +168,8 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
       r.z += x.z;
       r.w += x.w;
     }
-    // (where rows repeat, the pooled rows also stay cached for the projection that reads them next)
-    if constexpr (KEEP) *reinterpret_cast<f32x4*>(dst + col) = f32x4{r.x, r.y, r.z, r.w};
-    else __builtin_nontemporal_store(f32x4{r.x, r.y, r.z, r.w}, reinterpret_cast<f32x4*>(dst + col));
+    // plain stores: the projection that follows reads the pooled rows from cache
+    *reinterpret_cast<f32x4*>(dst + col) = f32x4{r.x, r.y, r.z, r.w};
   }
 }
 
