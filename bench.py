@@ -628,8 +628,8 @@ def cpu_baseline(cfg, seconds):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the memory layer's "
-              "multi-GPU sharding is not part of this build.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the memory layer is not "
+              "sharded across GPUs.", file=sys.stderr)
         sys.exit(2)
     import torch
 
