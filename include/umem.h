@@ -17,10 +17,13 @@
  *     kernels on `stream` (NULL = the default stream).  Scratch memory comes from the caller
  *     (`ws`, sized by umem_workspace_size).
  *   - Calls are asynchronous.  The returned status covers argument validation and launch
- *     errors only.  On any error nothing is enqueued and no output is written.  Device-side
- *     faults (e.g. an index out of range in a caller-supplied bag) are not detected.  A HIP
- *     error that an earlier call left pending in the calling thread is cleared, unreported,
- *     before a call launches its kernels.
+ *     errors only.  Every argument is validated before the first launch: on a validation error
+ *     (UMEM_ERR_INVALID_ARG, UMEM_ERR_UNSUPPORTED, UMEM_ERR_WORKSPACE) nothing is enqueued and
+ *     no output is written.  UMEM_ERR_HIP reports a launch that the HIP runtime refused; in an
+ *     entry point that launches several kernels, the kernels enqueued before that one stay
+ *     enqueued and may write outputs and scratch.  Device-side faults (e.g. an index out of
+ *     range in a caller-supplied bag) are not detected.  A HIP error that an earlier call left
+ *     pending in the calling thread is cleared, unreported, before a call launches its kernels.
  *   - Ties: every selection orders by (score desc, index asc) -- the per-axis key index, or the
  *     logical flat index i*n + j on the grid; -0.0 equals +0.0; NaN ranks below -inf.
  *     Selections are returned sorted in that order.

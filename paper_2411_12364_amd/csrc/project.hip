@@ -210,17 +210,34 @@ int split_count(int M, int N, int K) {
 
 size_t round_up256(size_t x) { return (x + 255) / 256 * 256; }
 
+// A's buffer range is 32-bit: a GEMM is launched in bands of at most this many rows of A, whose
+// bytes stay below 2^31 (a multiple of BM).
+int64_t band_rows(int K) {
+  return std::max<int64_t>(BM, (((INT64_C(1) << 31) - 1) / (static_cast<int64_t>(K) * 4)) / BM * BM);
+}
+
+// Partial-sum bytes of one launch (one band) of `rows` rows.
+size_t band_partial_bytes(int rows, int N, int K) {
+  const int S = split_count(rows, N, K);
+  return S > 1 ? round_up256(static_cast<size_t>(S) * rows * N * sizeof(float)) : 0;
+}
+
 }  // namespace
 
+// Each band chooses its own split count from its own tile count, and a band of fewer rows may
+// split more ways than the whole matrix would (fewer tiles), so the scratch is the largest of
+// the bands' needs: the full bands and the last, shorter one.  The bands run one after the
+// other on one stream and share it.
 size_t gemm_partial_bytes(int M, int N, int K) {
-  const int S = split_count(M, N, K);
-  return S > 1 ? round_up256(static_cast<size_t>(S) * M * N * sizeof(float)) : 0;
+  const int64_t band = band_rows(K);
+  if (M <= band) return band_partial_bytes(M, N, K);
+  const int last = static_cast<int>(M - (M - 1) / band * band);
+  return std::max(band_partial_bytes(static_cast<int>(band), N, K), band_partial_bytes(last, N, K));
 }
 
 hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
                      hipStream_t s) {
-  // A's buffer range is 32-bit: launch bands of rows whose bytes stay below 2^31
-  const int64_t band = std::max<int64_t>(BM, (((INT64_C(1) << 31) - 1) / (static_cast<int64_t>(K) * 4)) / BM * BM);
+  const int64_t band = band_rows(K);
   if (M > band) {
     for (int64_t m = 0; m < M; m += band) {
       const int rows = static_cast<int>(std::min<int64_t>(band, M - m));

@@ -264,3 +264,47 @@ def test_backward_validation():
     a = [ds, 32, fake, fake, fake, fake, None, fake, None, fake]        # SoftMax needs w
     assert U.umem_score_backward(*a, fake, fake, fake, fake, None, fake, ns, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_score_backward_workspace_size(desc(heads=64, topm=32), 1 << 11)[0] == U.UMEM_ERR_UNSUPPORTED
+
+
+def _split_ways(rows, N, K):
+    """The projection GEMM's split of K, as its header states it: doubled while the launch has
+    fewer than 512 work items and each split keeps at least 4 K-steps of 64."""
+    tiles = -(-rows // 128) * -(-N // 128)
+    S = 1
+    while tiles * S < 512 and K // (2 * S) >= 4 * 64:
+        S *= 2
+    return S
+
+
+def _partials_needed(M, N, K):
+    """Bytes of split-K partials the largest launch of one GEMM writes.  A's bytes must stay in a
+    32-bit buffer range, so A is launched in bands of the largest multiple of 128 rows below
+    2 GiB; each band splits K for its own tile count."""
+    band = max(128, ((2 ** 31 - 1) // (K * 4)) // 128 * 128)
+    shapes = [M] if M <= band else [band, M - (M - 1) // band * band]
+    need = 0
+    for rows in shapes:
+        S = _split_ways(rows, N, K)
+        if S > 1:
+            need = max(need, S * rows * N * 4)
+    return need
+
+
+@pytest.mark.parametrize("T,E,dv,dvv,dout", [
+    (2048, 1, 1 << 18, 0, 128),      # two bands of 1920 and 128 rows: 64-way split of the first
+    (1921, 1, 1 << 18, 0, 128),
+    (400, 1, 1 << 20, 0, 8),         # bands of 384 and 16 rows
+    (16300, 16, 2048, 256, 0),       # the IVE projector alone at E = 16, 16.3K tokens
+    (512, 4, 4096, 1024, 2048),      # no band: the whole matrix in one launch
+])
+def test_project_workspace_covers_every_band(T, E, dv, dvv, dout):
+    """The split-K scratch covers the largest band: a band of fewer rows than the whole matrix
+    has fewer tiles and may split K more ways."""
+    st, n = U.umem_project_workspace_size(T, E, dv, dvv, dout)
+    assert st == U.UMEM_OK
+    if dvv == 0:
+        need = _partials_needed(T, dout, dv)
+    else:
+        tmp = -(-(T * dvv * 4) // 256) * 256 if dout else 0
+        need = tmp + max(_partials_needed(T, dvv, E * dv), _partials_needed(T, dout, dvv) if dout else 0)
+    assert n >= need, (n, need)

@@ -340,6 +340,35 @@ def test_project_standalone(T, E, dv, dvv, dout):
     assert err <= 2e-2
 
 
+def test_project_banded_split_k_stays_in_workspace():
+    """An output linear whose fp32 input (400 x 2^20, 1.68 GB) is launched in two bands of rows
+    (384 and 16) with K split per band: the partial sums stay inside the workspace the library
+    asked for (a guard region behind it keeps its fill), and sampled rows match the oracle."""
+    T, dv, dout = 400, 1 << 20, 8
+    log(f"[case] banded project T={T} K={dv} N={dout}")
+    st, nws = U.umem_project_workspace_size(T, 1, dv, 0, dout)
+    U.check(st)
+    guard = 1 << 20
+    ws = torch.full((nws + guard,), 0x5A, dtype=torch.uint8, device="cuda")
+    gen = torch.Generator(device="cuda").manual_seed(40)
+    pooled = torch.randn((T, 1, dv), generator=gen, dtype=torch.float32, device="cuda")
+    rng = np.random.default_rng(40)
+    wo = S.f32_to_bf16_bits(rng.standard_normal((dv, dout)) / np.sqrt(dv)).reshape(dv, dout)
+    out = torch.empty((T, dout), dtype=torch.float32, device="cuda")
+    U.check(U.umem_project(T, 1, dv, 0, dout, pooled, None,
+                           torch.from_numpy(CF.output_major(wo).view(np.int16)).cuda(), out, ws, nws))
+    torch.cuda.synchronize()
+    assert bool((ws[nws:] == 0x5A).all()), "split-K partials written past the workspace"
+    rows = np.array([0, 1, 200, 383, 384, 390, 399])
+    a = pooled[torch.from_numpy(rows).cuda(), 0].cpu().numpy().astype(np.float64)
+    ref = a @ S.bf16_bits_to_f32(wo).reshape(wo.shape).astype(np.float64)
+    got = out.cpu().numpy()[rows]
+    err = (np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1)).max()
+    log(f"[report] banded project: err={err:.2e}")
+    assert err <= 2e-2
+    del pooled, ws
+
+
 # ---------------------------------------------------------------- the paper-scale workloads
 
 def test_c2_prefill_sampled():
