@@ -51,7 +51,9 @@ typedef enum umem_status {
   UMEM_ERR_INVALID_ARG = -1, /* a null pointer, a bad size or a misaligned buffer */
   UMEM_ERR_UNSUPPORTED = -2, /* valid for the paper, beyond this library's limits (below) */
   UMEM_ERR_WORKSPACE = -3,   /* ws too small or misaligned */
-  UMEM_ERR_HIP = -4          /* a HIP launch failed */
+  UMEM_ERR_HIP = -4,         /* a HIP launch failed */
+  UMEM_ERR_SCRATCH_LIMIT = -5 /* umem_forward_noalloc: the call needs more scratch than
+                               * UMEM_STATIC_SCRATCH_BYTES */
 } umem_status;
 
 enum { UMEM_F32 = 0, UMEM_BF16 = 1 };             /* value-table element type */
@@ -197,6 +199,31 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
                          const void* values, const int32_t* perm, const uint16_t* w_proj,
                          const uint16_t* w_out, float* out, int32_t* idx_out,
                          float* w_out_scores, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Bytes of the library's static scratch array (one per GPU), which umem_forward_noalloc uses in
+ * place of a workspace argument. */
+#define UMEM_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* umem_forward for callers that cannot allocate memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the same kernels and results, with the
+ * workspace taken from a static array of UMEM_STATIC_SCRATCH_BYTES in each GPU's memory instead
+ * of the caller.  Neither this call nor the kernels it enqueues allocate or free memory.
+ *   Arguments as for umem_forward, without ws and ws_bytes.
+ *   UMEM_ERR_SCRATCH_LIMIT (nothing enqueued) when umem_workspace_size(desc, T) exceeds
+ *   UMEM_STATIC_SCRATCH_BYTES (the 20.07M-slot decode layer fits up to 708 tokens).
+ *   The array of a GPU is created with the library's code on that GPU and held until the process
+ *   ends; the first call on a device looks up its address (UMEM_ERR_HIP if that fails).  `stream`
+ *   must belong to the calling thread's current device.  Every call on one GPU uses the same
+ *   array and leaves its contents behind (nothing in it needs clearing between calls): calls
+ *   that may run at the same time on one GPU (other streams, other threads) race on it and must
+ *   be serialised by the caller. */
+UMEM_API umem_status umem_forward_noalloc(const umem_desc* desc, int32_t T, const float* q_row,
+                                          const float* q_col, const float* k_row,
+                                          const float* k_col, const float* core,
+                                          const void* values, const int32_t* perm,
+                                          const uint16_t* w_proj, const uint16_t* w_out,
+                                          float* out, int32_t* idx_out, float* w_out_scores,
+                                          hipStream_t stream);
 
 /* Backward of the gather-sum (eq. (1); eq. (15) per virtual block; eq. (17) per column slice),
  * for training: with the selection of the forward held fixed,

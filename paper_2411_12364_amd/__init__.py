@@ -26,12 +26,15 @@ UMEM_ERR_INVALID_ARG = -1
 UMEM_ERR_UNSUPPORTED = -2
 UMEM_ERR_WORKSPACE = -3
 UMEM_ERR_HIP = -4
+UMEM_ERR_SCRATCH_LIMIT = -5
+UMEM_STATIC_SCRATCH_BYTES = 64 << 20
 UMEM_F32, UMEM_BF16 = 0, 1
 UMEM_GRID_ADD, UMEM_GRID_TUCKER = 0, 1
 UMEM_W_RAW, UMEM_W_SOFTMAX = 0, 1
 
 EXPORTED = ("umem_workspace_size", "umem_axis_scores", "umem_select", "umem_score_topk",
             "umem_gather_sum", "umem_project_workspace_size", "umem_project", "umem_forward",
+            "umem_forward_noalloc",
             "umem_query_workspace_size", "umem_query", "umem_key_norm",
             "umem_gather_backward_workspace_size", "umem_gather_backward",
             "umem_score_backward_workspace_size", "umem_score_backward", "umem_status_string")
@@ -75,6 +78,7 @@ def _load() -> ctypes.CDLL:
         "umem_project_workspace_size": [I32, I32, I32, I32, I32, ctypes.POINTER(SZ)],
         "umem_project": [I32, I32, I32, I32, I32, P, P, P, P, P, SZ, P],
         "umem_forward": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
+        "umem_forward_noalloc": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P],
         "umem_query_workspace_size": [ctypes.POINTER(umem_query_desc), I32, I32, ctypes.POINTER(SZ)],
         "umem_query": [ctypes.POINTER(umem_query_desc), I32, I32, P, P, P, P, P, P, P, P, P, SZ, P],
         "umem_key_norm": [I32, I32, I32, P, P, P, ctypes.c_float, P, P],
@@ -179,6 +183,13 @@ def umem_forward(desc, T, q_row, q_col, k_row, k_col, core, values, perm, w_proj
     return _lib.umem_forward(_d(desc), T, _p(q_row), _p(q_col), _p(k_row), _p(k_col), _p(core),
                              _p(values), _p(perm), _p(w_proj), _p(w_out), _p(out), _p(idx_out),
                              _p(w_out_scores), _p(ws), ws_bytes, _s(stream))
+
+
+def umem_forward_noalloc(desc, T, q_row, q_col, k_row, k_col, core, values, perm, w_proj, w_out,
+                         out, idx_out, w_out_scores, stream=None) -> int:
+    return _lib.umem_forward_noalloc(_d(desc), T, _p(q_row), _p(q_col), _p(k_row), _p(k_col),
+                                     _p(core), _p(values), _p(perm), _p(w_proj), _p(w_out), _p(out),
+                                     _p(idx_out), _p(w_out_scores), _s(stream))
 
 
 def umem_query_workspace_size(qd, B, L):

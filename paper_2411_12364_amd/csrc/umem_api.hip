@@ -5,6 +5,7 @@
 #include <cmath>
 
 #include <algorithm>
+#include <mutex>
 
 #include "umem_internal.h"
 
@@ -435,12 +436,15 @@ UMEM_API umem_status umem_score_backward(const umem_desc* desc, int32_t T, const
                                           dq_row, dq_col, dk_row, dk_col, dcore, ws, stream));
 }
 
-UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float* q_row,
-                                  const float* q_col, const float* k_row, const float* k_col,
-                                  const float* core, const void* values, const int32_t* perm,
-                                  const uint16_t* w_proj, const uint16_t* w_out, float* out,
-                                  int32_t* idx_out, float* w_out_scores, void* ws,
-                                  size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+umem_status forward_into(const umem_desc* desc, int32_t T, const float* q_row, const float* q_col,
+                         const float* k_row, const float* k_col, const float* core,
+                         const void* values, const int32_t* perm, const uint16_t* w_proj,
+                         const uint16_t* w_out, float* out, int32_t* idx_out, float* w_out_scores,
+                         void* ws, size_t ws_bytes, hipStream_t stream) {
   umem_status st = check_desc(desc);
   if (st == UMEM_OK) st = check_tokens(T);
   if (st != UMEM_OK || T == 0) return st;
@@ -488,6 +492,69 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
   return hip_status(e);
 }
 
+// The scratch of umem_forward_noalloc: one array in each GPU's memory, loaded with the library's
+// code and held until the process ends.  Host code must not pass its name to a kernel (on the
+// host it is only a stand-in for the device symbol); the device address of each GPU's copy is
+// looked up once per device and kept in static_scratch_ptr.
+static __device__ __align__(256) unsigned char scratch[UMEM_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::once_flag scratch_once[kMaxDevices];
+void* scratch_ptr[kMaxDevices];
+hipError_t scratch_err[kMaxDevices];
+
+// The address of the current device's copy of `scratch` (its first call on a device looks it
+// up, with that device current).
+hipError_t static_scratch_ptr(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::call_once(scratch_once[dev], [dev] {
+    void* p = nullptr;
+    const hipError_t r = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    scratch_err[dev] = r;
+    scratch_ptr[dev] = r == hipSuccess ? p : nullptr;
+  });
+  *ptr = scratch_ptr[dev];
+  return scratch_err[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float* q_row,
+                                  const float* q_col, const float* k_row, const float* k_col,
+                                  const float* core, const void* values, const int32_t* perm,
+                                  const uint16_t* w_proj, const uint16_t* w_out, float* out,
+                                  int32_t* idx_out, float* w_out_scores, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  return forward_into(desc, T, q_row, q_col, k_row, k_col, core, values, perm, w_proj, w_out, out,
+                      idx_out, w_out_scores, ws, ws_bytes, stream);
+}
+
+UMEM_API umem_status umem_forward_noalloc(const umem_desc* desc, int32_t T, const float* q_row,
+                                          const float* q_col, const float* k_row,
+                                          const float* k_col, const float* core,
+                                          const void* values, const int32_t* perm,
+                                          const uint16_t* w_proj, const uint16_t* w_out,
+                                          float* out, int32_t* idx_out, float* w_out_scores,
+                                          hipStream_t stream) {
+  umem_status st = check_desc(desc);
+  if (st == UMEM_OK) st = check_tokens(T);
+  if (st != UMEM_OK || T == 0) return st;
+  // no kernel of the forward needs its scratch cleared beforehand: every part is written before
+  // it is read, so the contents a previous call left behind do not matter
+  if (layout(desc, T).total > UMEM_STATIC_SCRATCH_BYTES) return UMEM_ERR_SCRATCH_LIMIT;
+  st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
+  if (st != UMEM_OK) return st;
+  void* ws = nullptr;
+  if (static_scratch_ptr(&ws) != hipSuccess) return UMEM_ERR_HIP;
+  return forward_into(desc, T, q_row, q_col, k_row, k_col, core, values, perm, w_proj, w_out, out,
+                      idx_out, w_out_scores, ws, UMEM_STATIC_SCRATCH_BYTES, stream);
+}
+
 UMEM_API const char* umem_status_string(umem_status status) {
   switch (status) {
     case UMEM_OK: return "ok";
@@ -495,6 +562,7 @@ UMEM_API const char* umem_status_string(umem_status status) {
     case UMEM_ERR_UNSUPPORTED: return "unsupported by this library";
     case UMEM_ERR_WORKSPACE: return "workspace too small or misaligned";
     case UMEM_ERR_HIP: return "HIP launch error";
+    case UMEM_ERR_SCRATCH_LIMIT: return "needs more scratch than the static buffer holds";
   }
   return "unknown status";
 }
