@@ -398,3 +398,81 @@ ALL_PINS = [
     pin_tucker_rank_one_slices, pin_ive_materialised, pin_ive_concat_same_column,
     pin_golden_mcs, pin_mcs_scores_add_up, pin_mcs_dense_pool,
 ]
+
+
+# ---------------------------------------------------------------- the oracle at paper scale
+
+def exhaustive_topm_product_keys(q_row, q_col, K_row, K_col, m):
+    """The m best of all n*n slots of one (token, head) under eq. (1) with product keys: slot
+    (i, j) has the full key [K_row[i], K_col[j]], so its score against the full query
+    [q_row, q_col] is K_row[i].q_row + K_col[j].q_col.  The whole n x n grid is materialised in
+    fp64 and ordered by (score desc, flat index i*n + j asc).  Returns (flat indices, scores)."""
+    a = np.asarray(K_row, np.float64) @ np.asarray(q_row, np.float64)
+    b = np.asarray(K_col, np.float64) @ np.asarray(q_col, np.float64)
+    return _exhaustive_topm((a[:, None] + b[None, :]).reshape(-1), m)
+
+
+def exhaustive_topm_tucker(q_row, q_col, K_row, K_col, C, m):
+    """The m best of all n*n slots under the exact Tucker score of eqs. (4)-(5): with the r
+    slices of the query/key dim, S_row[rho, i] = K_row[i, slice rho] . q_row[slice rho] (the same
+    for columns) and g(i, j) = sum_{rho, sigma} S_row[rho, i] C[rho, sigma] S_col[sigma, j], the
+    whole n x n grid in fp64.  Returns (flat indices, scores)."""
+    C = np.asarray(C, np.float64)
+    r = C.shape[0]
+    w = len(q_row) // r
+    Sr = np.stack([np.asarray(K_row, np.float64)[:, s * w:(s + 1) * w] @ np.asarray(q_row[s * w:(s + 1) * w], np.float64)
+                   for s in range(r)])
+    Sc = np.stack([np.asarray(K_col, np.float64)[:, s * w:(s + 1) * w] @ np.asarray(q_col[s * w:(s + 1) * w], np.float64)
+                   for s in range(r)])
+    return _exhaustive_topm((Sr.T @ C @ Sc).reshape(-1), m)
+
+
+def _exhaustive_topm(g, m):
+    part = np.argpartition(-g, m - 1)[:m]
+    cut = g[part].min()                          # the m-th largest score
+    cand = np.flatnonzero(g >= cut)              # every slot that can rank among the m best
+    order = np.lexsort((cand, -g[cand]))         # score desc, then flat index asc
+    best = cand[order[:m]]
+    return best, g[best]
+
+
+def pin_exhaustive_topm_paper_scale(O, cfg_names=("decode-20M", "prefill-1M"), tokens=(0, 1, 2)):
+    """Sec. 3.1: with k >= m the two-phase top-m (per-axis top-k, then the grid) is the top-m of
+    all N slots.  Checked on the paper-scale layers the oracle is used at: 4480^2 = 20,070,400
+    slots of the decode layer and 1024^2 of the prefill layer (k = m = 32, two heads), against
+    the whole grid of eq. (1) scores.  Also the raw weights are the exact slot scores."""
+    from synth import configs as CF
+    for name in cfg_names:
+        cfg = CF.CONFIGS[name]
+        qr, qc = CF.queries(cfg, batch=0, tokens=np.asarray(tokens))
+        kr, kc = CF.keys(cfg)
+        res = O.score_topk(qr, qc, kr, kc, cfg.topk, cfg.topm)
+        for t in range(len(tokens)):
+            for h in range(cfg.heads):
+                want, g = exhaustive_topm_product_keys(qr[t, h], qc[t, h], kr[h], kc[h], cfg.topm)
+                assert np.array_equal(res["idx"][t, h], want), (name, t, h)
+                assert np.allclose(res["w"][t, h], g, rtol=1e-12, atol=1e-15), (name, t, h)
+
+
+SCALE_PINS = [pin_exhaustive_topm_paper_scale]
+
+
+def tucker_recall(O, cfg, tokens):
+    """Recall@m of the paper's rank-1 retrieval (eqs. (7)-(10): per-axis top-k on the leading
+    singular pair's factors, then the exact score of the k*k candidates) against the exhaustive
+    exact-Tucker top-m of all n*n slots (the core a head uses; with multi-core scoring, the sum
+    of its components, eq. (16)).  Not a pass/fail property: the rank-1 factors only approximate
+    the bilinear score (their product has either sign).  Returns per-(token, head) recalls."""
+    from synth import configs as CF
+    qr, qc = CF.queries(cfg, batch=0, tokens=np.asarray(tokens))
+    kr, kc = CF.keys(cfg)
+    core = np.asarray(CF.core(cfg), np.float64)
+    if cfg.cores > 1:
+        core = core.sum(axis=1)
+    res = O.score_topk(qr, qc, kr, kc, cfg.topk, cfg.topm, O.GRID_TUCKER, O.W_RAW, core, cfg.rank)
+    rec = np.zeros((len(tokens), cfg.heads))
+    for t in range(len(tokens)):
+        for h in range(cfg.heads):
+            want, _ = exhaustive_topm_tucker(qr[t, h], qc[t, h], kr[h], kc[h], core[h], cfg.topm)
+            rec[t, h] = len(set(want.tolist()) & set(res["idx"][t, h].tolist())) / cfg.topm
+    return rec

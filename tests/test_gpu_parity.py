@@ -226,15 +226,18 @@ def test_multi_core_scoring(kw):
 
 def test_paper_model_layer_sampled():
     """One memory layer of the paper's UltraMem-1.6B-x12 model (Kdim 448, 1792^2 slots, top-42 of
-    2 heads, r = 2, h = 2, E = 4, 8 KiB rows) at a 512-token decode batch."""
+    2 heads, r = 2, h = 2, E = 4, 8 KiB rows) at a 512-token decode batch: 256 of its tokens."""
     rng = np.random.default_rng(6)
-    run_and_check(CF.C6, tokens=np.sort(rng.choice(CF.C6.T, 8, replace=False)))
+    run_and_check(CF.C6, tokens=np.sort(rng.choice(CF.C6.T, 256, replace=False)))
 
 
 def test_c5_tucker_ive_mcs_sampled():
-    """The rank-2 Tucker + IVE layer with the paper's default two component cores."""
+    """The rank-2 Tucker + IVE layer with the paper's default two component cores: 256 tokens,
+    the first and last among them."""
     cfg = dataclasses.replace(CF.C5, cores=2, name="tucker-ive-mcs-4M")
-    run_and_check(cfg, tokens=np.array([0, 1, 2, 1023, 2048, 4095]))
+    rng = np.random.default_rng(55)
+    tokens = np.union1d([0, 1, 2, 1023, 2048, 4095], rng.choice(cfg.T, 250, replace=False))
+    run_and_check(cfg, tokens=tokens)
 
 
 # ---------------------------------------------------------------- a7 inside the selection
@@ -373,23 +376,52 @@ def test_project_banded_split_k_stays_in_workspace():
 
 def test_c2_prefill_sampled():
     rng = np.random.default_rng(2)
-    run_and_check(CF.C2, tokens=np.sort(rng.choice(CF.C2.T, 48, replace=False)))
+    run_and_check(CF.C2, tokens=np.sort(rng.choice(CF.C2.T, 256, replace=False)))
 
 
-def test_c3_decode_20m_full_size():
-    run_and_check(CF.C3)          # every token of the 32-token decode batch, 20.07M-slot table
+@pytest.fixture(scope="module")
+def c3_values():
+    """The 20.07M x 512 bf16 value table of the decode layer (20.55 GB), drawn once for the decode
+    tests of this module."""
+    cfg = CF.C3
+    v = torch.empty((cfg.n_values, cfg.dv), dtype=torch.bfloat16, device="cuda")
+    SD.fill_normal_(v, cfg.seed, S.TID_VALUES, CF.value_std(cfg))
+    yield v
+    del v
+    torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("T", [1, 1024])
-def test_c4_decode_batches(T):
+def test_c3_decode_20m_full_size(c3_values):
+    # every token of the 32-token decode batch, 20.07M-slot table
+    run_and_check(CF.C3, dl=SD.make_layer(CF.C3, values=c3_values))
+
+
+@pytest.mark.parametrize("T", CF.C4_BATCHES)
+def test_c4_decode_batches(T, c3_values):
+    """The decode batch sweep on the 20.07M-slot layer.  Up to 512 tokens the selection pools the
+    rows itself (scoring clears the output first: the split, 32 x 32 and, above 64 tokens, the
+    bf16-plane kernel); at 1024 the gather kernel pools them.  Every token up to 256, 256 of
+    1024."""
     rng = np.random.default_rng(T)
-    tokens = None if T <= 64 else np.sort(rng.choice(T, 32, replace=False))
-    run_and_check(CF.C3.with_tokens(T), batch=1, tokens=tokens)
+    tokens = None if T <= 256 else np.sort(rng.choice(T, 256, replace=False))
+    cfg = CF.C3.with_tokens(T)
+    run_and_check(cfg, batch=1, tokens=tokens, dl=SD.make_layer(cfg, batches=2, values=c3_values))
+
+
+@pytest.mark.parametrize("n_keys", [300, 301], ids=["planes", "tiled"])
+def test_fused_forward_many_tokens(n_keys):
+    """The forward with the selection pooling the rows for 64 < T <= 512 tokens (two heads, 1 KiB
+    bf16 rows, no projection): the scoring kernel, here the bf16-plane one (n % 4 == 0) or the
+    tiled fp32 MFMA one (n % 4 != 0), clears the output with its grid before the selection adds
+    both heads' rows into it.  A ragged last token tile (130 = 128 + 2)."""
+    cfg = small("fused-many", T=130, heads=2, dk=128, n_keys=n_keys, topk=16, topm=24, dv=512,
+                vdtype=CF.BF16, seed=31)
+    run_and_check(cfg)
 
 
 def test_c5_tucker_ive_sampled():
     rng = np.random.default_rng(5)
-    run_and_check(CF.C5, tokens=np.sort(rng.choice(CF.C5.T, 12, replace=False)))
+    run_and_check(CF.C5, tokens=np.sort(rng.choice(CF.C5.T, 256, replace=False)))
 
 
 @pytest.mark.parametrize("heads", [1, 2])

@@ -20,3 +20,30 @@ def test_rejects_nan_and_degenerate_core():
     with pytest.raises(ValueError):
         O.score_topk(np.zeros((1, 1, 2)), np.zeros((1, 1, 2)), np.zeros((1, 3, 2)),
                      np.zeros((1, 3, 2)), topk=2, topm=5)
+
+
+@pytest.mark.parametrize("pin", __import__("tests.pins", fromlist=["SCALE_PINS"]).SCALE_PINS,
+                         ids=lambda p: p.__name__)
+def test_pin_paper_scale(pin):
+    pin(O)
+
+
+@pytest.mark.parametrize("name", ["tucker-ive-4M", "tucker-ive-mcs-4M", "ultramem-1.6B-x12"])
+def test_report_tucker_recall(name, capsys):
+    """The recall of the rank-1 Tucker retrieval against the exhaustive exact-Tucker top-m on
+    sampled tokens of the Tucker layers (reported, not asserted beyond its range)."""
+    import dataclasses
+
+    import numpy as np
+
+    from synth import configs as CF
+    from tests.pins import tucker_recall
+    cfg = (dataclasses.replace(CF.C5, cores=2, name=name) if name == "tucker-ive-mcs-4M"
+           else {c.name: c for c in (CF.C5, CF.C6)}[name])
+    tokens = np.sort(np.random.default_rng(7).choice(cfg.T, 24, replace=False))
+    rec = tucker_recall(O, cfg, tokens)
+    assert ((rec >= 0) & (rec <= 1)).all()
+    with capsys.disabled():
+        print(f"\n[recall] {name}: rank-1 retrieval recall@{cfg.topm} of the exact Tucker top-"
+              f"{cfg.topm} over {rec.size} (token, head) pairs: mean {rec.mean():.4f}, "
+              f"min {rec.min():.4f}, max {rec.max():.4f}")
