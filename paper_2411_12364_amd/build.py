@@ -10,6 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libumem.so")
+PROBE_LIB = os.path.join(PKG, "libumem_probe.so")
 SOURCES = ["umem_api.hip", "score.hip", "select.hip", "gather.hip", "project.hip", "query.hip", "sort.hip", "backward.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -44,6 +45,10 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)
+    # the benchmark's read-bandwidth probes: a library of their own, outside the layer's ABI
+    tmp = PROBE_LIB + ".tmp"
+    _run([HIPCC, *FLAGS, "-shared", os.path.join(CSRC, "probe.hip"), "-o", tmp])
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 
