@@ -316,6 +316,15 @@ class Runner:
             tot += int(self.torch.unique(rows).numel())
         return tot / self.R
 
+    def time_probe_rows(self, probe, launches=64):
+        """Average seconds per launch of the read probe over exactly the rows the selections of
+        the rotating query batches gather (one launch per batch, T x bag rows), for comparison
+        with the gather kernel on the same rows (kept from time_kernels)."""
+        idxs, _ = self.queue_inputs
+        c = self.cfg
+        return self._graph_time([lambda b=b: probe.read_rows(self.dl.values, c.dv * c.vbytes,
+                                                              idxs[b % self.R]) for b in range(launches)])
+
     def time_kernels(self, launches_per_kernel, queue=False):
         """Average duration (us) of each kernel of the forward, launched back to back from a HIP
         graph with distinct inputs per launch: the scoring over the rotating query batches, the
@@ -676,22 +685,30 @@ def gather_figure(cfg, T, st, fused):
                 avg_us=round(st[name], 3), GBps=round(gbps, 1), frac_of_peak=round(gbps / HBM_PEAK_GBS, 4))
 
 
-def sweep(base_cfg, values, flusher, steps=512, warmup=30):
+def sweep(base_cfg, values, flusher, probe, steps=512, warmup=30):
     """The decode forward at T = 1 ... 1024 on the same table; the gather figure is taken from
-    the kernel that pools the rows in that forward."""
+    the kernel that pools the rows in that forward.  Where that is the gather kernel, the read
+    probe over exactly the same rows is timed beside it: the ceiling of one launch of that size."""
     res = []
     for T in (1, 4, 16, 64, 256, 1024):
         cfg = base_cfg.with_tokens(T)
         R = distinct_batches(T, cfg.bag * cfg.dv * cfg.vbytes)
         r = Runner(cfg, R, values, flusher)
         secs, n = r.time_forward(steps, warmup)
-        st = r.time_kernels(min(steps, 512))
+        st = r.time_kernels(min(steps, 512), queue=not r.fused)
         gf = gather_figure(cfg, T, st, r.fused)
-        res.append(dict(tokens=T, query_batches=R, us_per_step=round(secs / n * 1e6, 2),
-                        tokens_per_s=round(T * n / secs, 1),
-                        kernel_us={k: round(v, 2) for k, v in st.items()},
-                        gather_kernel=gf["kernel"], gather_GBps=gf["GBps"],
-                        gather_frac=gf["frac_of_peak"]))
+        row = dict(tokens=T, query_batches=R, us_per_step=round(secs / n * 1e6, 2),
+                   tokens_per_s=round(T * n / secs, 1),
+                   kernel_us={k: round(v, 2) for k, v in st.items()},
+                   gather_kernel=gf["kernel"], gather_GBps=gf["GBps"],
+                   gather_frac=gf["frac_of_peak"])
+        if not r.fused:
+            p_us = r.time_probe_rows(probe) * 1e6
+            row.update(probe_same_rows_us=round(p_us, 2),
+                       probe_same_rows_GBps=round(gf["row_bytes"] / (p_us * 1e-6) / 1e9, 1),
+                       gather_frac_of_probe=round(p_us / st["gather_kernel"], 4))
+            r.queue_inputs = None
+        res.append(row)
         log(f"sweep T={T}: {res[-1]}")
         del r
         import torch
@@ -826,7 +843,7 @@ def main():
     step_bytes = sum(kernel_work(cfg, cfg.T, fused)[k]["bytes"] for k in fwd_kernels)
     values = r.dl.values
     del r
-    sw = None if args.no_sweep else sweep(cfg, values, flusher)
+    sw = None if args.no_sweep else sweep(cfg, values, flusher, probe)
     del values
     torch.cuda.empty_cache()
     wl = None if args.no_workloads else [workload_report(c, flusher) for c in extra_workloads(CF)]
@@ -852,7 +869,8 @@ def main():
         "gather_queue": queue,
         "probe": probe_rep,
         "batch_sweep": None if sw is None else [
-            {k: s[k] for k in ("tokens", "us_per_step", "tokens_per_s", "gather_GBps", "gather_frac")}
+            {k: s[k] for k in ("tokens", "us_per_step", "tokens_per_s", "gather_GBps", "gather_frac",
+                               "probe_same_rows_GBps", "gather_frac_of_probe") if k in s}
             for s in sw],
         "workloads": None if wl is None else {
             w["workload"]: dict(us_per_step=w["us_per_step"], tokens_per_s=w["tokens_per_s"],
