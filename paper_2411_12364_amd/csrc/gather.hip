@@ -11,7 +11,10 @@
 // implicit value expansion the projection reads them next and finds them cached.  With implicit
 // value expansion the bag is first mapped through the shuffle and split by virtual block p (a
 // stable partition), and each block's rows are pooled into out[t, p, :].  From 2048 tokens on
-// (without expansion) a wave per token does the same work without LDS or barriers.
+// (without expansion) a wave per token does the same work without LDS or barriers.  Pooled rows
+// leave as fp32, or, for the forward's projection, rounded to bf16 (nearest even) by the same
+// instruction with which the projection GEMM rounds its A operand while staging it: the GEMM
+// then reads half the bytes and computes exactly what it computed from the fp32 rows.
 #include "umem_internal.h"
 
 namespace umem {
@@ -28,7 +31,23 @@ constexpr int kWaveTokensMin = UMEM_GATHER_WAVE_TOKENS;   // from here on, a wav
 #endif
 constexpr int kWaveBatch = UMEM_GATHER_WAVE_BATCH;       // 16-byte loads per lane per batch
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Four pooled values stored as fp32, or as bf16 bits (one v_cvt_pk_bf16_f32 per pair).
+template <bool NT>
+__device__ __forceinline__ void put4(float* dst, f32x4 v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(dst));
+  else *reinterpret_cast<f32x4*>(dst) = v;
+}
+template <bool NT>
+__device__ __forceinline__ void put4(uint16_t* dst, f32x4 v) {
+  const u32x2 p{__builtin_bit_cast(uint32_t, bf16x2{static_cast<__bf16>(v.x), static_cast<__bf16>(v.y)}),
+                __builtin_bit_cast(uint32_t, bf16x2{static_cast<__bf16>(v.z), static_cast<__bf16>(v.w)})};
+  if constexpr (NT) __builtin_nontemporal_store(p, reinterpret_cast<u32x2*>(dst));
+  else *reinterpret_cast<u32x2*>(dst) = p;
+}
 
 template <typename Elem>
 struct ElemTraits;
@@ -62,11 +81,11 @@ struct ElemTraits<uint16_t> {   // bf16 bit patterns
 // `slot(j)` gives entry j's position in idx / w (after the block partition, if any).  With
 // multi-core scoring (cores > 1) entry s has cores weights, w_of[s * cores + i], and a lane's
 // 16-byte chunk takes the weight of the column slice it lies in.
-template <typename Elem, int L, int CPL, bool KEEP, typename Slot>
+template <typename Elem, int L, int CPL, bool KEEP, typename Out, typename Slot>
 __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int dv, int cnt,
                                           const Slot& slot, const int32_t* __restrict__ rows_of,
                                           const float* __restrict__ w_of, int cores, float* red,
-                                          float* __restrict__ dst) {
+                                          Out* __restrict__ dst) {
   using TR = ElemTraits<Elem>;
   constexpr int EPC = TR::kPerChunk;
   constexpr int SUB = kWave / L;                   // rows a wave reads at once
@@ -169,25 +188,25 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
       r.w += x.w;
     }
     // plain stores: the projection that follows reads the pooled rows from cache
-    *reinterpret_cast<f32x4*>(dst + col) = f32x4{r.x, r.y, r.z, r.w};
+    put4<false>(dst + col, f32x4{r.x, r.y, r.z, r.w});
   }
 }
 
 // Without expansion the bag is read straight from idx / w (for rows of 64 lanes a wave's row
 // index is uniform and lives in scalar registers).  With expansion the bag is first mapped
 // through perm and stably partitioned by virtual block in LDS.
-template <typename Elem, int L, int CPL, bool KEEP>
+template <typename Elem, int L, int CPL, bool KEEP, typename Out>
 __global__ __launch_bounds__(THREADS) void gather_kernel(
     const Elem* __restrict__ values, int64_t n_values, int dv, int bag,
     const int32_t* __restrict__ idx, const float* __restrict__ w, const int32_t* __restrict__ perm,
-    int expand, int cores, float* __restrict__ out) {
+    int expand, int cores, Out* __restrict__ out) {
   extern __shared__ __align__(16) float red[];               // [red_rows][dv], then the bag
   const int t = blockIdx.x;
   const int32_t* __restrict__ idx_t = idx + static_cast<size_t>(t) * bag;
   const float* __restrict__ w_t = w + static_cast<size_t>(t) * bag * cores;
   if (expand == 1) {
-    pool_rows<Elem, L, CPL, KEEP>(values, dv, bag, [](int j) { return j; }, idx_t, w_t, cores, red,
-                                  out + static_cast<size_t>(t) * dv);
+    pool_rows<Elem, L, CPL, KEEP, Out>(values, dv, bag, [](int j) { return j; }, idx_t, w_t, cores,
+                                       red, out + static_cast<size_t>(t) * dv);
     return;
   }
   int32_t* rows = reinterpret_cast<int32_t*>(red + (dv <= 2048 ? NWAVES : 2) * dv);   // [bag]
@@ -222,8 +241,9 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
   __syncthreads();
   for (int p = 0; p < expand; ++p) {
     const int beg = bstart[p];
-    pool_rows<Elem, L, CPL, KEEP>(values, dv, bcount[p], [=](int j) { return order[beg + j]; }, rows,
-                                  w_t, cores, red, out + (static_cast<size_t>(t) * expand + p) * dv);
+    pool_rows<Elem, L, CPL, KEEP, Out>(values, dv, bcount[p], [=](int j) { return order[beg + j]; },
+                                       rows, w_t, cores, red,
+                                       out + (static_cast<size_t>(t) * expand + p) * dv);
     __syncthreads();
   }
 }
@@ -233,10 +253,10 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
 // per lane, and each row's index taken from its lane (readlane; a shuffle for sub-rows); the
 // row loads run double-buffered, batch b + 1 in flight while batch b accumulates.  With
 // thousands of tokens the CUs hold many such waves at once.
-template <typename Elem, int L, int CPL>
+template <typename Elem, int L, int CPL, typename Out>
 __global__ __launch_bounds__(THREADS) void gather_wave_kernel(
     const Elem* __restrict__ values, int dv, int T, int bag, const int32_t* __restrict__ idx,
-    const float* __restrict__ w, float* __restrict__ out) {
+    const float* __restrict__ w, Out* __restrict__ out) {
   using TR = ElemTraits<Elem>;
   constexpr int EPC = TR::kPerChunk;
   constexpr int SUB = kWave / L;
@@ -313,20 +333,19 @@ __global__ __launch_bounds__(THREADS) void gather_wave_kernel(
 #pragma unroll
       for (int e = 0; e < EPC; ++e) acc[c][e] += __shfl_xor(acc[c][e], off, kWave);
   if (sub == 0) {
-    float* dst = out + static_cast<size_t>(t) * dv;
+    Out* dst = out + static_cast<size_t>(t) * dv;
 #pragma unroll
     for (int c = 0; c < CPL; ++c)
 #pragma unroll
       for (int e = 0; e < EPC; e += 4)
-        __builtin_nontemporal_store(f32x4{acc[c][e], acc[c][e + 1], acc[c][e + 2], acc[c][e + 3]},
-                                    reinterpret_cast<f32x4*>(dst + (cl + L * c) * EPC + e));
+        put4<true>(dst + (cl + L * c) * EPC + e, f32x4{acc[c][e], acc[c][e + 1], acc[c][e + 2], acc[c][e + 3]});
   }
 }
 
-template <typename Elem>
+template <typename Elem, typename Out>
 hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int bag,
                         const int32_t* idx, const float* w, const int32_t* perm, int expand,
-                        int cores, float* out, hipStream_t s) {
+                        int cores, Out* out, hipStream_t s) {
   const int chunks = dv * static_cast<int>(sizeof(Elem)) / 16;
   const size_t lds = static_cast<size_t>(dv <= 2048 ? NWAVES : 2) * dv * 4 +
                     (expand > 1 ? static_cast<size_t>(bag) * 12 : 0);
@@ -338,13 +357,13 @@ hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int
   const bool keep = 4 * static_cast<int64_t>(T) * bag >= n_values;
 #define UMEM_GATHER(LL, CC)                                                                      \
   if (per_wave)                                                                                  \
-    hipLaunchKernelGGL((gather_wave_kernel<Elem, LL, CC>), grid, block, 0, s, values, dv, T, bag, \
-                       idx, w, out);                                                             \
+    hipLaunchKernelGGL((gather_wave_kernel<Elem, LL, CC, Out>), grid, block, 0, s, values, dv, T, \
+                       bag, idx, w, out);                                                        \
   else if (keep)                                                                                 \
-    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC, true>), grid, block, lds, s, values, n_values, \
-                       dv, bag, idx, w, perm, expand, cores, out);                               \
+    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC, true, Out>), grid, block, lds, s, values,      \
+                       n_values, dv, bag, idx, w, perm, expand, cores, out);                     \
   else                                                                                           \
-    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC, false>), grid, block, lds, s, values,          \
+    hipLaunchKernelGGL((gather_kernel<Elem, LL, CC, false, Out>), grid, block, lds, s, values,     \
                        n_values, dv, bag, idx, w, perm, expand, cores, out)
   switch (chunks) {
     case 1: UMEM_GATHER(1, 1); break;
@@ -367,6 +386,19 @@ hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int
   return hipGetLastError();
 }
 
+template <typename Out>
+hipError_t launch_any(int64_t n_values, int dv, int vdtype, const void* values, int T, int bag,
+                      const int32_t* idx, const float* w, const int32_t* perm, int expand,
+                      int cores, Out* out, hipStream_t s) {
+  clear_stale_error();
+  if (T == 0) return hipSuccess;
+  if (vdtype == UMEM_F32)
+    return launch_typed(static_cast<const float*>(values), n_values, dv, T, bag, idx, w, perm,
+                        expand, cores, out, s);
+  return launch_typed(static_cast<const uint16_t*>(values), n_values, dv, T, bag, idx, w, perm,
+                      expand, cores, out, s);
+}
+
 }  // namespace
 
 bool gather_row_supported(int dv, int vdtype) {
@@ -385,13 +417,13 @@ bool cores_supported(int dv, int vdtype, int cores) {
 hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* values, int T,
                          int bag, const int32_t* idx, const float* w, const int32_t* perm,
                          int expand, int cores, float* out, hipStream_t s) {
-  clear_stale_error();
-  if (T == 0) return hipSuccess;
-  if (vdtype == UMEM_F32)
-    return launch_typed(static_cast<const float*>(values), n_values, dv, T, bag, idx, w, perm,
-                        expand, cores, out, s);
-  return launch_typed(static_cast<const uint16_t*>(values), n_values, dv, T, bag, idx, w, perm,
-                      expand, cores, out, s);
+  return launch_any(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores, out, s);
+}
+
+hipError_t launch_gather_bf16(int64_t n_values, int dv, int vdtype, const void* values, int T,
+                              int bag, const int32_t* idx, const float* w, const int32_t* perm,
+                              int expand, int cores, uint16_t* out, hipStream_t s) {
+  return launch_any(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores, out, s);
 }
 
 }  // namespace umem

@@ -6,9 +6,10 @@
 // Trick 6 is a second GEMM of y by w_out [d_out, D'v].  Both operands are then rows of K.
 //
 // Tiles of 128 x 128 per workgroup, four waves of 64 x 64 (4 x 4 v_mfma_f32_16x16x32_bf16
-// tiles), K in steps of 64.  A (fp32) and B (bf16) are read with 16-byte buffer loads, whose
-// range check returns zeros past the rows of the matrix, so edge tiles need no branches; A is
-// rounded to bf16 (nearest even) as it is staged into LDS, B is copied.  The operand tiles are
+// tiles), K in steps of 64.  A (fp32, or bf16 when the producer already rounded it) and B (bf16)
+// are read with 16-byte buffer loads, whose range check returns zeros past the rows of the
+// matrix, so edge tiles need no branches; fp32 A is rounded to bf16 (nearest even) as it is
+// staged into LDS, bf16 A and B are copied.  The operand tiles are
 // double-buffered in LDS: while slice k is multiplied, slice k + 1 (fetched into registers
 // during step k - 1) is staged into the other buffer, and slice k + 2 is fetched after the
 // step's one barrier.  The output tile leaves through LDS as whole 128-byte lines.
@@ -45,11 +46,13 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// One K-slice of the operands in registers: eight 16-byte pieces of A (thread t, piece i: row
-// (t + 256 i) / 16, k ((t + 256 i) % 16) * 4) and four of B (row (t + 256 i) / 8, k
-// ((t + 256 i) % 8) * 8).
+// One K-slice of the operands in registers: of fp32 A eight 16-byte pieces (thread t, piece i:
+// row (t + 256 i) / 16, k ((t + 256 i) % 16) * 4), of bf16 A and of B four (row (t + 256 i) / 8,
+// k ((t + 256 i) % 8) * 8).
+template <typename AT>
 struct Slice {
-  u32x4 a[8];
+  static constexpr int kA = sizeof(AT) == 4 ? 8 : 4;
+  u32x4 a[kA];
   u32x4 b[4];
 };
 
@@ -61,13 +64,15 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t b
 
 // K-range [.., k_end) of this split; rows of K elements.  Rows past the matrix read as zeros by
 // the buffer range check; k past k_end is sent out of range explicitly.
+template <typename AT>
 __device__ __forceinline__ void fetch(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, int K,
-                                      int k_end, int m0, int n0, int k0, int tid, Slice& sl) {
+                                      int k_end, int m0, int n0, int k0, int tid, Slice<AT>& sl) {
+  constexpr int kPer = 16 / sizeof(AT);            // A elements per 16-byte piece
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < Slice<AT>::kA; ++i) {
     const int f = tid + THREADS * i;
-    const int gk = k0 + (f & 15) * 4;
-    const uint32_t off = static_cast<uint32_t>((m0 + (f >> 4)) * K + gk) * 4u;
+    const int gk = k0 + (f % (BK / kPer)) * kPer;
+    const uint32_t off = static_cast<uint32_t>((m0 + f / (BK / kPer)) * K + gk) * sizeof(AT);
     sl.a[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, gk < k_end ? off : kOutOfRange, 0, 0);
   }
 #pragma unroll
@@ -85,12 +90,16 @@ __device__ __forceinline__ uint32_t pack_bf16(uint32_t lo, uint32_t hi) {
                                               static_cast<__bf16>(__uint_as_float(hi))});
 }
 
-__device__ __forceinline__ void stage(const Slice& sl, uint16_t* As, uint16_t* Bs, int tid) {
+template <typename AT>
+__device__ __forceinline__ void stage(const Slice<AT>& sl, uint16_t* As, uint16_t* Bs, int tid) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < Slice<AT>::kA; ++i) {
     const int f = tid + THREADS * i;
-    *reinterpret_cast<u32x2*>(As + (f >> 4) * LDA + (f & 15) * 4) =
-        u32x2{pack_bf16(sl.a[i].x, sl.a[i].y), pack_bf16(sl.a[i].z, sl.a[i].w)};
+    if constexpr (sizeof(AT) == 4)
+      *reinterpret_cast<u32x2*>(As + (f >> 4) * LDA + (f & 15) * 4) =
+          u32x2{pack_bf16(sl.a[i].x, sl.a[i].y), pack_bf16(sl.a[i].z, sl.a[i].w)};
+    else
+      *reinterpret_cast<u32x4*>(As + (f >> 3) * LDA + (f & 7) * 8) = sl.a[i];
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -99,10 +108,11 @@ __device__ __forceinline__ void stage(const Slice& sl, uint16_t* As, uint16_t* B
   }
 }
 
-// A fp32 [M, K], B bf16 [N, K] (both rows of K, 16-byte aligned), C fp32 [M, N]; the bytes of A
-// and of B below 2^31.
+// A fp32 or bf16 [M, K], B bf16 [N, K] (both rows of K, 16-byte aligned), C fp32 [M, N]; the
+// bytes of A and of B below 2^31.
+template <typename AT>
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_bf16_kernel(
-    const float* __restrict__ A, const uint16_t* __restrict__ B, float* __restrict__ C, int M,
+    const AT* __restrict__ A, const uint16_t* __restrict__ B, float* __restrict__ C, int M,
     int N, int K, int n_tiles_n, int per_xcd, int n_tiles, int n_items, int k_chunk) {
   __shared__ __align__(16) uint16_t smem[2 * kTileElems];
   // item = split * n_tiles + tile; XCD x takes items [x per, (x + 1) per)
@@ -117,7 +127,7 @@ __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;         // this wave's 64 x 64 block of the tile
-  const __amdgpu_buffer_rsrc_t ra = rsrc(A, static_cast<uint32_t>(M) * K * 4u);
+  const __amdgpu_buffer_rsrc_t ra = rsrc(A, static_cast<uint32_t>(M) * K * static_cast<uint32_t>(sizeof(AT)));
   const __amdgpu_buffer_rsrc_t rb = rsrc(B, static_cast<uint32_t>(N) * K * 2u);
 
   f32x4 acc[4][4];
@@ -126,7 +136,7 @@ __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 #pragma unroll
     for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  Slice sl;
+  Slice<AT> sl;
   fetch(ra, rb, K, k_end, m0, n0, k_begin, tid, sl);
   stage(sl, smem, smem + BM * LDA, tid);
   __syncthreads();
@@ -235,13 +245,18 @@ size_t gemm_partial_bytes(int M, int N, int K) {
   return std::max(band_partial_bytes(static_cast<int>(band), N, K), band_partial_bytes(last, N, K));
 }
 
-hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
-                     hipStream_t s) {
+namespace {
+
+// The bands are sized for fp32 A whatever A's type, so that the scratch of the split-K partials
+// (gemm_partial_bytes) is the same for both.
+template <typename AT>
+hipError_t gemm_any(const AT* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
+                    hipStream_t s) {
   const int64_t band = band_rows(K);
   if (M > band) {
     for (int64_t m = 0; m < M; m += band) {
       const int rows = static_cast<int>(std::min<int64_t>(band, M - m));
-      hipError_t e = gemm_bf16(A + m * K, B, C + m * N, rows, N, K, part, s);
+      hipError_t e = gemm_any(A + m * K, B, C + m * N, rows, N, K, part, s);
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -251,7 +266,7 @@ hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, 
   const int S = split_count(M, N, K);
   const int per = (tiles * S + kXcds - 1) / kXcds;
   const int k_chunk = S > 1 ? ((K + S - 1) / S + BK - 1) / BK * BK : K;
-  hipLaunchKernelGGL(gemm_bf16_kernel, dim3(per * kXcds), dim3(THREADS), 0, s, A, B,
+  hipLaunchKernelGGL(gemm_bf16_kernel<AT>, dim3(per * kXcds), dim3(THREADS), 0, s, A, B,
                      S > 1 ? part : C, M, N, K, tn, per, tiles, tiles * S, k_chunk);
   if (S > 1) {
     const size_t n4 = static_cast<size_t>(M) * N / 4;     // N % 8 == 0
@@ -260,6 +275,18 @@ hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, 
                        reinterpret_cast<const f32x4*>(part), reinterpret_cast<f32x4*>(C), n4, S);
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
+                     hipStream_t s) {
+  return gemm_any(A, B, C, M, N, K, part, s);
+}
+
+hipError_t gemm_bf16(const uint16_t* A, const uint16_t* B, float* C, int M, int N, int K,
+                     float* part, hipStream_t s) {
+  return gemm_any(A, B, C, M, N, K, part, s);
 }
 
 size_t project_workspace_bytes(int T, int expand, int dv, int dv_virt, int d_out) {
@@ -271,9 +298,12 @@ size_t project_workspace_bytes(int T, int expand, int dv, int dv_virt, int d_out
   return tmp + std::max(p1, p2);
 }
 
-hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const float* pooled,
-                          const uint16_t* w_proj, const uint16_t* w_out, float* out, void* ws,
-                          hipStream_t s) {
+namespace {
+
+template <typename PT>
+hipError_t project_any(int T, int expand, int dv, int dv_virt, int d_out, const PT* pooled,
+                       const uint16_t* w_proj, const uint16_t* w_out, float* out, void* ws,
+                       hipStream_t s) {
   clear_stale_error();
   if (T == 0) return hipSuccess;
   char* base = static_cast<char*>(ws);
@@ -287,6 +317,20 @@ hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, con
   hipError_t e = gemm_bf16(pooled, w_proj, tmp, T, dv_virt, expand * dv, part, s);
   if (e != hipSuccess) return e;
   return gemm_bf16(tmp, w_out, out, T, d_out, dv_virt, part, s);
+}
+
+}  // namespace
+
+hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const float* pooled,
+                          const uint16_t* w_proj, const uint16_t* w_out, float* out, void* ws,
+                          hipStream_t s) {
+  return project_any(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws, s);
+}
+
+hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const uint16_t* pooled,
+                          const uint16_t* w_proj, const uint16_t* w_out, float* out, void* ws,
+                          hipStream_t s) {
+  return project_any(T, expand, dv, dv_virt, d_out, pooled, w_proj, w_out, out, ws, s);
 }
 
 }  // namespace umem

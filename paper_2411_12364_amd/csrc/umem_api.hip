@@ -63,6 +63,9 @@ umem_status check_desc(const umem_desc* d) {
                          !gemm_weight_supported(d->dv_virt, static_cast<int64_t>(d->expand) * d->dv) ||
                          !gemm_weight_supported(d->d_out, d->dv_virt)))
     return UMEM_ERR_UNSUPPORTED;
+  // the output linear alone reads the pooled rows (bf16) in 16-byte pieces of 8
+  if (d->dv_virt == 0 && d->d_out > 0 && (d->dv % 8 != 0 || !gemm_weight_supported(d->d_out, d->dv)))
+    return UMEM_ERR_UNSUPPORTED;
   return UMEM_OK;
 }
 
@@ -85,7 +88,7 @@ struct Layout {
   size_t factors, sel, idx, w, pooled, proj, total;
 };
 
-// Workspace: [rank-1 factors (Tucker)] [selection scores] [idx] [w] [pooled] [projection
+// Workspace: [rank-1 factors (Tucker)] [selection scores] [idx] [w] [pooled, bf16] [projection
 // scratch: the intermediate and split-K partials; before the projection, the scoring's bf16
 // planes of queries and keys, dead once the scores are written]
 Layout layout(const umem_desc* d, int32_t T) {
@@ -102,7 +105,7 @@ Layout layout(const umem_desc* d, int32_t T) {
   off += round_up(th * d->topm * n_cores(*d) * sizeof(float));
   L.pooled = off;
   if (d->dv_virt > 0 || d->d_out > 0)
-    off += round_up(static_cast<size_t>(T) * d->expand * d->dv * sizeof(float));
+    off += round_up(static_cast<size_t>(T) * d->expand * d->dv * sizeof(uint16_t));
   L.proj = off;
   const size_t proj = (d->dv_virt > 0 || d->d_out > 0)
                           ? project_workspace_bytes(T, d->expand, d->dv, d->dv_virt, d->d_out) : 0;
@@ -464,7 +467,8 @@ umem_status forward_into(const umem_desc* desc, int32_t T, const float* q_row, c
   float* sel = reinterpret_cast<float*>(base + L.sel);
   int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(base + L.idx);
   float* w = w_out_scores ? w_out_scores : reinterpret_cast<float*>(base + L.w);
-  float* pooled = project ? reinterpret_cast<float*>(base + L.pooled) : out;
+  // with a projection the pooled rows go to the workspace in bf16, as its GEMM takes them
+  uint16_t* pooled = reinterpret_cast<uint16_t*>(base + L.pooled);
   st = check_gather(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, desc->expand,
                     n_cores(*desc), out);
   if (st != UMEM_OK) return st;
@@ -483,12 +487,15 @@ umem_status forward_into(const umem_desc* desc, int32_t T, const float* q_row, c
   if (e == hipSuccess)
     e = launch_select(*desc, T, sel, q_row, q_col, k_row, k_col, core, idx, w, nullptr,
                       fused ? values : nullptr, fused ? out : nullptr, stream);
-  if (e == hipSuccess && !fused)
+  if (e == hipSuccess && !fused && !project)
     e = launch_gather(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, perm,
-                      desc->expand, n_cores(*desc), pooled, stream);
+                      desc->expand, n_cores(*desc), out, stream);
   if (e == hipSuccess && project)
-    e = run_project(T, desc->expand, desc->dv, desc->dv_virt, desc->d_out, pooled, w_proj, w_out,
-                    out, base + L.proj, stream);
+    e = launch_gather_bf16(desc->n_values, desc->dv, desc->vdtype, values, T, bag, idx, w, perm,
+                           desc->expand, n_cores(*desc), pooled, stream);
+  if (e == hipSuccess && project)
+    e = launch_project(T, desc->expand, desc->dv, desc->dv_virt, desc->d_out, pooled, w_proj,
+                       w_out, out, base + L.proj, stream);
   return hip_status(e);
 }
 

@@ -65,6 +65,11 @@ bool select_pools(const umem_desc& d);
 hipError_t launch_gather(int64_t n_values, int dv, int vdtype, const void* values, int T,
                          int bag, const int32_t* idx, const float* w, const int32_t* perm,
                          int expand, int cores, float* out, hipStream_t s);
+// The same with the pooled rows rounded to bf16 (nearest even) as they are stored, for the
+// projection, whose GEMM rounds its A operand the same way: out [T, expand, dv] bf16 bits.
+hipError_t launch_gather_bf16(int64_t n_values, int dv, int vdtype, const void* values, int T,
+                              int bag, const int32_t* idx, const float* w, const int32_t* perm,
+                              int expand, int cores, uint16_t* out, hipStream_t s);
 
 // Multi-core scoring: the number of component cores of a layer (0 counts as 1), and whether
 // rows of this shape can be split into h column slices (each slice whole 16-byte chunks).
@@ -82,6 +87,10 @@ inline bool gemm_weight_supported(int64_t N, int64_t K) {
 }
 hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, int K, float* part,
                      hipStream_t s);
+// The same with A already bf16 bits (16-byte aligned rows of K): the product is the one the fp32
+// form computes from the fp32 values that round to this A.
+hipError_t gemm_bf16(const uint16_t* A, const uint16_t* B, float* C, int M, int N, int K,
+                     float* part, hipStream_t s);
 
 // Stable sort of M (key, value) pairs with keys < 2^bits (sort.hip); the inputs are reordered
 // through ws (sort_workspace_bytes(M) bytes, 4-byte aligned) and the sorted arrays returned
@@ -120,6 +129,10 @@ hipError_t launch_key_norm(int heads, int n, int dk, const float* keys, const fl
 // split-K partials); w_proj == nullptr is the output linear alone ([T, dv] by [dv, d_out]).
 size_t project_workspace_bytes(int T, int expand, int dv, int dv_virt, int d_out);
 hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const float* pooled,
+                          const uint16_t* w_proj, const uint16_t* w_out, float* out, void* ws,
+                          hipStream_t s);
+// The same from pooled rows already rounded to bf16 (launch_gather_bf16): the same result.
+hipError_t launch_project(int T, int expand, int dv, int dv_virt, int d_out, const uint16_t* pooled,
                           const uint16_t* w_proj, const uint16_t* w_out, float* out, void* ws,
                           hipStream_t s);
 

@@ -229,5 +229,8 @@ def projections(cfg: Layer):
     if cfg.dv_virt == 0:
         return None, None
     wp = S.tensor_f32(cfg.seed, S.TID_W_PROJ, (cfg.expand, cfg.dv, cfg.dv_virt), 1.0 / math.sqrt(cfg.dv))
+    wp = S.f32_to_bf16_bits(wp).reshape(wp.shape)
+    if cfg.d_out == 0:       # the projectors alone
+        return wp, None
     wo = S.tensor_f32(cfg.seed, S.TID_W_OUT, (cfg.dv_virt, cfg.d_out), 1.0 / math.sqrt(cfg.dv_virt))
-    return S.f32_to_bf16_bits(wp).reshape(wp.shape), S.f32_to_bf16_bits(wo).reshape(wo.shape)
+    return wp, S.f32_to_bf16_bits(wo).reshape(wo.shape)

@@ -88,6 +88,8 @@ def test_workspace_size_layout():
     (dict(grid=1, rank=8), U.UMEM_ERR_UNSUPPORTED),
     (dict(dv=100), U.UMEM_ERR_UNSUPPORTED),                    # 200-byte rows
     (dict(d_out=100), U.UMEM_ERR_UNSUPPORTED),                 # weight rows of 16-byte pieces
+    (dict(dv=4, vdtype=0, d_out=64), U.UMEM_ERR_UNSUPPORTED),  # output linear alone: K = dv, 8 | K
+    (dict(dv=8, vdtype=0, d_out=64), U.UMEM_OK),
     (dict(expand=4, n_values=4480 * 1120, dv_virt=260), U.UMEM_ERR_UNSUPPORTED),
     (dict(heads=64, topm=64), U.UMEM_ERR_UNSUPPORTED),         # bag 4096
 ])

@@ -374,6 +374,50 @@ def test_project_banded_split_k_stays_in_workspace():
 
 # ---------------------------------------------------------------- the paper-scale workloads
 
+@pytest.mark.parametrize("kw", [
+    # expansion, both GEMMs, the projection's K split
+    dict(T=70, heads=2, dk=64, n_keys=96, topk=16, topm=24, dv=512, vdtype=CF.BF16, rank=2,
+         grid=CF.GRID_TUCKER, expand=4, dv_virt=64, d_out=128),
+    # the output linear alone, fp32 rows
+    dict(T=33, heads=1, dk=64, n_keys=64, topk=8, topm=8, dv=256, vdtype=CF.F32, d_out=96),
+    # a wave per token (2,100 tokens), the projectors alone
+    dict(T=2100, heads=1, dk=64, n_keys=64, topk=8, topm=8, dv=256, vdtype=CF.BF16, dv_virt=64),
+    # multi-core weights with expansion
+    dict(T=24, heads=2, dk=128, n_keys=128, rank=2, grid=CF.GRID_TUCKER, topk=16, topm=32,
+         dv=512, vdtype=CF.BF16, expand=4, dv_virt=256, d_out=192, cores=2),
+], ids=["ive-two-gemms", "output-linear", "wave-per-token", "multi-core"])
+def test_forward_projection_is_gather_then_project(kw):
+    """The forward hands its projection the pooled rows in bf16, rounded as the projection's GEMM
+    rounds an fp32 operand: its output equals umem_gather_sum (fp32 rows) followed by
+    umem_project, bit for bit."""
+    cfg = small("fwd-parts", **kw)
+    log(f"[case] forward = gather + project: {kw}")
+    dl = SD.make_layer(cfg)
+    T = cfg.T
+    w_proj, w_out = dl.w_proj, dl.w_out
+    if cfg.dv_virt == 0:    # the output linear alone: a weight [d_out, dv], output-major
+        rng = np.random.default_rng(5)
+        wo = S.f32_to_bf16_bits(rng.standard_normal((cfg.d_out, cfg.dv)) / np.sqrt(cfg.dv))
+        w_out = torch.from_numpy(wo.reshape(cfg.d_out, cfg.dv).view(np.int16)).cuda()
+    desc = G.desc_for(cfg)
+    out_f = torch.empty((T, cfg.d_out or cfg.dv_virt), dtype=torch.float32, device="cuda")
+    idx_f = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda")
+    w_f = torch.empty(G.weights_shape(cfg, T), dtype=torch.float32, device="cuda")
+    ws = G.workspace(desc, T)
+    U.check(U.umem_forward(desc, T, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core,
+                           dl.values, dl.perm, w_proj, w_out, out_f, idx_f, w_f, ws, ws.numel()),
+            "umem_forward")
+    pooled = G.gather(dl, idx_f, w_f, T)
+    st, nws = U.umem_project_workspace_size(T, cfg.expand, cfg.dv, cfg.dv_virt, cfg.d_out)
+    U.check(st)
+    ws_p = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
+    out_p = torch.empty_like(out_f)
+    U.check(U.umem_project(T, cfg.expand, cfg.dv, cfg.dv_virt, cfg.d_out, pooled, w_proj, w_out,
+                           out_p, ws_p, ws_p.numel()), "umem_project")
+    torch.cuda.synchronize()
+    assert torch.equal(out_f, out_p)
+
+
 def test_c2_prefill_sampled():
     rng = np.random.default_rng(2)
     run_and_check(CF.C2, tokens=np.sort(rng.choice(CF.C2.T, 256, replace=False)))
