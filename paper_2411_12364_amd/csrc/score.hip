@@ -319,19 +319,22 @@ __global__ __launch_bounds__(THREADS) void axis_scores_split(
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // Decode-sized T on v_mfma_f32_32x32x2f32: a workgroup covers 32 keys x 32 tokens of one (head,
-// axis) and its 4 waves split the dim into quarters of DW = dk / 4.  Lane l (token / key l % 32,
+// axis) and its 8 waves split the dim into eighths of DW = dk / 8.  Lane l (token / key l % 32,
 // half l / 32) holds dims d0 + (l / 32) * DW/2 .. + DW/2 - 1 of its token and of its key, so
-// MFMA i pairs dims d0 + i and d0 + DW/2 + i.  The four partial tiles meet in LDS; wave w adds
-// them (in wave order) for tokens 8w .. 8w + 7 and stores 128-byte runs of keys.
+// MFMA i pairs dims d0 + i and d0 + DW/2 + i.  The eight partial tiles meet in LDS; wave w adds
+// them (in wave order) for D registers 2w, 2w + 1 and stores 128-byte runs of keys.  Eight
+// waves rather than four (or sixteen) halve each wave's chain of dependent MFMAs and loads
+// (measured at decode-20M: 5.50 us with four, 5.19 with eight, 5.77 with sixteen).
+constexpr int kWideWaves = 8;
 template <int NV4>
-__global__ __launch_bounds__(THREADS) void axis_scores_wide(
+__global__ __launch_bounds__(kWideWaves * kWave) void axis_scores_wide(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
     const float* __restrict__ factors, float* __restrict__ sel, int T, int H, int n, int dk,
     int rank, float4* __restrict__ zero, int zero_n4) {
   clear_with_grid(zero, zero_n4);
   constexpr int HALF = 4 * NV4;                 // DW / 2 dims per lane
-  __shared__ float part[4][16][kWave];          // the four waves' D fragments
+  __shared__ float part[kWideWaves][16][kWave];   // the waves' D fragments
   const int axis = blockIdx.z & 1;
   const int h = blockIdx.z >> 1;
   const float* __restrict__ q = axis ? q_col : q_row;
@@ -359,7 +362,7 @@ __global__ __launch_bounds__(THREADS) void axis_scores_wide(
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qf[i].z, kf[i].z, acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qf[i].w, kf[i].w, acc, 0, 0, 0);
   }
-  // a wave's quarter of the dims lies in one slice (the launcher checks 4 % rank == 0): fold it
+  // a wave's eighth of the dims lies in one slice (the launcher checks 8 % rank == 0): fold it
   if (factors != nullptr) {
     const float f = factors[(h * 2 + axis) * kMaxRank + (wave * 2 * HALF) / (dk / rank)];
 #pragma unroll
@@ -370,10 +373,12 @@ __global__ __launch_bounds__(THREADS) void axis_scores_wide(
   __syncthreads();
   // D register j of lane l: token 8 (j / 4) + 4 (l / 32) + j % 4, key l % 32
 #pragma unroll
-  for (int jj = 0; jj < 4; ++jj) {
-    const int j = 4 * wave + jj;
-    const float o = ((part[0][j][lane] + part[1][j][lane]) + part[2][j][lane]) + part[3][j][lane];
-    const int t = blockIdx.y * 32 + 8 * wave + 4 * hh + jj;
+  for (int jj = 0; jj < 16 / kWideWaves; ++jj) {
+    const int j = (16 / kWideWaves) * wave + jj;
+    float o = part[0][j][lane];
+#pragma unroll
+    for (int v = 1; v < kWideWaves; ++v) o += part[v][j][lane];
+    const int t = blockIdx.y * 32 + 8 * (j / 4) + 4 * hh + j % 4;
     // nontemporal: the selection reads the scores from other XCDs, so this XCD's L2 has no use
     // for them (measured: decode-20M step 16.53 -> 16.29 us)
     if (t < T && key < n)
@@ -670,14 +675,15 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
 #undef UMEM_SPLIT
     return hipGetLastError();
   }
-  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && T > 16 && T <= 64 && 4 % d.rank == 0) {
+  if ((d.dk == 64 || d.dk == 128 || d.dk == 256) && T > 16 && T <= 64 && kWideWaves % d.rank == 0) {
     dim3 grid((d.n_keys + 31) / 32, (T + 31) / 32, d.heads * 2);
 #define UMEM_WIDE(NV4)                                                                            \
-  hipLaunchKernelGGL((axis_scores_wide<NV4>), grid, dim3(THREADS), 0, s, q_row, q_col, k_row,     \
-                     k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank, zero, zero_n4)
-    if (d.dk == 64) UMEM_WIDE(2);
-    else if (d.dk == 128) UMEM_WIDE(4);
-    else UMEM_WIDE(8);
+  hipLaunchKernelGGL((axis_scores_wide<NV4>), grid, dim3(kWideWaves * kWave), 0, s, q_row,       \
+                     q_col, k_row, k_col, c, sel, T, d.heads, d.n_keys, d.dk, d.rank, zero,     \
+                     zero_n4)
+    if (d.dk == 64) UMEM_WIDE(1);
+    else if (d.dk == 128) UMEM_WIDE(2);
+    else UMEM_WIDE(4);
 #undef UMEM_WIDE
     return hipGetLastError();
   }
