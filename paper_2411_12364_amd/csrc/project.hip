@@ -289,6 +289,22 @@ hipError_t gemm_bf16(const uint16_t* A, const uint16_t* B, float* C, int M, int 
   return gemm_any(A, B, C, M, N, K, part, s);
 }
 
+hipError_t gemm_bf16_parts(const uint16_t* A, const uint16_t* B, float* C, int M, int N, int K,
+                           float* part, hipStream_t s, int* splits) {
+  const int S = split_count(M, N, K);
+  if (M > band_rows(K) || S == 1) {
+    *splits = 1;
+    return gemm_any(A, B, C, M, N, K, part, s);
+  }
+  *splits = S;
+  const int tiles = n_tiles(M, N);
+  const int per = (tiles * S + kXcds - 1) / kXcds;
+  const int k_chunk = ((K + S - 1) / S + BK - 1) / BK * BK;
+  hipLaunchKernelGGL(gemm_bf16_kernel<uint16_t>, dim3(per * kXcds), dim3(THREADS), 0, s, A, B, part,
+                     M, N, K, (N + BN - 1) / BN, per, tiles, tiles * S, k_chunk);
+  return hipGetLastError();
+}
+
 size_t project_workspace_bytes(int T, int expand, int dv, int dv_virt, int d_out) {
   if (T == 0) return 0;
   if (dv_virt == 0) return gemm_partial_bytes(T, d_out, dv);          // the output linear alone

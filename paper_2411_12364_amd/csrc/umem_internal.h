@@ -91,6 +91,11 @@ hipError_t gemm_bf16(const float* A, const uint16_t* B, float* C, int M, int N, 
 // form computes from the fp32 values that round to this A.
 hipError_t gemm_bf16(const uint16_t* A, const uint16_t* B, float* C, int M, int N, int K,
                      float* part, hipStream_t s);
+// The same, but a GEMM split over K (in one band of rows) leaves its *splits partial products in
+// part ([*splits][M][N], to be added in split order) instead of adding them into C; *splits = 1
+// means C holds the product.
+hipError_t gemm_bf16_parts(const uint16_t* A, const uint16_t* B, float* C, int M, int N, int K,
+                           float* part, hipStream_t s, int* splits);
 
 // Stable sort of M (key, value) pairs with keys < 2^bits (sort.hip); the inputs are reordered
 // through ws (sort_workspace_bytes(M) bytes, 4-byte aligned) and the sorted arrays returned
