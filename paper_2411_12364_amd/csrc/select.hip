@@ -280,7 +280,7 @@ __device__ __forceinline__ void additive_tables(int k, int m, SelectShared& sh) 
       const int c = (m + a) / (a + 1);                   // ceil(m / r), r = a + 1
       sh.th_col[a + 1] = static_cast<uint8_t>(c <= k ? c : 0);
     }
-    carry += __shfl(first + len, kWave - 1, kWave);
+    carry = __shfl(first + len, kWave - 1, kWave);   // first already counts the earlier rows
   }
   if (lane == 0) sh.grid_total = carry;
 }

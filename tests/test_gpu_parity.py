@@ -126,6 +126,25 @@ def test_edge_shapes(kw):
     run_and_check(small("edge", **kw))
 
 
+# The library's own limits (`umem_internal.h`), each at its maximum in one case: n = 8192 keys per
+# axis, k = 90 and m = 256 (additive); Dk = 1024 with the Tucker rank 4 (the query rows fill
+# the 512 threads); a bag of 2048 rows of 8 KiB; the Tucker k = 64 with E = 64 and h = 8 cores.
+# With k > 64 the additive grid's candidate table is built in two passes of a wave; the k = 70
+# case runs that over 16 (token, head) pairs.
+@pytest.mark.parametrize("kw", [
+    dict(T=3, heads=1, dk=64, n_keys=8192, topk=90, topm=256, dv=8, vdtype=CF.BF16),
+    dict(T=8, heads=2, dk=64, n_keys=2048, topk=70, topm=256, dv=8, vdtype=CF.BF16),
+    dict(T=5, heads=2, dk=1024, n_keys=300, rank=4, grid=CF.GRID_TUCKER, topk=16, topm=64,
+         dv=256, vdtype=CF.F32),
+    dict(T=4, heads=8, dk=64, n_keys=256, topk=32, topm=256, dv=4096, vdtype=CF.BF16),
+    dict(T=5, heads=2, dk=256, n_keys=512, rank=4, grid=CF.GRID_TUCKER, topk=64, topm=256, dv=64,
+         vdtype=CF.BF16, expand=64, dv_virt=64, cores=8),
+], ids=["n-8192-k-90-m-256", "k-70-m-256", "dk-1024-rank-4", "bag-2048-rows-8KiB",
+        "tucker-k-64-E-64-h-8"])
+def test_library_limits(kw):
+    run_and_check(small("limit", **kw))
+
+
 # The Tucker grid's exact per-slice scores (eq. (4)) split each key row over G = 16, 8 or 4 lanes
 # (by 2k) and those over the slices (G, G/2 or G/4 lanes per slice for rank 1, 2, 3-4); these
 # cases take every split, the idle lanes of rank 3, a slice of 7 pieces over 2 lanes, and rows
