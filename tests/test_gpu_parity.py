@@ -139,10 +139,18 @@ def test_edge_shapes(kw):
     dict(T=4, heads=8, dk=64, n_keys=256, topk=32, topm=256, dv=4096, vdtype=CF.BF16),
     dict(T=5, heads=2, dk=256, n_keys=512, rank=4, grid=CF.GRID_TUCKER, topk=64, topm=256, dv=64,
          vdtype=CF.BF16, expand=64, dv_virt=64, cores=8),
+    # 64 heads (one factor pair each), the Tucker grid
+    dict(T=3, heads=64, dk=64, n_keys=128, rank=2, grid=CF.GRID_TUCKER, topk=16, topm=32, dv=64,
+         vdtype=CF.BF16),
+    # the selection pooling the rows itself at its limits: 512 tokens, m = 64, rows of 2 KiB
+    dict(T=512, heads=2, dk=128, n_keys=256, topk=32, topm=64, dv=1024, vdtype=CF.BF16),
+    # n not a multiple of 4 at the largest per-thread share: 32 keys per thread and axis
+    dict(T=2, heads=1, dk=64, n_keys=8191, topk=32, topm=32, dv=8, vdtype=CF.BF16),
 ], ids=["n-8192-k-90-m-256", "k-70-m-256", "dk-1024-rank-4", "bag-2048-rows-8KiB",
-        "tucker-k-64-E-64-h-8"])
+        "tucker-k-64-E-64-h-8", "heads-64", "pooled-T-512-m-64-2KiB", "n-8191"])
 def test_library_limits(kw):
-    run_and_check(small("limit", **kw))
+    cfg = small("limit", **kw)
+    run_and_check(cfg, tokens=None if cfg.T <= 64 else np.arange(0, cfg.T, 7))
 
 
 # The Tucker grid's exact per-slice scores (eq. (4)) split each key row over G = 16, 8 or 4 lanes
