@@ -56,6 +56,8 @@ def run_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expa
     # d_pooled beyond one XCD's L2 (4 MB)
     (256, CF.F32, 1, 16, 4200, 1, 500),
     (512, CF.BF16, 4, 32, 600, 2, 300),       # IVE blocks, two cores
+    # the library's limits: a bag of 2048, E = 64, eight cores
+    (64, CF.BF16, 64, 2048, 5, 8, 4096),
 ])
 def test_gather_backward(dv, vdtype, expand, bag, T, cores, Np):
     rng = np.random.default_rng(dv + bag + T + cores)
@@ -162,6 +164,11 @@ SCORE_CASES = [
              seed=60, rank=1, grid=CF.GRID_TUCKER),
     CF.Layer("tucker-r3", T=11, heads=1, dk=84, n_keys=70, topk=14, topm=40, dv=8, vdtype=CF.F32,
              seed=61, rank=3, grid=CF.GRID_TUCKER),
+    # the library's limits: n = 8192, Dk = 1024, k = 90, m = 256; 64 heads
+    CF.Layer("add-limits", T=3, heads=1, dk=1024, n_keys=8192, topk=90, topm=256, dv=8,
+             vdtype=CF.F32, seed=62),
+    CF.Layer("tucker-h64", T=3, heads=64, dk=64, n_keys=128, topk=16, topm=32, dv=8, vdtype=CF.F32,
+             seed=63, rank=2, grid=CF.GRID_TUCKER),
 ]
 
 
