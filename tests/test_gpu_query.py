@@ -79,6 +79,9 @@ CASES = [
     CF.FE6,
     CF.FrontEnd("prefill-chunk", B=2, L=300, d_model=1024, conv_k=4, heads=2, dk=128, shared=False,
                 seed=24),
+    # the limits: eight taps, Dk = 1024 (16 values per lane in the LayerNorm, which then adds
+    # the query linear's 8 split partials in two batches)
+    CF.FrontEnd("limits", B=3, L=9, d_model=2048, conv_k=8, heads=2, dk=1024, shared=False, seed=25),
 ]
 
 
