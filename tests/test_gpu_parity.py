@@ -315,6 +315,8 @@ def test_select_pools_like_gather(kw):
     # thousands of tokens: a wave per token (ragged last workgroup, sub-rows, long rows)
     (512, CF.BF16, 1, 64, 4099, 1), (64, CF.BF16, 1, 33, 4100, 1), (2048, CF.BF16, 1, 20, 4096, 1),
     (256, CF.F32, 1, 7, 5001, 1),
+    # ... with rows of 16 and 32 bytes: 64 and 32 rows at once per wave
+    (8, CF.BF16, 1, 70, 2100, 1), (16, CF.BF16, 1, 33, 2050, 1),
     # multi-core weights (eq. (17)): column slices, with IVE, sub-rows, many tokens
     (512, CF.BF16, 1, 64, 37, 2), (1024, CF.BF16, 4, 100, 37, 4), (64, CF.BF16, 1, 33, 70, 4),
     (256, CF.F32, 1, 33, 4099, 2), (3072, CF.BF16, 1, 20, 9, 8),
