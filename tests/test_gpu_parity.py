@@ -194,18 +194,23 @@ def test_exact_ties_lower_index(kw):
 # ---------------------------------------------------------------- a1 + a2 alone, every kernel
 
 @pytest.mark.parametrize("kw", [
-    dict(T=40, heads=2, dk=128, n_keys=200),                                  # split, 2 tiles
-    dict(T=40, heads=2, dk=128, n_keys=200, rank=2, grid=CF.GRID_TUCKER),     # split + fold
+    # 16 < T <= 64: 32 x 32 tiles, eight waves splitting Dk (Dk / 64 loads per lane and operand)
+    dict(T=40, heads=2, dk=128, n_keys=200),                                  # wide, 2 token tiles
+    dict(T=40, heads=2, dk=128, n_keys=200, rank=2, grid=CF.GRID_TUCKER),     # wide + fold
+    dict(T=64, heads=1, dk=256, n_keys=33),                                   # wide, dk = 256
+    dict(T=33, heads=2, dk=64, n_keys=100),                                   # wide, dk = 64
+    dict(T=50, heads=1, dk=128, n_keys=96, rank=4, grid=CF.GRID_TUCKER),      # wide + rank-4 fold
+    # T <= 16: 16 x 16 tiles, four waves splitting Dk
     dict(T=9, heads=1, dk=64, n_keys=70, rank=4, grid=CF.GRID_TUCKER),        # split, 1 chunk
-    dict(T=64, heads=1, dk=256, n_keys=33),                                   # split, 4 chunks
+    dict(T=12, heads=2, dk=128, n_keys=150, rank=2, grid=CF.GRID_TUCKER),     # split, 2 chunks
     dict(T=100, heads=1, dk=256, n_keys=130, rank=2, grid=CF.GRID_TUCKER),    # tiled MFMA
     dict(T=70, heads=3, dk=64, n_keys=200),                                   # tiled MFMA
     dict(T=5, heads=2, dk=12, n_keys=33, rank=3, grid=CF.GRID_TUCKER),        # vector ALU
     # many tokens on bf16 planes: ragged token and key tiles, three dk steps; dk = 448
     dict(T=200, heads=3, dk=96, n_keys=300, rank=2, grid=CF.GRID_TUCKER),
     dict(T=130, heads=1, dk=448, n_keys=260),
-], ids=["split", "split-tucker2", "split-tucker4", "split-dk256", "tiled-tucker2", "tiled",
-        "valu-tucker3", "planes-tucker2", "planes-dk448"])
+], ids=["wide", "wide-tucker2", "wide-dk256", "wide-dk64", "wide-tucker4", "split-tucker4",
+        "split-tucker2", "tiled-tucker2", "tiled", "valu-tucker3", "planes-tucker2", "planes-dk448"])
 def test_axis_scores_kernels(kw):
     cfg = small("scores", topk=4, topm=4, **kw)
     log(f"[case] axis scores {kw}")
