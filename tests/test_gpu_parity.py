@@ -281,7 +281,11 @@ def test_c5_tucker_ive_mcs_sampled():
          weight=CF.W_SOFTMAX),
     dict(T=9, heads=2, dk=128, n_keys=90, rank=2, grid=CF.GRID_TUCKER, topk=10, topm=20, dv=512,
          vdtype=CF.BF16),
-], ids=["f32-1KiB", "bf16-2KiB-m40", "softmax-m64", "tucker"])
+    dict(T=20, heads=2, dk=64, n_keys=128, topk=16, topm=32, dv=512, vdtype=CF.F32),
+    # multi-core weights on 2 KiB rows: each lane's two chunks take their own slices' weights
+    dict(T=24, heads=2, dk=128, n_keys=128, rank=2, grid=CF.GRID_TUCKER, topk=16, topm=48,
+         dv=1024, vdtype=CF.BF16, cores=4),
+], ids=["f32-1KiB", "bf16-2KiB-m40", "softmax-m64", "tucker", "f32-2KiB", "mcs4-2KiB"])
 def test_select_pools_like_gather(kw):
     """umem_select with values/pooled: the same idx and w as without, and pooled rows that match
     the oracle's gather of them."""
@@ -297,7 +301,7 @@ def test_select_pools_like_gather(kw):
     outs = []
     for pool in (False, True):
         idx = torch.empty((T, H, m), dtype=torch.int32, device="cuda")
-        w = torch.empty((T, H, m), dtype=torch.float32, device="cuda")
+        w = torch.empty(G.weights_shape(cfg, T), dtype=torch.float32, device="cuda")
         pooled = torch.zeros((T, cfg.dv), dtype=torch.float32, device="cuda")
         U.check(U.umem_select(desc, T, sel, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core,
                               idx, w, None, dl.values if pool else None, pooled if pool else None),
