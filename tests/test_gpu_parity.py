@@ -519,6 +519,33 @@ def test_deterministic(heads):
         assert torch.equal(x, y)
 
 
+def test_two_streams_concurrently():
+    """Forwards of two layers (one pooling inside the selection, one with expansion and the
+    projection) issued alternately on two streams, each with its own workspace, give the results
+    each gives alone: every launch goes to the caller's stream and the library holds no state
+    between calls."""
+    cfgs = [small("s1", T=40, heads=2, n_keys=200, topk=16, topm=24, dv=512, vdtype=CF.BF16),
+            small("s2", T=130, heads=2, dk=64, n_keys=96, topk=16, topm=24, dv=512, vdtype=CF.BF16,
+                  rank=2, grid=CF.GRID_TUCKER, expand=4, dv_virt=64, d_out=128)]
+    dls = [SD.make_layer(c, batches=2) for c in cfgs]
+    want = []
+    for dl, c in zip(dls, cfgs):
+        want.append([G.forward(dl, c.T, b) for b in range(2)])
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    got = [[None, None], [None, None]]
+    for rep in range(3):
+        for b in range(2):
+            for i, (dl, c) in enumerate(zip(dls, cfgs)):
+                with torch.cuda.stream(streams[i]):
+                    got[i][b] = G.forward(dl, c.T, b)
+        torch.cuda.synchronize()
+        for i in range(2):
+            for b in range(2):
+                for x, y in zip(got[i][b], want[i][b]):
+                    assert torch.equal(x, y), (rep, i, b)
+
+
 def test_hip_graph_replay_matches_eager():
     """Forwards captured in a HIP graph, replayed several times with eager work in between, give
     the eager results bit for bit."""
