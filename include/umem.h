@@ -108,10 +108,11 @@ UMEM_API umem_status umem_workspace_size(const umem_desc* desc, int32_t T, size_
  *                                  cores with multi-core scoring (their sum is the core)
  *   sel           fp32 [2, T, H, n] out: [0] row scores, [1] column scores
  *   ws            256-byte aligned scratch: the singular vectors (Tucker grid, 2 KiB), then for
- *                 T > 64 tokens the bf16 planes of the many-token kernel (2 * 3 * (T + n_keys) *
- *                 heads * dk * 2 bytes where dk % 32 == 0, (dk / rank) % 8 == 0 and n_keys % 4 ==
- *                 0); a workspace sized
- *                 by umem_workspace_size suffices; may be NULL where neither is needed */
+ *                 T > 64 tokens the fp16 planes of the many-token kernel and their rows'
+ *                 exponents (2 * 2 * (T + n_keys) * heads * dk * 2 + 2 * (T + n_keys) * heads * 4
+ *                 bytes where dk % 32 == 0, (dk / rank) % 8 == 0 and n_keys % 4 == 0); a
+ *                 workspace sized by umem_workspace_size suffices; may be NULL where neither is
+ *                 needed */
 UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const float* q_row,
                                       const float* q_col, const float* k_row, const float* k_col,
                                       const float* core, float* sel, void* ws, size_t ws_bytes,
@@ -210,7 +211,7 @@ UMEM_API umem_status umem_forward(const umem_desc* desc, int32_t T, const float*
  * of the caller.  Neither this call nor the kernels it enqueues allocate or free memory.
  *   Arguments as for umem_forward, without ws and ws_bytes.
  *   UMEM_ERR_SCRATCH_LIMIT (nothing enqueued) when umem_workspace_size(desc, T) exceeds
- *   UMEM_STATIC_SCRATCH_BYTES (the 20.07M-slot decode layer fits up to 708 tokens).
+ *   UMEM_STATIC_SCRATCH_BYTES (the 20.07M-slot decode layer fits up to 779 tokens).
  *   The array of a GPU is created with the library's code on that GPU and held until the process
  *   ends; the first call on a device looks up its address (UMEM_ERR_HIP if that fails).  `stream`
  *   must belong to the calling thread's current device.  Every call on one GPU uses the same

@@ -386,45 +386,72 @@ __global__ __launch_bounds__(kWideWaves * kWave) void axis_scores_wide(
   }
 }
 
-// ---------------------------------------------------------------- scores on bf16 matrix cores
+// ---------------------------------------------------------------- scores on fp16 matrix cores
 // For many tokens the scores are one GEMM per (head, axis): with the slice factors folded into
 // the query (sum_rho f_rho sum_{d in rho} q_d K_d = sum_d (f_rho(d) q_d) K_d), S = Q' K^T with
-// both operands rows of dk.  fp32 MFMA runs at 1/16 of the bf16 rate, so the GEMM is done on
-// bf16 MFMA in fp32 precision: each fp32 x is split exactly into three bf16 parts x = x1 + x2 + x3
-// (x1 = bf16(x), x2 = bf16(x - x1), x3 = x - x1 - x2; each part holds the next 8 bits of the
-// significand), and q . k = sum of the six products q_i k_j with i + j <= 4 (the three dropped
-// ones are below 2^-24 of the leading term).  Each product of two bf16 is exact in fp32 and the
-// MFMA accumulates in fp32, so the scores carry fp32-level rounding, at 6/16 of the fp32 MFMA
-// time.
+// both operands rows of dk.  fp32 MFMA runs at 1/16 of the fp16 rate, so the GEMM is done on
+// fp16 MFMA in fp32 precision.  Each row is first scaled by a power of two 2^s (exact) that puts
+// its largest magnitude in [2^14, 2^15), which keeps every part below fp16's largest value and
+// its small parts clear of fp16's subnormals; then each scaled x is split into two fp16 parts,
+// x1 = fp16(x) (11 significant bits) and x2 = fp16(x - x1) (x - x1 is exact; x2 keeps its next
+// 11 bits, so x - x1 - x2 is below 2^-22 |x|).  q . k = 2^-(s_q + s_k) (q1 k1 + q1 k2 + q2 k1):
+// each product of two fp16 is exact in fp32, the MFMA accumulates in fp32, and the dropped
+// product q2 k2 and the split's remainders are of order 2^-22 of the terms, below the fp32
+// rounding of a plain fp32 product sum (measured on the workloads' inputs: 4e-8 to 1.1e-7 of
+// sum |q_d k_d| against 2e-7 to 3.3e-7 for plain fp32).  The three products cost 3/16 of the
+// fp32 MFMA time.
 //
-// split_planes_kernel writes the three planes of Q' and K in the workspace, per (axis, plane,
-// head) a [rows, dk] block; axis_scores_x6 is a 128 x 128 tile of (tokens x keys) per
-// workgroup, four waves of 64 x 64 (4 x 4 v_mfma_f32_16x16x32_bf16 tiles x 6 products), dk in
-// steps of 32 through LDS with the next slice prefetched into registers, and the scores leave
-// through LDS as whole 128-byte lines (nontemporal).
+// split_planes_kernel writes the two planes of Q' and K and every row's exponent s in the
+// workspace, per (axis, plane, head) a [rows, dk] block; axis_scores_planes is a 128 x 128 tile
+// of (tokens x keys) per workgroup, four waves of 64 x 64 (4 x 4 v_mfma_f32_16x16x32_f16 tiles
+// x 3 products), dk in steps of 32 through LDS with the next slice prefetched into registers,
+// and the scores leave through LDS as whole 128-byte lines (nontemporal), each multiplied by its
+// 2^-(s_q + s_k) on the way out.
 constexpr int XT = 128, XN = 128, XK = 32;
-constexpr int XLD = XK;                       // LDS pitch in bf16 (64-byte rows, chunks swizzled)
+constexpr int XLD = XK;                       // LDS pitch in fp16 (64-byte rows, chunks swizzled)
 constexpr int XLDC = 64 + 4;                  // LDS pitch of the epilogue's fp32 rows
+constexpr int XPL = 2;                        // fp16 planes per operand
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Queries (both axes, scaled by their slice factors) then keys, eight dims per thread (two
-// 16-byte loads, one 16-byte store per plane).  Planes: Qp[axis][p][h][t][dk] (T rows per head),
-// Kp[axis][p][h][i][dk].
+// The workspace blocks of the planes: Qp[axis][p][h][t][dk], Kp[axis][p][h][i][dk] (fp16 bits),
+// then the rows' exponents Qs[axis][h][t], Ks[axis][h][i].
+struct PlaneLayout {
+  uint16_t* Qp;
+  uint16_t* Kp;
+  int32_t* Qs;
+  int32_t* Ks;
+};
+__host__ __device__ inline size_t plane_elems(int T, int H, int n, int dk) {
+  return static_cast<size_t>(2) * XPL * (static_cast<size_t>(T) + n) * H * dk;
+}
+PlaneLayout plane_layout(void* planes, int T, int H, int n, int dk) {
+  PlaneLayout L;
+  L.Qp = static_cast<uint16_t*>(planes);
+  L.Kp = L.Qp + static_cast<size_t>(2) * XPL * T * H * dk;
+  L.Qs = reinterpret_cast<int32_t*>(L.Qp + plane_elems(T, H, n, dk));
+  L.Ks = L.Qs + static_cast<size_t>(2) * H * T;
+  return L;
+}
+
+// One row per group of G lanes (G = 4 .. 64, a power of two, G >= dk / 8 unless dk > 512):
+// queries (both axes, scaled by their slice factors) first, then keys.  A lane holds 8 dims per
+// chunk, chunks c = lane + G j; the group's largest magnitude sets the row's exponent.
+template <int G>
 __global__ __launch_bounds__(THREADS) void split_planes_kernel(
     const float* __restrict__ q_row, const float* __restrict__ q_col,
     const float* __restrict__ k_row, const float* __restrict__ k_col,
-    const float* __restrict__ factors, int T, int H, int n, int dk, int width,
-    uint16_t* __restrict__ Qp, uint16_t* __restrict__ Kp) {
+    const float* __restrict__ factors, int T, int H, int n, int dk, int width, PlaneLayout L) {
+  constexpr int kMaxChunks = 2;                    // dk <= 1024: at most 128 chunks of 8 over 64 lanes
   const int d8n = dk / 8;
-  const size_t nq = static_cast<size_t>(2) * T * H * d8n, nk = static_cast<size_t>(2) * H * n * d8n;
-  for (size_t x = static_cast<size_t>(blockIdx.x) * THREADS + threadIdx.x; x < nq + nk;
-       x += static_cast<size_t>(gridDim.x) * THREADS) {
-    const bool query = x < nq;
-    const size_t y = query ? x : x - nq;
-    const int d8 = static_cast<int>(y % d8n);
-    const size_t r = y / d8n;                          // (axis, t, h) or (axis, h, i)
+  const int lg = threadIdx.x & (G - 1);
+  const size_t nq = static_cast<size_t>(2) * T * H, rows_all = nq + static_cast<size_t>(2) * H * n;
+  const size_t groups = static_cast<size_t>(gridDim.x) * (THREADS / G);
+  for (size_t r = static_cast<size_t>(blockIdx.x) * (THREADS / G) + threadIdx.x / G; r < rows_all;
+       r += groups) {
+    // (the loop bound is uniform over a group: its G lanes take the same rows)
+    const bool query = r < nq;
     int axis, h;
     size_t src_row, dst_row, rows;
     if (query) {
@@ -436,63 +463,81 @@ __global__ __launch_bounds__(THREADS) void split_planes_kernel(
       dst_row = static_cast<size_t>(h) * T + t;
       rows = static_cast<size_t>(H) * T;
     } else {
-      axis = static_cast<int>(r / (static_cast<size_t>(H) * n));
-      src_row = r % (static_cast<size_t>(H) * n);
+      const size_t y = r - nq;
+      axis = static_cast<int>(y / (static_cast<size_t>(H) * n));
+      src_row = y % (static_cast<size_t>(H) * n);
       h = static_cast<int>(src_row / n);
       dst_row = src_row;
       rows = static_cast<size_t>(H) * n;
     }
-    const float* src = (query ? (axis ? q_col : q_row) : (axis ? k_col : k_row)) + src_row * dk + 8 * d8;
-    const float4 v0 = *reinterpret_cast<const float4*>(src);
-    const float4 v1 = *reinterpret_cast<const float4*>(src + 4);
-    float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-    if (query && factors != nullptr) {
-      const float f = factors[(h * 2 + axis) * kMaxRank + (8 * d8) / width];   // width % 8 == 0
+    const float* src = (query ? (axis ? q_col : q_row) : (axis ? k_col : k_row)) + src_row * dk;
+    float v[kMaxChunks][8];
+    float mx = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] *= f;
+    for (int j = 0; j < kMaxChunks; ++j) {
+      const int c = lg + G * j;
+      if (c < d8n) {
+        const float4 v0 = *reinterpret_cast<const float4*>(src + 8 * c);
+        const float4 v1 = *reinterpret_cast<const float4*>(src + 8 * c + 4);
+        float f = 1.0f;
+        if (query && factors != nullptr) f = factors[(h * 2 + axis) * kMaxRank + (8 * c) / width];
+        v[j][0] = v0.x * f; v[j][1] = v0.y * f; v[j][2] = v0.z * f; v[j][3] = v0.w * f;
+        v[j][4] = v1.x * f; v[j][5] = v1.y * f; v[j][6] = v1.z * f; v[j][7] = v1.w * f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(v[j][e]));
+      }
     }
-    bf16x8 p[3];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const __bf16 a = static_cast<__bf16>(v[e]);
-      const float r1 = v[e] - static_cast<float>(a);            // exact
-      const __bf16 b = static_cast<__bf16>(r1);
-      p[0][e] = a;
-      p[1][e] = b;
-      p[2][e] = static_cast<__bf16>(r1 - static_cast<float>(b));   // exact: at most 8 bits left
+    for (int off = 1; off < G; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+    // mx in [2^(k-1), 2^k) (frexp's exponent k): 2^(15 - k) puts it in [2^14, 2^15)
+    const int sc = mx > 0.0f ? 15 - __builtin_amdgcn_frexp_expf(mx) : 0;
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j) {
+      const int c = lg + G * j;
+      if (c < d8n) {
+        f16x8 p[XPL];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = ldexpf(v[j][e], sc);                       // exact
+          const _Float16 a = static_cast<_Float16>(x);
+          p[0][e] = a;
+          p[1][e] = static_cast<_Float16>(x - static_cast<float>(a));   // x - a is exact
+        }
+        uint16_t* dst = query ? L.Qp : L.Kp;
+#pragma unroll
+        for (int pl = 0; pl < XPL; ++pl)
+          *reinterpret_cast<f16x8*>(dst + ((static_cast<size_t>(axis) * XPL + pl) * rows + dst_row) * dk + 8 * c) = p[pl];
+      }
     }
-    uint16_t* dst = query ? Qp : Kp;
-#pragma unroll
-    for (int pl = 0; pl < 3; ++pl)
-      *reinterpret_cast<bf16x8*>(dst + ((static_cast<size_t>(axis) * 3 + pl) * rows + dst_row) * dk + 8 * d8) = p[pl];
+    if (lg == 0) (query ? L.Qs : L.Ks)[static_cast<size_t>(axis) * rows + dst_row] = sc;
   }
 }
 
-// One 16-byte piece per thread and plane-row chunk: piece f of 3 * 128 * 4 (plane f / 512, row
-// (f % 512) / 4, dims 8 (f % 4) ..), six per thread per operand.
+// One 16-byte piece per thread and plane-row chunk: piece f of 2 * 128 * 4 (plane f / 512, row
+// (f % 512) / 4, dims 8 (f % 4) ..), four per thread per operand.
 struct XSlice {
-  u32x4 a[6], b[6];
+  u32x4 a[2 * XPL], b[2 * XPL];
 };
 
 // Where 16-byte chunk ch of tile row `row` sits in LDS: the chunk index is XORed with row bits
 // 1..3, so that the eight (or sixteen) lanes an LDS cycle serves, rows r..r+7 of one chunk when
 // fragments are read and rows r, r+1 (r..r+3) of all four chunks when tiles are staged, fall on
 // distinct banks with 32 (or 64) banks of 4 bytes.
-__device__ __forceinline__ int x6_pos(int row, int ch) {
+__device__ __forceinline__ int x_pos(int row, int ch) {
   return row * XLD + 8 * (ch ^ (((row >> 1) ^ (row >> 3)) & 3));
 }
 
-// The tile's next K-slice (32 dims) of the three planes of Q' (tokens t0..) and K (keys i0..) into
+// The tile's next K-slice (32 dims) of the two planes of Q' (tokens t0..) and K (keys i0..) into
 // registers.  Buffer loads over one (axis, plane, head) block each: rows past T (or n) fall
 // outside the block's range and read as zeros, and the addresses are 32-bit lane offsets on
 // scalar bases (no 64-bit address per load to keep live).
-__device__ __forceinline__ void x6_fetch(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Kb,
-                                         size_t qplane, size_t kplane, int T, int n, int dk,
-                                         int t0, int i0, int k0, int tid, XSlice& sl) {
-  static_assert(THREADS == 256, "a thread's six pieces: planes j / 2, rows tid / 4 + 64 (j % 2)");
+__device__ __forceinline__ void x_fetch(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Kb,
+                                        size_t qplane, size_t kplane, int T, int n, int dk,
+                                        int t0, int i0, int k0, int tid, XSlice& sl) {
+  static_assert(THREADS == 256, "a thread's pieces: planes j / 2, rows tid / 4 + 64 (j % 2)");
   const uint32_t qbytes = static_cast<uint32_t>(T) * dk * 2u, kbytes = static_cast<uint32_t>(n) * dk * 2u;
 #pragma unroll
-  for (int j = 0; j < 6; ++j) {
+  for (int j = 0; j < 2 * XPL; ++j) {
     const int pl = j >> 1, row = (tid >> 2) + 64 * (j & 1), col = k0 + 8 * (tid & 3);
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(Qa + pl * qplane), static_cast<short>(0), static_cast<int>(qbytes), 0x00020000);
@@ -503,13 +548,16 @@ __device__ __forceinline__ void x6_fetch(const uint16_t* __restrict__ Qa, const 
   }
 }
 
-__global__ __launch_bounds__(THREADS) void axis_scores_x6(
-    const uint16_t* __restrict__ Qp, const uint16_t* __restrict__ Kp, float* __restrict__ sel,
-    int T, int H, int n, int dk, float4* __restrict__ zero, int zero_n4) {
+__global__ __launch_bounds__(THREADS) void axis_scores_planes(
+    PlaneLayout L, float* __restrict__ sel, int T, int H, int n, int dk, float4* __restrict__ zero,
+    int zero_n4) {
   clear_with_grid(zero, zero_n4);
-  __shared__ __align__(16) uint16_t smem[2 * 3 * XT * XLD];   // [A | B][plane][row][k]
+  // [A | B][plane][row][k] during the K-steps, the waves' fp32 output rows in the epilogue
+  constexpr int kTileElems = 2 * XPL * XT * XLD, kOutElems = 4 * 32 * XLDC * 2;
+  __shared__ __align__(16) uint16_t smem[kTileElems > kOutElems ? kTileElems : kOutElems];
+  __shared__ int32_t sexp[XT + XN];                               // the tile's row exponents
   uint16_t* As = smem;
-  uint16_t* Bs = smem + 3 * XT * XLD;
+  uint16_t* Bs = smem + XPL * XT * XLD;
   // Tiles in (key tile, token tile, head/axis) order, dealt to the eight XCDs in contiguous runs
   // (workgroups go to XCDs round-robin): each XCD walks its own token tiles against every key tile
   // of a head and axis, so both operands' planes are reused from its L2.  The grid is persistent
@@ -531,19 +579,27 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
     h = tz >> 1;
     i0 = (txy % nx) * XN;
     t0 = (txy / nx) * XT;
-    Qa = Qp + static_cast<size_t>(axis) * 3 * qplane + static_cast<size_t>(h) * T * dk;
-    Kb = Kp + static_cast<size_t>(axis) * 3 * kplane + static_cast<size_t>(h) * n * dk;
+    Qa = L.Qp + static_cast<size_t>(axis) * XPL * qplane + static_cast<size_t>(h) * T * dk;
+    Kb = L.Kp + static_cast<size_t>(axis) * XPL * kplane + static_cast<size_t>(h) * n * dk;
   };
   int axis, h, i0, t0;
   const uint16_t *Qa, *Kb;
   coords(first + jt, axis, h, i0, t0, Qa, Kb);
   XSlice sl;
-  x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, 0, tid, sl);
+  x_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, 0, tid, sl);
   while (true) {
     const bool has_next = jt + gx < cnt;
     int naxis = 0, nh = 0, ni0 = 0, nt0 = 0;
     const uint16_t *nQa = Qa, *nKb = Kb;
     if (has_next) coords(first + jt + gx, naxis, nh, ni0, nt0, nQa, nKb);
+    // this tile's row exponents (token rows, then key rows), staged before the last K-step's barrier
+    int32_t e_mine = 0;
+    {
+      const int rr = tid < XT ? t0 + tid : i0 + tid - XT;
+      if (tid < XT ? rr < T : rr < n)
+        e_mine = tid < XT ? L.Qs[(static_cast<size_t>(axis) * H + h) * T + rr]
+                          : L.Ks[(static_cast<size_t>(axis) * H + h) * n + rr];
+    }
     f32x4 acc[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
@@ -551,35 +607,33 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
       for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < dk; k0 += XK) {
 #pragma unroll
-      for (int j = 0; j < 6; ++j) {
+      for (int j = 0; j < 2 * XPL; ++j) {
         const int f = tid + THREADS * j;
         const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
-        *reinterpret_cast<u32x4*>(As + pl * XT * XLD + x6_pos(row, ch)) = sl.a[j];
-        *reinterpret_cast<u32x4*>(Bs + pl * XN * XLD + x6_pos(row, ch)) = sl.b[j];
+        *reinterpret_cast<u32x4*>(As + pl * XT * XLD + x_pos(row, ch)) = sl.a[j];
+        *reinterpret_cast<u32x4*>(Bs + pl * XN * XLD + x_pos(row, ch)) = sl.b[j];
       }
+      if (k0 + XK >= dk) sexp[tid] = e_mine;
       __syncthreads();
-      if (k0 + XK < dk) x6_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + XK, tid, sl);
-      else if (has_next) x6_fetch(nQa, nKb, qplane, kplane, T, n, dk, nt0, ni0, 0, tid, sl);
+      if (k0 + XK < dk) x_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + XK, tid, sl);
+      else if (has_next) x_fetch(nQa, nKb, qplane, kplane, T, n, dk, nt0, ni0, 0, tid, sl);
       // lane: row (token or key) lane % 16 of a 16-block, dims 8 (lane / 16) ... + 7
-      bf16x8 af[3][4], bfr[3][4];
+      f16x8 af[XPL][4], bfr[XPL][4];
 #pragma unroll
-      for (int pl = 0; pl < 3; ++pl)
+      for (int pl = 0; pl < XPL; ++pl)
 #pragma unroll
         for (int a = 0; a < 4; ++a) {
-          af[pl][a] = *reinterpret_cast<const bf16x8*>(As + pl * XT * XLD + x6_pos(wm * 64 + a * 16 + (lane & 15), lane >> 4));
-          bfr[pl][a] = *reinterpret_cast<const bf16x8*>(Bs + pl * XN * XLD + x6_pos(wn * 64 + a * 16 + (lane & 15), lane >> 4));
+          af[pl][a] = *reinterpret_cast<const f16x8*>(As + pl * XT * XLD + x_pos(wm * 64 + a * 16 + (lane & 15), lane >> 4));
+          bfr[pl][a] = *reinterpret_cast<const f16x8*>(Bs + pl * XN * XLD + x_pos(wn * 64 + a * 16 + (lane & 15), lane >> 4));
         }
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          // the six products of significance 2^-16 and above, smaller ones first
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[2][a], bfr[0][b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[1][b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[2][b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][a], bfr[0][b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[1][b], acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][a], bfr[0][b], acc[a][b], 0, 0, 0);
+          // the three products of significance 2^-11 and above, smaller ones first
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[1][a], bfr[0][b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[0][a], bfr[1][b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[0][a], bfr[0][b], acc[a][b], 0, 0, 0);
         }
       __syncthreads();
     }
@@ -602,8 +656,14 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
 #pragma unroll
       for (int it = 0; it < 8; ++it) {
         const int row = (lane >> 4) + 4 * it, c4 = (lane & 15) * 4;
-        const int t = t0 + wm * 64 + half * 32 + row, key = i0 + wn * 64 + c4;
-        const f32x4 v = *reinterpret_cast<const f32x4*>(Cs + row * XLDC + c4);
+        const int tl = wm * 64 + half * 32 + row, kl = wn * 64 + c4;
+        const int t = t0 + tl, key = i0 + kl;
+        f32x4 v = *reinterpret_cast<const f32x4*>(Cs + row * XLDC + c4);
+        const int eq = sexp[tl];
+        v.x = ldexpf(v.x, -(eq + sexp[XT + kl]));                     // exact
+        v.y = ldexpf(v.y, -(eq + sexp[XT + kl + 1]));
+        v.z = ldexpf(v.z, -(eq + sexp[XT + kl + 2]));
+        v.w = ldexpf(v.w, -(eq + sexp[XT + kl + 3]));
         if (t < T && key < n)      // n % 4 == 0: the piece is whole
           __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(sel + ((static_cast<size_t>(axis) * T + t) * H + h) * n + key));
       }
@@ -619,12 +679,11 @@ __global__ __launch_bounds__(THREADS) void axis_scores_x6(
     t0 = nt0;
     Qa = nQa;
     Kb = nKb;
-    __syncthreads();          // the epilogue's LDS rows are free before the next tile is staged
+    __syncthreads();          // the epilogue's LDS rows and sexp are free before the next tile
   }
 }
-static_assert(4 * 32 * XLDC * 4 <= 2 * 3 * XT * XLD * 2, "epilogue staging fits the tiles' LDS");
 
-bool scores_use_x6(const umem_desc& d, int T) {
+bool scores_use_planes(const umem_desc& d, int T) {
   return T > 64 && d.dk % XK == 0 && d.n_keys % 4 == 0 && (d.dk / d.rank) % 8 == 0;
 }
 
@@ -649,8 +708,9 @@ hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, h
 }
 
 size_t score_planes_bytes(const umem_desc& d, int T) {
-  if (!scores_use_x6(d, T)) return 0;
-  return static_cast<size_t>(2) * 3 * (static_cast<size_t>(T) + d.n_keys) * d.heads * d.dk * sizeof(uint16_t);
+  if (!scores_use_planes(d, T)) return 0;
+  return plane_elems(T, d.heads, d.n_keys, d.dk) * sizeof(uint16_t) +
+         static_cast<size_t>(2) * (static_cast<size_t>(T) + d.n_keys) * d.heads * sizeof(int32_t);
 }
 
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
@@ -687,18 +747,26 @@ hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, con
 #undef UMEM_WIDE
     return hipGetLastError();
   }
-  // (the x6 kernel stores 16-byte pieces of sel)
-  if (scores_use_x6(d, T) && planes != nullptr && reinterpret_cast<uintptr_t>(sel) % 16 == 0) {
-    uint16_t* Qp = static_cast<uint16_t*>(planes);
-    uint16_t* Kp = Qp + static_cast<size_t>(2) * 3 * T * d.heads * d.dk;
-    const size_t items = static_cast<size_t>(2) * (static_cast<size_t>(T) + d.n_keys) * d.heads * d.dk / 8;
-    const unsigned blocks = static_cast<unsigned>(std::min<size_t>((items + THREADS - 1) / THREADS, 8192));
-    hipLaunchKernelGGL(split_planes_kernel, dim3(blocks), dim3(THREADS), 0, s, q_row, q_col, k_row,
-                       k_col, c, T, d.heads, d.n_keys, d.dk, d.dk / d.rank, Qp, Kp);
+  // (the plane kernel stores 16-byte pieces of sel)
+  if (scores_use_planes(d, T) && planes != nullptr && reinterpret_cast<uintptr_t>(sel) % 16 == 0) {
+    const PlaneLayout L = plane_layout(planes, T, d.heads, d.n_keys, d.dk);
+    const size_t rows = static_cast<size_t>(2) * (static_cast<size_t>(T) + d.n_keys) * d.heads;
+    const int d8n = d.dk / 8;                      // 4 .. 128 (dk % 32 == 0, dk <= 1024)
+    const int G = d8n <= 4 ? 4 : (d8n <= 8 ? 8 : (d8n <= 16 ? 16 : (d8n <= 32 ? 32 : 64)));
+    const unsigned blocks = static_cast<unsigned>(std::min<size_t>((rows * G + THREADS - 1) / THREADS, 8192));
+#define UMEM_SPLIT_PLANES(GG)                                                                      \
+  hipLaunchKernelGGL(split_planes_kernel<GG>, dim3(blocks), dim3(THREADS), 0, s, q_row, q_col,      \
+                     k_row, k_col, c, T, d.heads, d.n_keys, d.dk, d.dk / d.rank, L)
+    if (G == 4) UMEM_SPLIT_PLANES(4);
+    else if (G == 8) UMEM_SPLIT_PLANES(8);
+    else if (G == 16) UMEM_SPLIT_PLANES(16);
+    else if (G == 32) UMEM_SPLIT_PLANES(32);
+    else UMEM_SPLIT_PLANES(64);
+#undef UMEM_SPLIT_PLANES
     // a persistent grid of 8 gx workgroups (two per CU, as registers allow), gx per XCD
     const long long ntiles = static_cast<long long>((d.n_keys + XN - 1) / XN) * ((T + XT - 1) / XT) * d.heads * 2;
     const dim3 grid(static_cast<unsigned>(8 * std::min<long long>((ntiles + 7) / 8, 64)));
-    hipLaunchKernelGGL(axis_scores_x6, grid, dim3(THREADS), 0, s, Qp, Kp, sel, T, d.heads, d.n_keys,
+    hipLaunchKernelGGL(axis_scores_planes, grid, dim3(THREADS), 0, s, L, sel, T, d.heads, d.n_keys,
                        d.dk, zero, zero_n4);
     return hipGetLastError();
   }

@@ -202,7 +202,7 @@ UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const fl
   if (st == UMEM_OK) st = check_scoring_ptrs(desc, q_row, q_col, k_row, k_col, core);
   if (st == UMEM_OK && (sel == nullptr || !aligned(sel, 4))) st = UMEM_ERR_INVALID_ARG;
   const bool tucker = desc->grid == UMEM_GRID_TUCKER;
-  // [factors (Tucker)] [bf16 planes of the many-token path]
+  // [factors (Tucker)] [fp16 planes of the many-token path]
   const size_t planes_at = tucker ? round_up(kFactorBytes) : 0;
   const size_t planes = score_planes_bytes(*desc, T);
   const size_t need = planes > 0 ? planes_at + planes : (tucker ? kFactorBytes : 0);

@@ -41,8 +41,9 @@ hipError_t launch_rank1(const umem_desc& d, const float* core, float* factors, h
 
 // Selection scores; factors is the output of launch_rank1 (Tucker) or NULL (additive).  With
 // zero_out set the same grid also clears zero_out[0, zero_floats) (a multiple of 4 floats).
-// Scratch of the many-token scoring path (bf16 planes of queries and keys), or 0 where the
-// shape takes another kernel; launch_axis_scores needs it as planes then.
+// Scratch of the many-token scoring path (fp16 planes of queries and keys and their rows'
+// exponents), or 0 where the shape takes another kernel; launch_axis_scores needs it as planes
+// then.
 size_t score_planes_bytes(const umem_desc& d, int T);
 hipError_t launch_axis_scores(const umem_desc& d, int T, const float* q_row, const float* q_col,
                               const float* k_row, const float* k_col, const float* factors,

@@ -110,8 +110,9 @@ def test_entry_points_reject_before_launch():
     tucker = desc(grid=1, rank=2)
     assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, None, fake, fake, 1 << 20, 0) == U.UMEM_ERR_INVALID_ARG
     assert U.umem_axis_scores(tucker, 8, fake, fake, fake, fake, fake, fake, None, 0, 0) == U.UMEM_ERR_WORKSPACE
-    # more than 64 tokens: the bf16 planes of the scoring need their scratch after the factors
-    planes = 2 * 3 * (100 + 4480) * 2 * 128 * 2
+    # more than 64 tokens: the fp16 planes of the scoring and their rows' exponents need their
+    # scratch after the factors
+    planes = 2 * 2 * (100 + 4480) * 2 * 128 * 2 + 2 * (100 + 4480) * 2 * 4
     st, nfull = U.umem_workspace_size(tucker, 100)
     assert st == U.UMEM_OK and nfull >= 2048 + planes
     assert U.umem_axis_scores(tucker, 100, fake, fake, fake, fake, fake, fake, fake, 2048, 0) == U.UMEM_ERR_WORKSPACE

@@ -206,7 +206,7 @@ def test_exact_ties_lower_index(kw):
     dict(T=100, heads=1, dk=256, n_keys=130, rank=2, grid=CF.GRID_TUCKER),    # tiled MFMA
     dict(T=70, heads=3, dk=64, n_keys=200),                                   # tiled MFMA
     dict(T=5, heads=2, dk=12, n_keys=33, rank=3, grid=CF.GRID_TUCKER),        # vector ALU
-    # many tokens on bf16 planes: ragged token and key tiles, three dk steps; dk = 448
+    # many tokens on fp16 planes: ragged token and key tiles, three dk steps; dk = 448
     dict(T=200, heads=3, dk=96, n_keys=300, rank=2, grid=CF.GRID_TUCKER),
     dict(T=130, heads=1, dk=448, n_keys=260),
 ], ids=["wide", "wide-tucker2", "wide-dk256", "wide-dk64", "wide-tucker4", "split-tucker4",
@@ -237,6 +237,41 @@ def test_axis_scores_kernels(kw):
         err = np.abs(got[a] - want) / (scale + 1e-30)
         log(f"[report] axis {a}: max err / sum|q k| = {err.max():.2e}")
         assert err.max() <= 1e-5, (a, err.max())
+
+
+def test_planes_row_exponents():
+    """The fp16-plane scoring scales every query and key row by its own power of two before the
+    split: rows scaled by 2^-40 .. 2^40, a zero row, a row with one nonzero element and a row whose
+    elements span 2^-40 .. 1 all keep their scores within 1e-6 of sum |q_d k_d| of the fp64
+    value."""
+    cfg = small("exps", T=130, heads=2, dk=64, n_keys=256, topk=4, topm=4, dv=8, vdtype=CF.BF16)
+    desc = G.desc_for(cfg)
+    T, H, n, dk = cfg.T, cfg.heads, cfg.n_keys, cfg.dk
+    rng = np.random.default_rng(77)
+    qr, qc = CF.queries(cfg)
+    kr, kc = CF.keys(cfg)
+    qr = qr * np.exp2(rng.integers(-40, 41, size=(T, H, 1))).astype(np.float32)
+    kr = kr * np.exp2(rng.integers(-40, 41, size=(H, n, 1))).astype(np.float32)
+    qr[0] = 0.0
+    kr[:, 0] = 0.0
+    qr[1] = 0.0
+    qr[1, :, 5] = 1.0
+    qr[2] = (rng.standard_normal((H, dk)) * np.exp2(-np.linspace(0, 40, dk))).astype(np.float32)
+    kc[:, 3] = kc[:, 3] * np.float32(2.0 ** 40)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    sel = torch.empty((2, T, H, n), dtype=torch.float32, device="cuda")
+    ws = G.workspace(desc, T)
+    U.check(U.umem_axis_scores(desc, T, dev(qr), dev(qc), dev(kr), dev(kc), None, sel, ws,
+                               ws.numel()), "umem_axis_scores")
+    torch.cuda.synchronize()
+    got = G.host(sel).astype(np.float64)
+    for a, (q, K) in enumerate(((qr, kr), (qc, kc))):
+        want = O.axis_scores(q, K, 1)[:, :, 0, :]
+        scale = np.einsum("thd,hnd->thn", np.abs(q.astype(np.float64)), np.abs(K.astype(np.float64)))
+        err = np.abs(got[a] - want) / (scale + 1e-300)
+        log(f"[report] row exponents, axis {a}: max err / sum|q k| = {err.max():.2e}")
+        assert err.max() <= 1e-6, (a, err.max())
+        assert np.all(got[a][(scale == 0)] == 0.0)
 
 
 # ---------------------------------------------------------------- multi-core scoring
@@ -482,7 +517,7 @@ def test_c3_decode_20m_full_size(c3_values):
 def test_c4_decode_batches(T, c3_values):
     """The decode batch sweep on the 20.07M-slot layer.  Up to 512 tokens the selection pools the
     rows itself (scoring clears the output first: the split, 32 x 32 and, above 64 tokens, the
-    bf16-plane kernel); at 1024 the gather kernel pools them.  Every token up to 256, 256 of
+    fp16-plane kernel); at 1024 the gather kernel pools them.  Every token up to 256, 256 of
     1024."""
     rng = np.random.default_rng(T)
     tokens = None if T <= 256 else np.sort(rng.choice(T, 256, replace=False))
@@ -493,7 +528,7 @@ def test_c4_decode_batches(T, c3_values):
 @pytest.mark.parametrize("n_keys", [300, 301], ids=["planes", "tiled"])
 def test_fused_forward_many_tokens(n_keys):
     """The forward with the selection pooling the rows for 64 < T <= 512 tokens (two heads, 1 KiB
-    bf16 rows, no projection): the scoring kernel, here the bf16-plane one (n % 4 == 0) or the
+    bf16 rows, no projection): the scoring kernel, here the fp16-plane one (n % 4 == 0) or the
     tiled fp32 MFMA one (n % 4 != 0), clears the output with its grid before the selection adds
     both heads' rows into it.  A ragged last token tile (130 = 128 + 2)."""
     cfg = small("fused-many", T=130, heads=2, dk=128, n_keys=n_keys, topk=16, topm=24, dv=512,
@@ -585,7 +620,7 @@ def test_hip_graph_replay_matches_eager():
 
 
 def test_graph_replay_projected_layer_stale_workspace():
-    """A Tucker + IVE layer with projection at 130 tokens (scoring on bf16 planes, the expanded
+    """A Tucker + IVE layer with projection at 130 tokens (scoring on fp16 planes, the expanded
     gather, the projection with a split K) captured in a HIP graph and replayed with a
     garbage-filled workspace and eager work between replays gives the eager results bit for
     bit: nothing reads the workspace before writing it."""

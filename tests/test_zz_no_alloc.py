@@ -37,11 +37,11 @@ def test_static_scratch_limit_on_the_host():
     """The largest decode-20M batch whose workspace fits the static array, and the first that
     does not: the latter is refused (nothing reaches the GPU; the pointers are never read)."""
     d = _desc(CF.C3)
-    fits = [T for T in (707, 708, 709) if U.umem_workspace_size(d, T)[1] <= U.UMEM_STATIC_SCRATCH_BYTES]
-    assert fits == [707, 708]
+    fits = [T for T in (778, 779, 780) if U.umem_workspace_size(d, T)[1] <= U.UMEM_STATIC_SCRATCH_BYTES]
+    assert fits == [778, 779]
     fake = 1 << 20
     args = [fake] * 4 + [None, fake, None, None, None, fake, None, None, 0]
-    assert U.umem_forward_noalloc(d, 709, *args) == U.UMEM_ERR_SCRATCH_LIMIT
+    assert U.umem_forward_noalloc(d, 780, *args) == U.UMEM_ERR_SCRATCH_LIMIT
     assert U.umem_status_string(U.UMEM_ERR_SCRATCH_LIMIT) != "unknown status"
     assert U.umem_forward_noalloc(d, 0, *([None] * 12), 0) == U.UMEM_OK
     bad = _desc(dataclasses.replace(CF.C3, topk=0))
@@ -60,7 +60,7 @@ CASES = [
     # two heads, 1 KiB rows: the selection pools the rows (the scoring clears the output)
     (_small("noalloc-pooled", T=40, heads=2, dk=128, n_keys=150, topk=16, topm=24, dv=512,
             vdtype=CF.BF16), (40, 9)),
-    # rank-2 Tucker + IVE + projection: bf16-plane scoring at 130 tokens, the expanded gather,
+    # rank-2 Tucker + IVE + projection: fp16-plane scoring at 130 tokens, the expanded gather,
     # both GEMMs (the scratch holds the planes, the pooled rows and the intermediate)
     (_small("noalloc-projected", T=130, heads=2, dk=64, n_keys=96, topk=16, topm=24, dv=512,
             vdtype=CF.BF16, rank=2, grid=CF.GRID_TUCKER, expand=4, dv_virt=64, d_out=128), (130, 20)),
