@@ -404,9 +404,10 @@ __global__ __launch_bounds__(kWideWaves * kWave) void axis_scores_wide(
 // split_planes_kernel writes the two planes of Q' and K and every row's exponent s in the
 // workspace, per (axis, plane, head) a [rows, dk] block; axis_scores_planes is a 128 x 128 tile
 // of (tokens x keys) per workgroup, four waves of 64 x 64 (4 x 4 v_mfma_f32_16x16x32_f16 tiles
-// x 3 products), dk in steps of 32 through LDS with the next slice prefetched into registers,
-// and the scores leave through LDS as whole 128-byte lines (nontemporal), each multiplied by its
-// 2^-(s_q + s_k) on the way out.
+// x 3 products), dk in steps of 32 through two LDS buffers (slice k + 1, prefetched into
+// registers, is staged into one while slice k is multiplied from the other; one barrier per
+// step), and the scores leave through LDS as whole 128-byte lines (nontemporal), each multiplied
+// by its 2^-(s_q + s_k) on the way out.
 constexpr int XT = 128, XN = 128, XK = 32;
 constexpr int XLD = XK;                       // LDS pitch in fp16 (64-byte rows, chunks swizzled)
 constexpr int XLDC = 64 + 4;                  // LDS pitch of the epilogue's fp32 rows
@@ -552,18 +553,16 @@ __global__ __launch_bounds__(THREADS) void axis_scores_planes(
     PlaneLayout L, float* __restrict__ sel, int T, int H, int n, int dk, float4* __restrict__ zero,
     int zero_n4) {
   clear_with_grid(zero, zero_n4);
-  // [A | B][plane][row][k] during the K-steps, the waves' fp32 output rows in the epilogue
+  // two buffers of [A | B][plane][row][k] during the K-steps, the waves' fp32 output rows in the
+  // epilogue
   constexpr int kTileElems = 2 * XPL * XT * XLD, kOutElems = 4 * 32 * XLDC * 2;
-  __shared__ __align__(16) uint16_t smem[kTileElems > kOutElems ? kTileElems : kOutElems];
+  __shared__ __align__(16) uint16_t smem[2 * kTileElems > kOutElems ? 2 * kTileElems : kOutElems];
   __shared__ int32_t sexp[XT + XN];                               // the tile's row exponents
-  uint16_t* As = smem;
-  uint16_t* Bs = smem + XPL * XT * XLD;
   // Tiles in (key tile, token tile, head/axis) order, dealt to the eight XCDs in contiguous runs
   // (workgroups go to XCDs round-robin): each XCD walks its own token tiles against every key tile
   // of a head and axis, so both operands' planes are reused from its L2.  The grid is persistent
-  // (8 gx workgroups, gx per XCD): workgroup s of an XCD takes the XCD's tiles s, s + gx, ..., and
-  // the last K-step of a tile fetches the first slice of the next one, under the MFMAs and the
-  // epilogue.
+  // (8 gx workgroups, gx per XCD): workgroup s of an XCD takes the XCD's tiles s, s + gx, ...; the
+  // first slice of the next tile and its row exponents are fetched during the last K-step.
   const int nx = (n + XN - 1) / XN, ny = (T + XT - 1) / XT;
   const int ntiles = nx * ny * 2 * H;
   const int xcd = blockIdx.x & 7, gx = gridDim.x >> 3, per = ntiles >> 3, extra = ntiles & 7;
@@ -582,41 +581,48 @@ __global__ __launch_bounds__(THREADS) void axis_scores_planes(
     Qa = L.Qp + static_cast<size_t>(axis) * XPL * qplane + static_cast<size_t>(h) * T * dk;
     Kb = L.Kp + static_cast<size_t>(axis) * XPL * kplane + static_cast<size_t>(h) * n * dk;
   };
+  // thread tid's row exponent of a tile: token row t0 + tid (tid < XT), key row i0 + tid - XT
+  auto exponent = [&](int axis, int h, int i0, int t0) {
+    const int rr = tid < XT ? t0 + tid : i0 + tid - XT;
+    if (tid < XT ? rr >= T : rr >= n) return 0;
+    return tid < XT ? L.Qs[(static_cast<size_t>(axis) * H + h) * T + rr]
+                    : L.Ks[(static_cast<size_t>(axis) * H + h) * n + rr];
+  };
+  auto stage = [&](const XSlice& sl, uint16_t* buf) {
+#pragma unroll
+    for (int j = 0; j < 2 * XPL; ++j) {
+      const int f = tid + THREADS * j;
+      const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
+      *reinterpret_cast<u32x4*>(buf + pl * XT * XLD + x_pos(row, ch)) = sl.a[j];
+      *reinterpret_cast<u32x4*>(buf + XPL * XT * XLD + pl * XN * XLD + x_pos(row, ch)) = sl.b[j];
+    }
+  };
   int axis, h, i0, t0;
   const uint16_t *Qa, *Kb;
   coords(first + jt, axis, h, i0, t0, Qa, Kb);
   XSlice sl;
   x_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, 0, tid, sl);
+  int32_t e_mine = exponent(axis, h, i0, t0);
   while (true) {
     const bool has_next = jt + gx < cnt;
     int naxis = 0, nh = 0, ni0 = 0, nt0 = 0;
     const uint16_t *nQa = Qa, *nKb = Kb;
     if (has_next) coords(first + jt + gx, naxis, nh, ni0, nt0, nQa, nKb);
-    // this tile's row exponents (token rows, then key rows), staged before the last K-step's barrier
-    int32_t e_mine = 0;
-    {
-      const int rr = tid < XT ? t0 + tid : i0 + tid - XT;
-      if (tid < XT ? rr < T : rr < n)
-        e_mine = tid < XT ? L.Qs[(static_cast<size_t>(axis) * H + h) * T + rr]
-                          : L.Ks[(static_cast<size_t>(axis) * H + h) * n + rr];
-    }
+    stage(sl, smem);                                    // slice 0 (fetched earlier) into buffer 0
+    sexp[tid] = e_mine;
+    __syncthreads();
+    if (XK < dk) x_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, XK, tid, sl);
+    else if (has_next) x_fetch(nQa, nKb, qplane, kplane, T, n, dk, nt0, ni0, 0, tid, sl);
+    if (has_next) e_mine = exponent(naxis, nh, ni0, nt0);
     f32x4 acc[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
       for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int buf = 0;
     for (int k0 = 0; k0 < dk; k0 += XK) {
-#pragma unroll
-      for (int j = 0; j < 2 * XPL; ++j) {
-        const int f = tid + THREADS * j;
-        const int pl = f >> 9, row = (f & 511) >> 2, ch = f & 3;
-        *reinterpret_cast<u32x4*>(As + pl * XT * XLD + x_pos(row, ch)) = sl.a[j];
-        *reinterpret_cast<u32x4*>(Bs + pl * XN * XLD + x_pos(row, ch)) = sl.b[j];
-      }
-      if (k0 + XK >= dk) sexp[tid] = e_mine;
-      __syncthreads();
-      if (k0 + XK < dk) x_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + XK, tid, sl);
-      else if (has_next) x_fetch(nQa, nKb, qplane, kplane, T, n, dk, nt0, ni0, 0, tid, sl);
+      const uint16_t* As = smem + buf * kTileElems;
+      const uint16_t* Bs = As + XPL * XT * XLD;
       // lane: row (token or key) lane % 16 of a 16-block, dims 8 (lane / 16) ... + 7
       f16x8 af[XPL][4], bfr[XPL][4];
 #pragma unroll
@@ -635,7 +641,12 @@ __global__ __launch_bounds__(THREADS) void axis_scores_planes(
           acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[0][a], bfr[1][b], acc[a][b], 0, 0, 0);
           acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[0][a], bfr[0][b], acc[a][b], 0, 0, 0);
         }
+      // slice k + 1 (in registers) into the other buffer while these MFMAs run; one barrier
+      if (k0 + XK < dk) stage(sl, smem + (buf ^ 1) * kTileElems);
       __syncthreads();
+      if (k0 + 2 * XK < dk) x_fetch(Qa, Kb, qplane, kplane, T, n, dk, t0, i0, k0 + 2 * XK, tid, sl);
+      else if (k0 + XK < dk && has_next) x_fetch(nQa, nKb, qplane, kplane, T, n, dk, nt0, ni0, 0, tid, sl);
+      buf ^= 1;
     }
     // D layout: lane holds tokens 4 (lane / 16) + r of key lane % 16.  Each wave's 64 x 64 block
     // leaves in two halves of 32 tokens through LDS (free after the last barrier), as 16-byte
