@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
 FP32_PEAK_TFLOPS = 157.3       # MI355X dense fp32 matrix
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix
+F16_PEAK_TFLOPS = 2500.0       # MI355X dense fp16 matrix
 # Vector lane-operations per second: 256 CUs x 4 SIMDs x 16 lanes per clock (a wave64 instruction
 # every 4 cycles) x 2.4 GHz.  The selection is compare/select work, one lane-op per element
 # examined at the least.
@@ -411,16 +412,22 @@ def roofline_for(cfg, T, name, avg_us, workload, fused, unique_row_bytes=None):
     if name == "axis_scores_kernel":
         tr = measured_traffic(name, workload)
         if work["flops"] / work["bytes"] > FP32_PEAK_TFLOPS * 1e3 / HBM_PEAK_GBS:
-            # the method's fp32 flops; the fp16-plane kernel issues three fp16 products per fp32
-            # one, reported beside against the fp16 peak (the same as bf16's)
+            # the method's flops at fp32 accuracy.  The fp32-MFMA kernel is priced on the fp32
+            # peak; the fp16-plane kernel computes on fp16 MFMA and is priced on that dtype's peak
+            # (the same as bf16's), with its three issued fp16 products per method flop and the
+            # fp32 peak's fraction reported beside.
             achieved = work["flops"] / (avg_us * 1e-6) / 1e12
-            r = dict(base, bound="mfma", achieved=round(achieved, 2), peak=FP32_PEAK_TFLOPS,
-                     unit="TFLOP/s", frac=round(achieved / FP32_PEAK_TFLOPS, 4), traffic=tr,
+            planes = scores_on_planes(cfg, T)
+            peak = F16_PEAK_TFLOPS if planes else FP32_PEAK_TFLOPS
+            r = dict(base, bound="mfma", achieved=round(achieved, 2), peak=peak,
+                     unit="TFLOP/s", frac=round(achieved / peak, 4), traffic=tr,
+                     mfma_dtype="f16 (two parts per fp32 operand)" if planes else "f32",
                      intermediate_bytes=work["intermediate"])
-            if scores_on_planes(cfg, T):
+            if planes:
                 issued = 3 * achieved
                 r.update(issued_fp16_TFLOPs=round(issued, 1),
-                         issued_frac_of_fp16_peak=round(issued / BF16_PEAK_TFLOPS, 4))
+                         issued_frac_of_fp16_peak=round(issued / F16_PEAK_TFLOPS, 4),
+                         frac_of_fp32_peak=round(achieved / FP32_PEAK_TFLOPS, 4))
             return r
         achieved = work["bytes"] / (avg_us * 1e-6) / 1e9
         return dict(base, bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
