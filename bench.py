@@ -391,7 +391,8 @@ class Runner:
                     frac_of_peak=round(rows / secs / 1e9 / HBM_PEAK_GBS, 4),
                     probe_same_rows_GBps=round(rows / probe_secs / 1e9, 1),
                     frac_of_probe=round(probe_secs / secs, 4),
-                    algorithmic_GBps=round(algo / secs / 1e9, 1))
+                    algorithmic_GBps=round(algo / secs / 1e9, 1),
+                    algorithmic_frac_of_peak=round(algo / secs / 1e9 / HBM_PEAK_GBS, 4))
 
 
 def scores_on_planes(cfg, T):

@@ -212,13 +212,18 @@ __device__ inline void rank1_factors(const float* C, int r, int parts, float* u_
       m[i][j] = acc;
       v[i][j] = (i == j) ? 1.0 : 0.0;
     }
+  // A rotation is skipped once its off-diagonal element is below 2^-60 of both diagonal
+  // elements (it would move them by less than their last bit); the sweeps end when one skips all
+  // six.  An exact zero (the padding, a zero column of C) is always skipped.
   for (int sweep = 0; sweep < 12; ++sweep) {
+    bool rotated = false;
 #pragma unroll
     for (int p = 0; p < 3; ++p)
 #pragma unroll
       for (int q = p + 1; q < 4; ++q) {
         const double apq = m[p][q];
-        if (fabs(apq) <= 1e-300) continue;
+        if (fabs(apq) <= 1e-300 || fabs(apq) <= 0x1p-60 * fmin(fabs(m[p][p]), fabs(m[q][q]))) continue;
+        rotated = true;
         const double theta = (m[q][q] - m[p][p]) / (2.0 * apq);
         const double tt = (theta >= 0.0 ? 1.0 : -1.0) / (fabs(theta) + sqrt(theta * theta + 1.0));
         const double cs = 1.0 / sqrt(tt * tt + 1.0);
@@ -243,6 +248,7 @@ __device__ inline void rank1_factors(const float* C, int r, int parts, float* u_
           v[k][q] = sn * vkp + cs * vkq;
         }
       }
+    if (!rotated) break;
   }
   int best = 0;
   double lam = m[0][0];

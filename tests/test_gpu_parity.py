@@ -239,6 +239,57 @@ def test_axis_scores_kernels(kw):
         assert err.max() <= 1e-5, (a, err.max())
 
 
+def _special_cores(rank, rng):
+    """Cores whose leading singular pair the fp64 Jacobi sweeps must find in edge conditions: a
+    diagonal core (nothing to rotate), a zero column (rank-deficient), leading singular values
+    1e-3 apart, scales of 1e-20 and 1e18, and all entries negative."""
+    r = rank
+    cores = [np.diag(np.arange(r, 0, -1)).astype(np.float32)]
+    z = rng.standard_normal((r, r)).astype(np.float32)
+    z[:, -1] = 0.0
+    cores.append(z)
+    u_, _ = np.linalg.qr(rng.standard_normal((r, r)))
+    v_, _ = np.linalg.qr(rng.standard_normal((r, r)))
+    s = np.linspace(1.0, 0.4, r)
+    s[1] = 1.0 - 1e-3
+    cores.append((u_ @ np.diag(s) @ v_.T).astype(np.float32))
+    cores.append(rng.standard_normal((r, r)).astype(np.float32) * np.float32(1e-20))
+    cores.append(rng.standard_normal((r, r)).astype(np.float32) * np.float32(1e18))
+    cores.append(-np.abs(rng.standard_normal((r, r))).astype(np.float32))
+    return np.stack(cores)
+
+
+@pytest.mark.parametrize("T,rank,dk", [(12, 2, 128), (12, 4, 64), (130, 2, 96), (40, 2, 128)],
+                         ids=["split-r2", "split-r4", "planes-r2", "wide-r2"])
+def test_rank1_fold_special_cores(T, rank, dk):
+    """The rank-1 factors of the Tucker core (eqs. (8)-(10)) folded into the axis scores, for the
+    cores of _special_cores (one per head), against the oracle's factors."""
+    cores = _special_cores(rank, np.random.default_rng(31 + rank))
+    H = cores.shape[0]
+    cfg = small("rank1", T=T, heads=H, dk=dk, n_keys=100, topk=4, topm=4, rank=rank,
+                grid=CF.GRID_TUCKER)
+    log(f"[case] rank-1 fold T={T} rank={rank} dk={dk}")
+    dl = SD.make_layer(cfg)
+    dl.core = torch.from_numpy(cores).cuda()
+    desc = G.desc_for(cfg)
+    n = cfg.n_keys
+    sel = torch.empty((2, T, H, n), dtype=torch.float32, device="cuda")
+    ws = G.workspace(desc, T)
+    U.check(U.umem_axis_scores(desc, T, dl.q_row[0], dl.q_col[0], dl.k_row, dl.k_col, dl.core, sel,
+                               ws, ws.numel()), "umem_axis_scores")
+    torch.cuda.synchronize()
+    got = G.host(sel).astype(np.float64)
+    qr, qc = CF.queries(cfg)
+    kr, kc = CF.keys(cfg)
+    f = [O.rank1_factors(cores[h].astype(np.float64)) for h in range(H)]
+    for a, (q, K, v) in enumerate(((qr, kr, [x[0] for x in f]), (qc, kc, [x[1] for x in f]))):
+        want = O.selection_scores(O.axis_scores(q, K, rank), v)
+        scale = np.einsum("thd,hnd->thn", np.abs(q.astype(np.float64)), np.abs(K.astype(np.float64)))
+        err = np.abs(got[a] - want) / (scale + 1e-30)
+        log(f"[report] axis {a}: max err / sum|q k| = {err.max():.2e}")
+        assert err.max() <= 1e-5, (a, err.max())
+
+
 def test_planes_row_exponents():
     """The fp16-plane scoring scales every query and key row by its own power of two before the
     split: rows scaled by 2^-40 .. 2^40, a zero row, a row with one nonzero element and a row whose
