@@ -89,7 +89,7 @@ struct Layout {
 };
 
 // Workspace: [rank-1 factors (Tucker)] [selection scores] [idx] [w] [pooled, bf16] [projection
-// scratch: the intermediate and split-K partials; before the projection, the scoring's bf16
+// scratch: the intermediate and split-K partials; before the projection, the scoring's fp16
 // planes of queries and keys, dead once the scores are written]
 Layout layout(const umem_desc* d, int32_t T) {
   Layout L{};
