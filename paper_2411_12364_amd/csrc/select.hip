@@ -534,14 +534,8 @@ __device__ void pool_rows(const void* __restrict__ values, int dv, int m, bool s
 
 // ---------------------------------------------------------------- the kernel
 
-// The Tucker variant for up to 16 scores per thread (n <= 4096) is held to 64 VGPRs (a few
-// values spill to scratch), so that four workgroups of eight waves share a CU instead of three:
-// the 1.6B-x12 layer's selection 37.2 -> 35.4 us, tucker-ive-4M's 357.5 -> 355.3 us, the same
-// bits.
 template <int NV, int VEC, int MODE>
-__global__ __launch_bounds__(THREADS)
-__attribute__((amdgpu_waves_per_eu(MODE == kModeTucker && NV * VEC <= 16 ? 8 : 2)))
-void select_kernel(
+__global__ __launch_bounds__(THREADS) void select_kernel(
     const float* __restrict__ sel, const float* __restrict__ q_row,
     const float* __restrict__ q_col, const float* __restrict__ k_row,
     const float* __restrict__ k_col, const float* __restrict__ core_all,
