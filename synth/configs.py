@@ -225,9 +225,13 @@ def output_major(w: np.ndarray) -> np.ndarray:
 
 
 def projections(cfg: Layer):
-    """IVE projectors W_p as bf16 bits [E, Dv, D'v] and output linear bf16 bits [D'v, d_out]."""
+    """IVE projectors W_p as bf16 bits [E, Dv, D'v] and output linear bf16 bits [D'v, d_out]; a
+    layer with the output linear alone (D'v = 0) has no W_p and W_out [Dv, d_out]."""
     if cfg.dv_virt == 0:
-        return None, None
+        if cfg.d_out == 0:
+            return None, None
+        wo = S.tensor_f32(cfg.seed, S.TID_W_OUT, (cfg.dv, cfg.d_out), 1.0 / math.sqrt(cfg.dv))
+        return None, S.f32_to_bf16_bits(wo).reshape(wo.shape)
     wp = S.tensor_f32(cfg.seed, S.TID_W_PROJ, (cfg.expand, cfg.dv, cfg.dv_virt), 1.0 / math.sqrt(cfg.dv))
     wp = S.f32_to_bf16_bits(wp).reshape(wp.shape)
     if cfg.d_out == 0:       # the projectors alone

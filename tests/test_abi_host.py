@@ -311,3 +311,14 @@ def test_project_workspace_covers_every_band(T, E, dv, dvv, dout):
         tmp = -(-(T * dvv * 4) // 256) * 256 if dout else 0
         need = tmp + max(_partials_needed(T, dvv, E * dv), _partials_needed(T, dout, dvv) if dout else 0)
     assert n >= need, (n, need)
+
+
+def test_random_layers_are_accepted():
+    """Every seeded random layer of tests/test_gpu_random_layers.py passes the descriptor checks
+    (so its GPU case tests the kernels, not a refusal)."""
+    from tests.gpu_util import desc_for
+    from tests.test_gpu_random_layers import N_CASES, random_layer
+    for i in range(N_CASES):
+        cfg = random_layer(i)
+        st, nbytes = U.umem_workspace_size(desc_for(cfg), cfg.T)
+        assert st == U.UMEM_OK, (i, cfg)

@@ -59,7 +59,7 @@ def run_and_check(cfg, batch=0, tokens=None, gap=P.GAP, expect_no_exempt=False, 
     rep["pooled_err"] = err
     if cfg.dv_virt or cfg.d_out:
         wp, wo = CF.projections(cfg)
-        y_ref = O.ive_project(ref_pooled, S.bf16_bits_to_f32(wp).reshape(wp.shape),
+        y_ref = O.ive_project(ref_pooled, None if wp is None else S.bf16_bits_to_f32(wp).reshape(wp.shape),
                               None if wo is None else S.bf16_bits_to_f32(wo).reshape(wo.shape))
         got = G.host(out_f)[t_sel].astype(np.float64)
         perr = np.abs(got - y_ref).max(axis=1) / np.abs(y_ref).max(axis=1)
@@ -518,11 +518,7 @@ def test_forward_projection_is_gather_then_project(kw):
     log(f"[case] forward = gather + project: {kw}")
     dl = SD.make_layer(cfg)
     T = cfg.T
-    w_proj, w_out = dl.w_proj, dl.w_out
-    if cfg.dv_virt == 0:    # the output linear alone: a weight [d_out, dv], output-major
-        rng = np.random.default_rng(5)
-        wo = S.f32_to_bf16_bits(rng.standard_normal((cfg.d_out, cfg.dv)) / np.sqrt(cfg.dv))
-        w_out = torch.from_numpy(wo.reshape(cfg.d_out, cfg.dv).view(np.int16)).cuda()
+    w_proj, w_out = dl.w_proj, dl.w_out      # the output linear alone: w_out [d_out, dv]
     desc = G.desc_for(cfg)
     out_f = torch.empty((T, cfg.d_out or cfg.dv_virt), dtype=torch.float32, device="cuda")
     idx_f = torch.empty((T, cfg.heads, cfg.topm), dtype=torch.int32, device="cuda")
