@@ -71,3 +71,50 @@ def test_random_layer(i):
     from tests.test_gpu_parity import run_and_check
     cfg = random_layer(i)
     run_and_check(cfg, tokens=None if cfg.T <= 64 else np.arange(0, cfg.T, 5))
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("i", range(0, N_CASES, 2))
+def test_random_layer_backward(i):
+    """The backward of every other random layer at the GPU forward's own selection, against the
+    backward oracle: the value-row and weight gradients (eqs. (1), (15), (17) differentiated),
+    then the query, key and core gradients (eqs. (2)-(4), (10), (16) differentiated)."""
+    import torch
+    import oracle.backward_oracle as B
+    from synth import device as SD
+    from tests import gpu_util as G
+    from tests.test_gpu_backward import RTOL, rel, run_gather_backward, run_score_backward
+    cfg = random_layer(i)
+    print(f"[case] random backward {cfg}", flush=True)
+    dl = SD.make_layer(cfg)
+    T = cfg.T
+    idx, w, _ = G.score_topk(dl, T, 0)
+    rng = np.random.default_rng(700 + i)
+    # b1: value rows and weights
+    dp = rng.standard_normal((T, cfg.expand, cfg.dv)).astype(np.float32)
+    dV = torch.zeros((cfg.n_values, cfg.dv), dtype=torch.float32, device="cuda")
+    wshape = (T, cfg.bag) + ((cfg.cores,) if cfg.cores > 1 else ())
+    dw_g = run_gather_backward(cfg.n_values, cfg.dv, cfg.vdtype, dl.values, T, cfg.bag,
+                               idx.reshape(T, cfg.bag), w.reshape(wshape), dl.perm, cfg.expand,
+                               cfg.cores, torch.from_numpy(dp).cuda(), dV)
+    # b2: queries, keys, core
+    dw_s = rng.standard_normal(tuple(w.shape)).astype(np.float32)
+    dq_row, dq_col, dk_row, dk_col, dcore = run_score_backward(cfg, dl, idx, w, torch.from_numpy(dw_s).cuda())
+    torch.cuda.synchronize()
+    idx_h, w_h = G.host(idx), G.host(w)
+    rows, dV_ref, dw_ref = B.gather_backward(G.value_rows_fn(cfg), idx_h.reshape(T, cfg.bag),
+                                             w_h.reshape(wshape), dp, CF.perm(cfg), cfg.n_values,
+                                             cfg.expand)
+    errs = dict(dV=rel(G.host(dV)[rows], dV_ref), dw=rel(G.host(dw_g), dw_ref))
+    qr, qc = CF.queries(cfg)
+    kr, kc = CF.keys(cfg)
+    core = CF.core(cfg)
+    res = B.score_backward(qr, qc, kr, kc, idx_h, dw_s, w_h, cfg.grid, cfg.weight,
+                           None if cfg.cores > 1 else core, cfg.rank,
+                           core if cfg.cores > 1 else None)
+    errs.update(dq_row=rel(G.host(dq_row), res["dq_row"]), dq_col=rel(G.host(dq_col), res["dq_col"]),
+                dk_row=rel(G.host(dk_row), res["dK_row"]), dk_col=rel(G.host(dk_col), res["dK_col"]))
+    if dcore is not None:
+        errs["dcore"] = rel(G.host(dcore), res["dC"])
+    print(f"[report] random backward {cfg.name}: {errs}", flush=True)
+    assert max(errs.values()) <= RTOL, errs
