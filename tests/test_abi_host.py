@@ -322,3 +322,14 @@ def test_random_layers_are_accepted():
         cfg = random_layer(i)
         st, nbytes = U.umem_workspace_size(desc_for(cfg), cfg.T)
         assert st == U.UMEM_OK, (i, cfg)
+
+
+def test_random_front_ends_are_accepted():
+    from tests.test_gpu_random_layers import N_FRONT_ENDS, random_front_end
+    for i in range(N_FRONT_ENDS):
+        fe = random_front_end(i)
+        d = U.umem_query_desc()
+        d.d_model, d.conv_k, d.heads, d.dk = fe.d_model, fe.conv_k, fe.heads, fe.dk
+        d.shared, d.eps = int(fe.shared), fe.eps
+        st, nbytes = U.umem_query_workspace_size(d, fe.B, fe.L)
+        assert st == U.UMEM_OK, (i, fe)

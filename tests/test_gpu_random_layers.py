@@ -65,6 +65,26 @@ def random_layer(i: int) -> CF.Layer:
                     dv_virt=dv_virt, d_out=d_out, queries=queries, cores=cores)
 
 
+N_FRONT_ENDS = 16
+
+
+def random_front_end(i: int) -> CF.FrontEnd:
+    """A query front-end inside the library's limits (Sec. 3.2 Tricks 2, 4, 5): hidden width a
+    multiple of 8, up to eight taps, 1-4 heads of Dk up to 1024, shared or separate queries, with
+    or without history."""
+    rng = np.random.default_rng(9500 + i)
+    shared = bool(rng.random() < 0.5)
+    heads = int(rng.integers(1, 5))
+    while True:
+        dk = int(rng.choice([int(rng.integers(1, 129)), int(rng.integers(129, 1025))]))
+        if ((1 if shared else 2) * heads * dk) % 8 == 0:
+            break
+    return CF.FrontEnd(f"random-fe-{i}", B=int(rng.integers(1, 9)), L=int(rng.integers(1, 65)),
+                       d_model=8 * int(rng.integers(1, 257)), conv_k=int(rng.integers(1, 9)),
+                       heads=heads, dk=dk, shared=shared, seed=600 + i,
+                       history=bool(rng.random() < 0.7))
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("i", range(N_CASES))
 def test_random_layer(i):
@@ -118,3 +138,28 @@ def test_random_layer_backward(i):
         errs["dcore"] = rel(G.host(dcore), res["dC"])
     print(f"[report] random backward {cfg.name}: {errs}", flush=True)
     assert max(errs.values()) <= RTOL, errs
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("i", range(N_FRONT_ENDS))
+def test_random_front_end(i):
+    """Random query front-ends against the front-end oracle (causal convolution, query linear,
+    per-head LayerNorm), to the tolerance of the bf16 query linear."""
+    from tests.test_gpu_query import (Q_RTOL, ROUNDED_RTOL, oracle_queries, rounded_rows_queries,
+                                      row_err, run_query)
+    fe = random_front_end(i)
+    inp, q_row, q_col, _ = run_query(fe)
+    got = (q_row.cpu().numpy(), q_col.cpu().numpy())
+    # 1. against the oracle's steps with the query linear's documented input rounding
+    ref16 = rounded_rows_queries(fe, inp)
+    e16 = max(row_err(got[a], ref16[:, 0 if fe.shared else a]) for a in (0, 1))
+    # 2. against the plain fp64 oracle, to the query tolerance; a LayerNorm over a handful of
+    # values (Dk < 16) can divide the linear's rounding by a spread far below the values' size,
+    # so there the first check stands alone
+    qr_ref, qc_ref = oracle_queries(fe, inp)
+    er, ec = row_err(got[0], qr_ref), row_err(got[1], qc_ref)
+    print(f"[report] {fe}: against bf16-rounded rows {e16:.2e}; against fp64 q_row {er:.2e}, "
+          f"q_col {ec:.2e}", flush=True)
+    assert e16 <= ROUNDED_RTOL
+    if fe.dk >= 16:
+        assert er <= Q_RTOL and ec <= Q_RTOL
