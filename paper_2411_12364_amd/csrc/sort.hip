@@ -1,17 +1,21 @@
 // Stable sort of (key, value) pairs of 32-bit unsigned keys: least-significant-digit radix sort
-// with 8-bit digits, ceil(bits / 8) passes.  The backward passes use it to bring all
-// contributions to one value row (or key row) together, in their original order, so that one
-// wave sums them in a fixed order and the gradient does not depend on timing.
+// in as few passes of at most 11-bit digits as the key width needs (ceil(bits / 11) passes of
+// ceil(bits / passes) bits: 20-bit row keys in two passes of 10).  The backward passes use it to
+// bring all contributions to one value row (or key row) together, in their original order, so
+// that one wave sums them in a fixed order and the gradient does not depend on timing.
 //
-// Per pass, over tiles of 4096 pairs (256 threads x 16 steps):
-//  * sort_hist_kernel: the tile's digit histogram (LDS atomics), stored digit-major [256][tiles];
-//  * scan_exclusive turns the 256 * tiles counts into exclusive offsets (digit by digit, tile by
+// Per pass, over tiles of 4096 pairs (256 threads x 16 steps), with 2^D digit values:
+//  * sort_hist_kernel: the tile's digit histogram (LDS atomics), stored digit-major
+//    [2^D][tiles];
+//  * scan_exclusive turns the 2^D * tiles counts into exclusive offsets (digit by digit, tile by
 //    tile: the order the stable pass writes in): chunk sums, then each chunk rescanned from the
 //    sum of the chunks before it;
 //  * sort_scatter_kernel: the tile again (all of its pairs loaded up front), 256 consecutive
 //    pairs per step; a pair's place is its digit's running offset in this tile + the count of
 //    equal digits in earlier waves of this step + its rank among equal digits in its own wave
-//    (eight ballots match the digit).
+//    (D ballots match the digit).  Each wave's first pair of a digit posts the wave's count of
+//    it, and after the step adds it to the digit's running offset and clears its post, so a step
+//    costs the same whatever 2^D is.
 #include <utility>
 
 #include "umem_internal.h"
@@ -23,6 +27,8 @@ constexpr int kThreads = 256;
 constexpr int kSteps = 16;
 constexpr int kTile = kThreads * kSteps;
 constexpr int kWaves = kThreads / kWave;
+constexpr int kMaxDigitBits = 11;
+constexpr int kMaxDigits = 1 << kMaxDigitBits;
 
 __device__ __forceinline__ uint64_t lanes_below() {
   const unsigned lane = threadIdx.x & (kWave - 1);
@@ -30,19 +36,22 @@ __device__ __forceinline__ uint64_t lanes_below() {
 }
 
 __global__ __launch_bounds__(kThreads) void sort_hist_kernel(const uint32_t* __restrict__ keys,
-                                                             int M, int shift,
+                                                             int M, int shift, int dbits,
                                                              uint32_t* __restrict__ hist,
                                                              int tiles) {
-  __shared__ uint32_t cnt[256];
-  cnt[threadIdx.x] = 0;
+  __shared__ uint32_t cnt[kMaxDigits];
+  const int nd = 1 << dbits;
+  const uint32_t mask = static_cast<uint32_t>(nd - 1);
+  for (int d = threadIdx.x; d < nd; d += kThreads) cnt[d] = 0;
   __syncthreads();
   const int base = blockIdx.x * kTile;
   for (int q = 0; q < kSteps; ++q) {
     const int pos = base + q * kThreads + threadIdx.x;
-    if (pos < M) atomicAdd(&cnt[(keys[pos] >> shift) & 255u], 1u);
+    if (pos < M) atomicAdd(&cnt[(keys[pos] >> shift) & mask], 1u);
   }
   __syncthreads();
-  hist[static_cast<size_t>(threadIdx.x) * tiles + blockIdx.x] = cnt[threadIdx.x];
+  for (int d = threadIdx.x; d < nd; d += kThreads)
+    hist[static_cast<size_t>(d) * tiles + blockIdx.x] = cnt[d];
 }
 
 // ---------------------------------------------------------------- exclusive scan
@@ -109,13 +118,19 @@ __global__ __launch_bounds__(kThreads) void scan_apply_kernel(uint32_t* __restri
 
 __global__ __launch_bounds__(kThreads) void sort_scatter_kernel(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
-    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int M, int shift,
+    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int M, int shift, int dbits,
     const uint32_t* __restrict__ offs, int tiles) {
-  __shared__ uint32_t base[256];
-  __shared__ uint32_t wcnt[kWaves][256];
+  __shared__ uint32_t base[kMaxDigits];
+  __shared__ uint32_t wcnt[kWaves][kMaxDigits];
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
-  base[tid] = offs[static_cast<size_t>(tid) * tiles + blockIdx.x];
+  const int nd = 1 << dbits;
+  const uint32_t mask = static_cast<uint32_t>(nd - 1);
+  for (int d = tid; d < nd; d += kThreads) {
+    base[d] = offs[static_cast<size_t>(d) * tiles + blockIdx.x];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) wcnt[w][d] = 0;
+  }
   const int tile0 = blockIdx.x * kTile;
   uint32_t kin[kSteps], vin[kSteps];
 #pragma unroll
@@ -124,37 +139,39 @@ __global__ __launch_bounds__(kThreads) void sort_scatter_kernel(
     kin[q] = pos < M ? keys_in[pos] : 0u;
     vin[q] = pos < M ? vals_in[pos] : 0u;
   }
+  __syncthreads();
 #pragma unroll
   for (int q = 0; q < kSteps; ++q) {
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) wcnt[w][tid] = 0;
-    __syncthreads();
     const int pos = tile0 + q * kThreads + tid;
     const bool valid = pos < M;
     const uint32_t key = kin[q];
-    const uint32_t val = vin[q];
-    const uint32_t digit = (key >> shift) & 255u;
+    const uint32_t digit = (key >> shift) & mask;
     uint64_t peers = __ballot(valid);
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const uint64_t ones = __ballot(valid && ((digit >> b) & 1u));
-      peers &= ((digit >> b) & 1u) ? ones : ~ones;
+    for (int b = 0; b < kMaxDigitBits; ++b) {
+      if (b < dbits) {
+        const uint64_t ones = __ballot(valid && ((digit >> b) & 1u));
+        peers &= ((digit >> b) & 1u) ? ones : ~ones;
+      }
     }
     const uint32_t rank = static_cast<uint32_t>(__popcll(peers & lanes_below()));
-    if (valid && rank == 0) wcnt[wave][digit] = static_cast<uint32_t>(__popcll(peers));
+    const uint32_t here = static_cast<uint32_t>(__popcll(peers));
+    const bool leader = valid && rank == 0;
+    if (leader) wcnt[wave][digit] = here;
     __syncthreads();
     if (valid) {
       uint32_t dst = base[digit] + rank;
       for (int w = 0; w < wave; ++w) dst += wcnt[w][digit];
       keys_out[dst] = key;
-      vals_out[dst] = val;
+      vals_out[dst] = vin[q];
     }
     __syncthreads();
-    uint32_t add = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) add += wcnt[w][tid];
-    base[tid] += add;
-    // the next step's clearing of wcnt follows this read only after its own barrier
+    // the digit's running offset takes every wave's count (LDS atomics: an integer sum, exact in
+    // any order); each post is cleared by the wave that made it
+    if (leader) {
+      atomicAdd(&base[digit], here);
+      wcnt[wave][digit] = 0;
+    }
     __syncthreads();
   }
 }
@@ -176,8 +193,8 @@ hipError_t scan_exclusive(uint32_t* v, int n, uint32_t* sums, hipStream_t s) {
 
 size_t sort_workspace_bytes(int M) {
   const size_t tiles = (static_cast<size_t>(M) + kTile - 1) / kTile;
-  return 2 * static_cast<size_t>(M) * sizeof(uint32_t) + 256 * tiles * sizeof(uint32_t) +
-         scan_workspace_bytes(static_cast<int>(256 * tiles)) + 256;
+  return 2 * static_cast<size_t>(M) * sizeof(uint32_t) + kMaxDigits * tiles * sizeof(uint32_t) +
+         scan_workspace_bytes(static_cast<int>(kMaxDigits * tiles)) + 256;
 }
 
 hipError_t sort_pairs(uint32_t* keys, uint32_t* vals, int M, int bits, void* ws, hipStream_t s,
@@ -185,17 +202,21 @@ hipError_t sort_pairs(uint32_t* keys, uint32_t* vals, int M, int bits, void* ws,
   uint32_t* k2 = static_cast<uint32_t*>(ws);
   uint32_t* v2 = k2 + M;
   uint32_t* hist = v2 + M;
-  uint32_t* sums = hist + 256 * static_cast<size_t>((M + kTile - 1) / kTile);
+  uint32_t* sums = hist + kMaxDigits * static_cast<size_t>((M + kTile - 1) / kTile);
   uint32_t *ka = keys, *va = vals, *kb = k2, *vb = v2;
   const int tiles = (M + kTile - 1) / kTile;
-  const int passes = (M <= 1 || bits <= 0) ? 0 : (bits + 7) / 8;
+  const int passes = (M <= 1 || bits <= 0) ? 0 : (bits + kMaxDigitBits - 1) / kMaxDigitBits;
+  const int dbits = passes > 0 ? (bits + passes - 1) / passes : 0;      // <= kMaxDigitBits
+  if (static_cast<int64_t>(tiles) << dbits > static_cast<int64_t>(kScanChunk) * kScanChunk)
+    return hipErrorInvalidValue;                          // beyond the scan (M of 2^25 and more)
   for (int pass = 0; pass < passes; ++pass) {
-    const int shift = 8 * pass;
-    hipLaunchKernelGGL(sort_hist_kernel, dim3(tiles), dim3(kThreads), 0, s, ka, M, shift, hist, tiles);
-    hipError_t e = scan_exclusive(hist, 256 * tiles, sums, s);
+    const int shift = dbits * pass;
+    hipLaunchKernelGGL(sort_hist_kernel, dim3(tiles), dim3(kThreads), 0, s, ka, M, shift, dbits,
+                       hist, tiles);
+    hipError_t e = scan_exclusive(hist, tiles << dbits, sums, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(tiles), dim3(kThreads), 0, s, ka, va, kb, vb, M,
-                       shift, hist, tiles);
+                       shift, dbits, hist, tiles);
     std::swap(ka, kb);
     std::swap(va, vb);
   }
