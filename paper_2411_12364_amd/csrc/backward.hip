@@ -386,9 +386,17 @@ __global__ __launch_bounds__(score_bwd_waves<NG>() * kWave) void score_bwd_kerne
   __shared__ ScoreBwdLds<NG> lds[W];
   const int lane = threadIdx.x & (kWave - 1);
   ScoreBwdLds<NG>& sh = lds[threadIdx.x / kWave];
-  const size_t th = static_cast<size_t>(blockIdx.x) * W + threadIdx.x / kWave;
-  if (th >= static_cast<size_t>(T) * H) return;      // wave-uniform
-  const int h = static_cast<int>(th % H);
+  // (token, head) pairs in head-major order, dealt to the eight XCDs in contiguous runs
+  // (workgroups go to XCDs round-robin): an XCD's pairs then share few heads, and their key rows
+  // stay in its L2 for the two passes over them below
+  const int64_t pairs = static_cast<int64_t>(T) * H;
+  const int64_t nwg = gridDim.x, per = nwg >> 3, extra = nwg & 7;
+  const int64_t xcd = blockIdx.x & 7;
+  const int64_t wg = xcd * per + (xcd < extra ? xcd : extra) + (blockIdx.x >> 3);
+  const int64_t q = wg * W + threadIdx.x / kWave;
+  if (q >= pairs) return;                             // wave-uniform
+  const int h = static_cast<int>(q / T);
+  const size_t th = static_cast<size_t>(q % T) * H + h;
   const int R = tucker ? rank : 1;
   bool valid[NG];
   uint32_t key[2][NG];                                 // row, column of each slot
