@@ -651,8 +651,15 @@ __global__ __launch_bounds__(THREADS) void key_bwd_seg_kernel(
     uint32_t* __restrict__ counts, uint32_t* __restrict__ heads) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t n_pieces = counts[0];
-  for (uint32_t pk = blockIdx.x * NWAVES + threadIdx.x / kWave; pk < n_pieces;
-       pk += gridDim.x * NWAVES) {
+  // The pieces (in (axis, head, key) order) are split into eight contiguous ranges, one per XCD
+  // (workgroups go to XCDs round-robin), so that an XCD's waves read the query rows of few
+  // (axis, head) blocks and find them in its L2.
+  const uint32_t xcd = blockIdx.x & 7u, groups = gridDim.x < 8u ? gridDim.x : 8u;
+  const uint32_t lo = static_cast<uint32_t>(static_cast<uint64_t>(n_pieces) * xcd / groups);
+  const uint32_t hi = static_cast<uint32_t>(static_cast<uint64_t>(n_pieces) * (xcd + 1) / groups);
+  const uint32_t xcd_waves = ((gridDim.x - xcd + 7u) >> 3) * NWAVES;   // this XCD's waves
+  for (uint32_t pk = lo + (blockIdx.x >> 3) * NWAVES + threadIdx.x / kWave; pk < hi;
+       pk += xcd_waves) {
   const int ps = static_cast<int>(list[pk]);
   const uint32_t key = keys[ps];                     // never the sentinel: not listed
   int pe;
