@@ -5,16 +5,18 @@
 // bytes = 16 * L * CPL); a wave keeps U rows in flight.  The loads are nontemporal unless the
 // launch reads at least a quarter as many rows as the table holds: then rows repeat (more than
 // one read in nine even if slots were drawn uniformly, far more with clustered queries) and are
-// worth keeping in L2 and the MALL.  Accumulation is fp32 in registers; the sub-rows of a wave are combined with
-// shuffles, and the four waves' partial rows in LDS behind one barrier, always in wave order
-// (the result does not depend on timing).  Pooled rows are written with plain stores: with
-// implicit value expansion the projection reads them next and finds them cached.  With implicit
-// value expansion the bag is first mapped through the shuffle and split by virtual block p (a
-// stable partition), and each block's rows are pooled into out[t, p, :].  From 2048 tokens on
-// (without expansion) a wave per token does the same work without LDS or barriers.  Pooled rows
-// leave as fp32, or, for the forward's projection, rounded to bf16 (nearest even) by the same
-// instruction with which the projection GEMM rounds its A operand while staging it: the GEMM
-// then reads half the bytes and computes exactly what it computed from the fp32 rows.
+// worth keeping in L2 and the MALL.  Accumulation is fp32 in registers; the sub-rows of a wave
+// are combined with shuffles, and the four waves' partial rows in LDS behind one barrier, always
+// in wave order (the result does not depend on timing).  Pooled rows are written with plain
+// stores: with implicit value expansion the projection reads them next and finds them cached.
+// With implicit value expansion the bag is first mapped through the shuffle and split by
+// virtual block p (a stable partition), and each block's rows are pooled into out[t, p, :]; with
+// a multiple of four blocks each wave pools whole blocks, first entry to last, so the blocks
+// stream side by side with no barrier between them.  From 2048 tokens on (without expansion) a
+// wave per token does the same work without LDS or barriers.  Pooled rows leave as fp32, or, for
+// the forward's projection, rounded to bf16 (nearest even) by the same instruction with which
+// the projection GEMM rounds its A operand while staging it: the GEMM then reads half the bytes
+// and computes exactly what it computed from the fp32 rows.
 #include "umem_internal.h"
 
 namespace umem {
@@ -24,6 +26,13 @@ constexpr int THREADS = 256;
 constexpr int NWAVES = THREADS / kWave;
 constexpr int kWaveTokensMin = 2048;   // from here on, a wave per token
 constexpr int kWaveBatch = 8;          // 16-byte loads per lane per batch of the wave-per-token form
+
+// Partial rows the waves of one token combine in LDS: none when each wave pools whole virtual
+// blocks (expand a multiple of the wave count); else one per wave, or two for rows over 2048
+// elements (waves 2, 3 are folded into 0, 1 first).
+__host__ __device__ constexpr int reduce_rows(int dv, int expand) {
+  return expand > 1 && expand % NWAVES == 0 ? 0 : (dv <= 2048 ? NWAVES : 2);
+}
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -70,33 +79,27 @@ struct ElemTraits<uint16_t> {   // bf16 bit patterns
   }
 };
 
-// Rows of one bag (or of one virtual block of it) are split into NWAVES contiguous ranges, one
-// per wave; sub-group `sub` of a wave (L lanes) reads entries beg + SUB * i + sub of its range.
-// `slot(j)` gives entry j's position in idx / w (after the block partition, if any).  With
-// multi-core scoring (cores > 1) entry s has cores weights, w_of[s * cores + i], and a lane's
-// 16-byte chunk takes the weight of the column slice it lies in.
-template <typename Elem, int L, int CPL, bool KEEP, typename Out, typename Slot>
-__device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int dv, int cnt,
+// One wave's weighted sum of entries [wbeg, wend) into acc: sub-group `sub` of the wave (L
+// lanes) reads entries wbeg + SUB * i + sub in order, and the sub-rows are added by shuffles at
+// the end.  `slot(j)` gives entry j's position in idx / w (after the block partition, if any).
+// With multi-core scoring (cores > 1) entry s has cores weights, w_of[s * cores + i], and a
+// lane's 16-byte chunk takes the weight of the column slice it lies in.
+template <typename Elem, int L, int CPL, bool KEEP, typename Slot>
+__device__ __forceinline__ void wave_rows(const Elem* __restrict__ values, int dv, int wbeg, int wend,
                                           const Slot& slot, const int32_t* __restrict__ rows_of,
-                                          const float* __restrict__ w_of, int cores, float* red,
-                                          Out* __restrict__ dst) {
+                                          const float* __restrict__ w_of, int cores,
+                                          float (&acc)[CPL][ElemTraits<Elem>::kPerChunk]) {
   using TR = ElemTraits<Elem>;
   constexpr int EPC = TR::kPerChunk;
   constexpr int SUB = kWave / L;                   // rows a wave reads at once
   constexpr int U = (CPL >= 16) ? 1 : 16 / CPL;    // row batches in flight per wave
-  const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1);
-  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int lane = threadIdx.x & (kWave - 1);
   const int sub = lane / L;
   const int cl = lane % L;
-  const int per_wave = (cnt + NWAVES - 1) / NWAVES;
-  const int wbeg = wave * per_wave;
-  const int wend = min(cnt, wbeg + per_wave);
   int slice[CPL];                                  // this lane's chunks' core (0 with one core)
 #pragma unroll
   for (int c = 0; c < CPL; ++c) slice[c] = cores > 1 ? ((cl + L * c) * EPC) / (dv / cores) : 0;
 
-  float acc[CPL][EPC];
 #pragma unroll
   for (int c = 0; c < CPL; ++c)
 #pragma unroll
@@ -143,6 +146,26 @@ __device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int d
     for (int c = 0; c < CPL; ++c)
 #pragma unroll
       for (int e = 0; e < EPC; ++e) acc[c][e] += __shfl_xor(acc[c][e], off, kWave);
+}
+
+// Rows of one bag (or of one virtual block of it) split into NWAVES contiguous ranges, one per
+// wave, and the waves' sums combined into one pooled row.
+template <typename Elem, int L, int CPL, bool KEEP, typename Out, typename Slot>
+__device__ __forceinline__ void pool_rows(const Elem* __restrict__ values, int dv, int cnt,
+                                          const Slot& slot, const int32_t* __restrict__ rows_of,
+                                          const float* __restrict__ w_of, int cores, float* red,
+                                          Out* __restrict__ dst) {
+  constexpr int EPC = ElemTraits<Elem>::kPerChunk;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int sub = lane / L;
+  const int cl = lane % L;
+  const int per_wave = (cnt + NWAVES - 1) / NWAVES;
+  const int wbeg = wave * per_wave;
+  const int wend = min(cnt, wbeg + per_wave);
+  float acc[CPL][EPC];
+  wave_rows<Elem, L, CPL, KEEP>(values, dv, wbeg, wend, slot, rows_of, w_of, cores, acc);
   // The waves' partial rows meet in LDS and every thread adds, in wave order, the partials of
   // its columns, then stores them.  Rows of up to 2048 elements use NWAVES partial rows; longer
   // rows (up to 4096) first fold waves 2, 3 into 0, 1, within half the space.
@@ -203,7 +226,7 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
                                        red, out + static_cast<size_t>(t) * dv);
     return;
   }
-  int32_t* rows = reinterpret_cast<int32_t*>(red + (dv <= 2048 ? NWAVES : 2) * dv);   // [bag]
+  int32_t* rows = reinterpret_cast<int32_t*>(red + reduce_rows(dv, expand) * dv);   // [bag]
   int32_t* blk = rows + bag;                                       // [bag]
   int32_t* order = blk + bag;                                      // [bag]
   __shared__ int bstart[kMaxExpand + 1], bcount[kMaxExpand];
@@ -233,6 +256,30 @@ __global__ __launch_bounds__(THREADS) void gather_kernel(
     }
   }
   __syncthreads();
+  if (expand % NWAVES == 0) {
+    // a whole block per wave: the blocks stream side by side, with no barrier between them, and
+    // each pooled row leaves from its wave's registers
+    using TR = ElemTraits<Elem>;
+    constexpr int EPC = TR::kPerChunk;
+    const int w0 = __builtin_amdgcn_readfirstlane(wave);
+    const int cl = lane % L;
+    for (int p = w0; p < expand; p += NWAVES) {
+      const int beg = __builtin_amdgcn_readfirstlane(bstart[p]);
+      const int cnt = __builtin_amdgcn_readfirstlane(bcount[p]);
+      float acc[CPL][EPC];
+      wave_rows<Elem, L, CPL, KEEP>(values, dv, 0, cnt, [=](int j) { return order[beg + j]; },
+                                    rows, w_t, cores, acc);
+      if (lane < L) {
+        Out* dst = out + (static_cast<size_t>(t) * expand + p) * dv;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+#pragma unroll
+          for (int e = 0; e < EPC; e += 4)
+            put4<false>(dst + (cl + L * c) * EPC + e, f32x4{acc[c][e], acc[c][e + 1], acc[c][e + 2], acc[c][e + 3]});
+      }
+    }
+    return;
+  }
   for (int p = 0; p < expand; ++p) {
     const int beg = bstart[p];
     pool_rows<Elem, L, CPL, KEEP, Out>(values, dv, bcount[p], [=](int j) { return order[beg + j]; },
@@ -339,7 +386,7 @@ hipError_t launch_typed(const Elem* values, int64_t n_values, int dv, int T, int
                         const int32_t* idx, const float* w, const int32_t* perm, int expand,
                         int cores, Out* out, hipStream_t s) {
   const int chunks = dv * static_cast<int>(sizeof(Elem)) / 16;
-  const size_t lds = static_cast<size_t>(dv <= 2048 ? NWAVES : 2) * dv * 4 +
+  const size_t lds = static_cast<size_t>(reduce_rows(dv, expand)) * dv * 4 +
                     (expand > 1 ? static_cast<size_t>(bag) * 12 : 0);
   const dim3 block(THREADS);
   // thousands of tokens without expansion (or multi-core weights): a wave per token
