@@ -446,7 +446,10 @@ def test_select_pools_like_gather(kw):
     (512, CF.BF16, 1, 64, 37, 2), (1024, CF.BF16, 4, 100, 37, 4), (64, CF.BF16, 1, 33, 70, 4),
     (256, CF.F32, 1, 33, 4099, 2), (3072, CF.BF16, 1, 20, 9, 8),
     # 8 KiB rows with IVE and two cores (the paper's 1.6B-x12 layer)
-    (4096, CF.BF16, 4, 84, 37, 2)])
+    (4096, CF.BF16, 4, 84, 37, 2),
+    # whole virtual blocks per wave: four blocks each (E = 16), sixteen with sub-rows and two
+    # cores (E = 64), and a bag of one entry (three empty blocks)
+    (256, CF.F32, 16, 50, 37, 1), (64, CF.BF16, 64, 200, 37, 2), (512, CF.BF16, 4, 1, 37, 1)])
 def test_gather_standalone(dv, vdtype, expand, bag, T, cores):
     rng = np.random.default_rng(dv + bag + T + cores)
     Np = 5000
@@ -454,7 +457,8 @@ def test_gather_standalone(dv, vdtype, expand, bag, T, cores):
     values = torch.empty((Np, dv), dtype=vdt, device="cuda")
     SD.fill_normal_(values, 21, S.TID_VALUES, 1 / np.sqrt(dv))
     idx = rng.integers(0, Np * expand, size=(T, bag)).astype(np.int32)
-    idx[:, 1] = idx[:, 0]
+    if bag > 1:
+        idx[:, 1] = idx[:, 0]
     w = rng.standard_normal((T, bag) + ((cores,) if cores > 1 else ())).astype(np.float32)
     perm = rng.permutation(Np * expand).astype(np.int32) if expand > 1 else None
     out = torch.empty((T, expand, dv), dtype=torch.float32, device="cuda")
