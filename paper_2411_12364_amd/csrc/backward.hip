@@ -225,6 +225,11 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
     my_prow = (my_ent / bag) * expand + p;
   }
   const Elem* vrow = values + static_cast<size_t>(row) * dv;
+  // lane j holds entry j's weight gradient per core, summed over the column steps in order and
+  // written once at the end of the piece
+  float my_dw[kMaxCores];
+#pragma unroll
+  for (int c = 0; c < kMaxCores; ++c) my_dw[c] = 0.0f;
   for (int c0 = 0; c0 < dv; c0 += kWave * EPC) {
     const int col = c0 + lane * EPC;
     const bool active = col < dv;
@@ -278,12 +283,11 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
           acc[k + 2] = fmaf(wt[u], vv.z, acc[k + 2]);
           acc[k + 3] = fmaf(wt[u], vv.w, acc[k + 3]);
         }
-        for (int c = 0; c < cores; ++c) {
+#pragma unroll
+        for (int c = 0; c < kMaxCores; ++c) {
+          if (c >= cores) break;
           const float sc = wave_sum(sl == c ? dot : 0.0f);
-          if (lane == 0) {
-            float* d = dw + static_cast<size_t>(ent[u]) * cores + c;
-            *d = c0 == 0 ? sc : *d + sc;              // this wave is the entry's only writer
-          }
+          if (lane == j0 + u) my_dw[c] = c0 == 0 ? sc : my_dw[c] + sc;
         }
       }
     }
@@ -300,6 +304,13 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
 #pragma unroll
       for (int k = 0; k < EPC; k += 4)
         *reinterpret_cast<f32x4*>(dst + k) = f32x4{acc[k], acc[k + 1], acc[k + 2], acc[k + 3]};
+    }
+  }
+  if (lane < n_e) {                                   // this wave is the entries' only writer
+#pragma unroll
+    for (int c = 0; c < kMaxCores; ++c) {
+      if (c >= cores) break;
+      dw[static_cast<size_t>(my_ent) * cores + c] = my_dw[c];
     }
   }
   }
