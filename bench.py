@@ -575,18 +575,39 @@ def backward_report(r, launches=20):
                                    ws2, ws2.numel())
         if st:
             U.check(st, "umem_score_backward")
+    # the compact form: one gradient row per distinct row, written (the dense row is not read)
+    M = T * c.bag
+    rows = torch.empty((M,), dtype=torch.int32, device="cuda")
+    d_rows = torch.empty((M, c.dv), dtype=torch.float32, device="cuda")
+    n_rows = torch.empty((1,), dtype=torch.int32, device="cuda")
+
+    def gr():
+        st = U.umem_gather_backward_rows(c.n_values, c.dv, c.vdtype, dl.values, T, c.bag, idx, w,
+                                         dl.perm, c.expand, c.cores, dp, rows, d_rows, n_rows, dw,
+                                         ws1, ws1.numel())
+        if st:
+            U.check(st, "umem_gather_backward_rows")
     g_us = r._graph_time([gb] * launches) * 1e6
+    gr_us = r._graph_time([gr] * launches) * 1e6
     s_us = r._graph_time([sb] * launches) * 1e6
     uniq = r.unique_rows
-    algo = int(uniq * c.dv * (c.vbytes + 8) + T * c.expand * c.dv * 4 + T * c.bag * 4 * (2 + c.cores))
-    achieved = algo / (g_us * 1e-6) / 1e9
-    out = dict(gather_backward_us=round(g_us, 3), score_backward_us=round(s_us, 3),
+    # value row read and fp32 gradient row read and written per distinct row (the compact form:
+    # written only, plus its row number), d_pooled once, idx, w and dw per entry
+    per_entry = T * c.expand * c.dv * 4 + T * c.bag * 4 * (2 + c.cores)
+    algo = int(uniq * c.dv * (c.vbytes + 8) + per_entry)
+    algo_rows = int(uniq * (c.dv * (c.vbytes + 4) + 4) + per_entry)
+
+    def roof(kernel, us, nbytes):
+        achieved = nbytes / (us * 1e-6) / 1e9
+        return dict(kernel=kernel, bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS,
+                    unit="GB/s", frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
+                    avg_us=round(us, 3), algorithmic_bytes=nbytes)
+    out = dict(gather_backward_us=round(g_us, 3), gather_backward_rows_us=round(gr_us, 3),
+               score_backward_us=round(s_us, 3),
                tokens_per_s=round(T / ((g_us + s_us) * 1e-6), 1),
-               gather_backward_roofline=dict(kernel="gather_backward", bound="hbm",
-                                             achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                                             frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
-                                             avg_us=round(g_us, 3), algorithmic_bytes=algo))
-    del dV, ws1, ws2
+               gather_backward_roofline=roof("gather_backward", g_us, algo),
+               gather_backward_rows_roofline=roof("gather_backward_rows", gr_us, algo_rows))
+    del dV, ws1, ws2, d_rows
     return out
 
 

@@ -247,6 +247,25 @@ UMEM_API umem_status umem_gather_backward(int64_t n_values, int32_t dv, int32_t 
                                  const float* d_pooled, float* d_values, float* dw, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* The same backward (eq. (1); eq. (15); eq. (17)) with the value-row gradients returned
+ * compactly, one row per distinct physical row the bag touches, instead of added into a dense
+ * [n_values, dv] table (41 GB of fp32 for a 20M-slot table of 512-wide rows):
+ *   rows      int32 [T * bag] (capacity): the distinct physical rows, ascending; the first
+ *             *n_rows are written
+ *   d_rows    fp32 [T * bag, dv] (capacity), 16-byte aligned: d_rows[r] = sum over the entries
+ *             on rows[r] of w d_pooled (written, not accumulated; rows past *n_rows untouched)
+ *   n_rows    int32 [1], device memory: the number of distinct rows (written)
+ *   dw, everything else  as for umem_gather_backward; ws of umem_gather_backward_workspace_size
+ * d_rows[r] equals, bit for bit, what umem_gather_backward adds into a zeroed d_values row
+ * rows[r].  The dense gradient row is neither read nor written, so the call moves the value rows,
+ * d_pooled and the compact rows only.  T == 0 writes nothing (n_rows included). */
+UMEM_API umem_status umem_gather_backward_rows(int64_t n_values, int32_t dv, int32_t vdtype,
+                                      const void* values, int32_t T, int32_t bag,
+                                      const int32_t* idx, const float* w, const int32_t* perm,
+                                      int32_t expand, int32_t cores, const float* d_pooled,
+                                      int32_t* rows, float* d_rows, int32_t* n_rows, float* dw,
+                                      void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Backward of the scores (eqs. (2)-(4), (10), (16)) with the forward's selection held fixed: the
  * gradient reaches q, K and C only through the selected slots' scores (the top-k and top-m are
  * piecewise constant; the rank-1 factors only select).  Weight gradients become grid-score

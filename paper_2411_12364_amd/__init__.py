@@ -36,7 +36,7 @@ EXPORTED = ("umem_workspace_size", "umem_axis_scores", "umem_select", "umem_scor
             "umem_gather_sum", "umem_project_workspace_size", "umem_project", "umem_forward",
             "umem_forward_noalloc",
             "umem_query_workspace_size", "umem_query", "umem_key_norm",
-            "umem_gather_backward_workspace_size", "umem_gather_backward",
+            "umem_gather_backward_workspace_size", "umem_gather_backward", "umem_gather_backward_rows",
             "umem_score_backward_workspace_size", "umem_score_backward", "umem_status_string")
 
 
@@ -84,6 +84,8 @@ def _load() -> ctypes.CDLL:
         "umem_key_norm": [I32, I32, I32, P, P, P, ctypes.c_float, P, P],
         "umem_gather_backward_workspace_size": [I32, I32, I32, ctypes.POINTER(SZ)],
         "umem_gather_backward": [I64, I32, I32, P, I32, I32, P, P, P, I32, I32, P, P, P, P, SZ, P],
+        "umem_gather_backward_rows": [I64, I32, I32, P, I32, I32, P, P, P, I32, I32, P, P, P, P, P, P,
+                                      SZ, P],
         "umem_score_backward_workspace_size": [D, I32, ctypes.POINTER(SZ)],
         "umem_score_backward": [D, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
     }
@@ -221,6 +223,14 @@ def umem_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, exp
     return _lib.umem_gather_backward(n_values, dv, vdtype, _p(values), T, bag, _p(idx), _p(w),
                                      _p(perm), expand, cores, _p(d_pooled), _p(d_values), _p(dw),
                                      _p(ws), ws_bytes, _s(stream))
+
+
+def umem_gather_backward_rows(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores,
+                              d_pooled, rows, d_rows, n_rows, dw, ws, ws_bytes, stream=None) -> int:
+    return _lib.umem_gather_backward_rows(n_values, dv, vdtype, _p(values), T, bag, _p(idx), _p(w),
+                                          _p(perm), expand, cores, _p(d_pooled), _p(rows),
+                                          _p(d_rows), _p(n_rows), _p(dw), _p(ws), ws_bytes,
+                                          _s(stream))
 
 
 def umem_score_backward_workspace_size(desc, T):

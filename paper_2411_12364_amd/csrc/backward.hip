@@ -194,6 +194,61 @@ hipError_t list_pieces(const uint32_t* keys, int M, uint32_t sentinel, uint32_t*
   return hipGetLastError();
 }
 
+// Compact row output: run r of the sorted keys (the r-th distinct row, ascending) gets slot r.
+// Per chunk of kListChunk positions the run starts are counted, the counts scanned, then every
+// position's run number written (run_of), each run's row into rows_out[r], and the number of
+// runs into *n_runs.
+__device__ __forceinline__ bool is_run_start(const uint32_t* __restrict__ keys, int i, int M) {
+  return i < M && (i == 0 || keys[i - 1] != keys[i]);
+}
+
+__global__ __launch_bounds__(THREADS) void run_count_kernel(const uint32_t* __restrict__ keys, int M,
+                                                            uint32_t* __restrict__ offs) {
+  __shared__ uint32_t lds[THREADS];
+  const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
+  uint32_t c = 0;
+  for (int k = 0; k < kListPer; ++k) c += is_run_start(keys, beg + k, M);
+  uint32_t total;
+  block_prefix(c, lds, &total);
+  if (threadIdx.x == 0) offs[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(THREADS) void run_write_kernel(const uint32_t* __restrict__ keys, int M,
+                                                            const uint32_t* __restrict__ offs,
+                                                            uint32_t* __restrict__ run_of,
+                                                            int32_t* __restrict__ rows_out,
+                                                            int32_t* __restrict__ n_runs) {
+  __shared__ uint32_t lds[THREADS];
+  const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
+  uint32_t c = 0;
+  for (int k = 0; k < kListPer; ++k) c += is_run_start(keys, beg + k, M);
+  uint32_t total;
+  uint32_t at = offs[blockIdx.x] + block_prefix(c, lds, &total);   // runs started before beg
+  for (int k = 0; k < kListPer && beg + k < M; ++k) {
+    if (is_run_start(keys, beg + k, M)) rows_out[at++] = static_cast<int32_t>(keys[beg + k]);
+    run_of[beg + k] = at - 1;                         // position 0 starts a run: at >= 1 here
+  }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *n_runs = static_cast<int32_t>(offs[blockIdx.x] + total);
+}
+
+// run_of / rows_out / *n_runs of the sorted keys (no sentinel).  ws: list_workspace_bytes(M).
+hipError_t index_runs(const uint32_t* keys, int M, uint32_t* run_of, int32_t* rows_out,
+                      int32_t* n_runs, void* ws, hipStream_t s) {
+  const int chunks = (M + kListChunk - 1) / kListChunk;
+  uint32_t* offs = static_cast<uint32_t*>(ws);
+  uint32_t* sums = offs + chunks + 1;
+  hipLaunchKernelGGL(run_count_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, offs);
+  hipError_t e = scan_exclusive(offs, chunks, sums, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(run_write_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, offs, run_of,
+                     rows_out, n_runs);
+  return hipGetLastError();
+}
+
+// With run_of given (compact row output), a row's gradient goes to out[run_of[position] * dv],
+// written from zero; otherwise it is added into out[row * dv].  Either way the value stored is
+// (the row's previous value, or 0) + the row's sum, so a compact row holds exactly what the
+// dense form adds into a zeroed row.
 template <typename Elem>
 __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
     const uint32_t* __restrict__ rows, const uint32_t* __restrict__ ents, int M,
@@ -201,7 +256,7 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
     const float* __restrict__ w, const int32_t* __restrict__ perm, int64_t n_values, int expand,
     int cores, int bag, const float* __restrict__ d_pooled, float* __restrict__ d_values,
     float* __restrict__ dw, float* __restrict__ partial, const uint32_t* __restrict__ list,
-    uint32_t* __restrict__ counts, uint32_t* __restrict__ heads) {
+    uint32_t* __restrict__ counts, uint32_t* __restrict__ heads, const uint32_t* __restrict__ run_of) {
   constexpr int EPC = Chunk<Elem>::kElems;            // elements per 16-byte piece
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t n_pieces = counts[0];
@@ -225,6 +280,7 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
     my_prow = (my_ent / bag) * expand + p;
   }
   const Elem* vrow = values + static_cast<size_t>(row) * dv;
+  float* drow = d_values + static_cast<size_t>(run_of != nullptr ? run_of[ps] : row) * dv;
   // lane j holds entry j's weight gradient per core, summed over the column steps in order and
   // written once at the end of the piece
   float my_dw[kMaxCores];
@@ -242,12 +298,13 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
     }
     if (active) Chunk<Elem>::load(vrow + col, x);
     // a whole run adds into its gradient row: read that row now, under the entries' loads
+    // (a compact row starts from zero)
     const bool whole = run_start && run_end;
     f32x4 old[EPC / 4];
 #pragma unroll
     for (int k = 0; k < EPC / 4; ++k)
-      old[k] = (active && whole) ? *reinterpret_cast<const f32x4*>(d_values + static_cast<size_t>(row) * dv + col + 4 * k)
-                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+      old[k] = (active && whole && run_of == nullptr) ? *reinterpret_cast<const f32x4*>(drow + col + 4 * k)
+                                                      : f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j0 = 0; j0 < n_e; j0 += kInFlight) {    // wave-uniform
       int ent[kInFlight];
       float wt[kInFlight];
@@ -297,7 +354,7 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
       for (int k = 0; k < EPC; k += 4) {
         f32x4 v = old[k / 4];
         v.x += acc[k]; v.y += acc[k + 1]; v.z += acc[k + 2]; v.w += acc[k + 3];
-        *reinterpret_cast<f32x4*>(d_values + static_cast<size_t>(row) * dv + col + k) = v;
+        *reinterpret_cast<f32x4*>(drow + col + k) = v;
       }
     } else {                                          // cut by a segment edge: its partial row
       float* dst = partial + (static_cast<size_t>(2) * g + (run_start ? 1 : 0)) * dv + col;
@@ -322,7 +379,8 @@ __global__ __launch_bounds__(THREADS) void seg_join_kernel(const uint32_t* __res
                                                            float* __restrict__ out,
                                                            const uint32_t* __restrict__ heads,
                                                            const uint32_t* __restrict__ counts,
-                                                           int H, int n, float* __restrict__ out2) {
+                                                           int H, int n, float* __restrict__ out2,
+                                                           const uint32_t* __restrict__ run_of) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t n_heads = counts[1];
   for (uint32_t hk = blockIdx.x * NWAVES + threadIdx.x / kWave; hk < n_heads;
@@ -334,7 +392,9 @@ __global__ __launch_bounds__(THREADS) void seg_join_kernel(const uint32_t* __res
   const int g1 = (end - 1) / kSeg;
   // the row of this key: value rows directly, or (out2 given) key rows of the two axes
   float* dst;
-  if (out2 == nullptr) {
+  if (run_of != nullptr) {                           // compact rows: written from zero
+    dst = out + static_cast<size_t>(run_of[i]) * width;
+  } else if (out2 == nullptr) {
     dst = out + static_cast<size_t>(key) * width;
   } else {
     const int axis = static_cast<int>(key / (static_cast<uint32_t>(H) * n));
@@ -345,7 +405,7 @@ __global__ __launch_bounds__(THREADS) void seg_join_kernel(const uint32_t* __res
     for (int g = g0 + 1; g <= g1; ++g)
       acc += *reinterpret_cast<const f32x4*>(partial + static_cast<size_t>(2) * g * width + c);
     f32x4* d = reinterpret_cast<f32x4*>(dst + c);
-    f32x4 v = *d;
+    f32x4 v = run_of != nullptr ? f32x4{0.f, 0.f, 0.f, 0.f} : *d;
     v += acc;
     *d = v;
   }
@@ -760,15 +820,19 @@ size_t gather_backward_workspace_bytes(int T, int bag, int dv) {
   const int M = T * bag;
   if (M == 0) return 0;
   const size_t nseg = (static_cast<size_t>(M) + kSeg - 1) / kSeg;
-  return 3 * round_up256(static_cast<size_t>(M) * sizeof(uint32_t)) + round_up256(nseg * sizeof(uint32_t)) +
+  return 4 * round_up256(static_cast<size_t>(M) * sizeof(uint32_t)) + round_up256(nseg * sizeof(uint32_t)) +
          256 + round_up256(2 * nseg * dv * sizeof(float)) + round_up256(sort_workspace_bytes(M)) +
          round_up256(list_workspace_bytes(M));
 }
 
+// rows_out == nullptr: d_values is the dense [n_values, dv] gradient, added into.  Otherwise the
+// compact form: d_values is [T * bag, dv], row r the gradient of rows_out[r], the r-th distinct
+// row (ascending), and *n_rows the number of distinct rows.
 hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const void* values, int T,
                                   int bag, const int32_t* idx, const float* w, const int32_t* perm,
                                   int expand, int cores, const float* d_pooled, float* d_values,
-                                  float* dw, void* ws, hipStream_t s) {
+                                  float* dw, int32_t* rows_out, int32_t* n_rows, void* ws,
+                                  hipStream_t s) {
   clear_stale_error();
   const int M = T * bag;
   if (M == 0) return hipSuccess;
@@ -786,6 +850,7 @@ hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const vo
   float* partial = reinterpret_cast<float*>(p0);
   void* sws = p0 + round_up256(2 * nseg * dv * sizeof(float));
   void* lws = static_cast<char*>(sws) + round_up256(sort_workspace_bytes(M));
+  uint32_t* run_of = reinterpret_cast<uint32_t*>(static_cast<char*>(lws) + round_up256(list_workspace_bytes(M)));
   const unsigned kb = static_cast<unsigned>(std::min((M + THREADS - 1) / THREADS, 4096));
   hipLaunchKernelGGL(bwd_keys_kernel, dim3(kb), dim3(THREADS), 0, s, idx,
                      expand > 1 ? perm : nullptr, n_values, M, keys, vals);
@@ -797,18 +862,24 @@ hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const vo
   // row indices are below 2^31: the sentinel never occurs
   e = list_pieces(rows_sorted, M, 0xFFFFFFFFu, list, counts, lws, s);
   if (e != hipSuccess) return e;
+  const bool compact = rows_out != nullptr;
+  if (compact) {                                      // (reuses the list's scratch, now free)
+    e = index_runs(rows_sorted, M, run_of, rows_out, n_rows, lws, s);
+    if (e != hipSuccess) return e;
+  }
+  const uint32_t* ro = compact ? run_of : nullptr;
   if (vdtype == UMEM_F32)
     hipLaunchKernelGGL(gather_bwd_seg_kernel<float>, list_grid, dim3(THREADS), 0, s, rows_sorted,
                        ents_sorted, M, static_cast<const float*>(values), dv, idx, w,
                        expand > 1 ? perm : nullptr, n_values, expand, c, bag, d_pooled, d_values, dw,
-                       partial, list, counts, heads);
+                       partial, list, counts, heads, ro);
   else
     hipLaunchKernelGGL(gather_bwd_seg_kernel<uint16_t>, list_grid, dim3(THREADS), 0, s, rows_sorted,
                        ents_sorted, M, static_cast<const uint16_t*>(values), dv, idx, w,
                        expand > 1 ? perm : nullptr, n_values, expand, c, bag, d_pooled, d_values, dw,
-                       partial, list, counts, heads);
+                       partial, list, counts, heads, ro);
   hipLaunchKernelGGL(seg_join_kernel, list_grid, dim3(THREADS), 0, s, rows_sorted, M, dv, partial,
-                     d_values, heads, counts, 0, 0, nullptr);
+                     d_values, heads, counts, 0, 0, nullptr, ro);
   return hipGetLastError();
 }
 
@@ -883,7 +954,7 @@ hipError_t launch_score_backward(const umem_desc& d, int T, const float* q_row, 
   hipLaunchKernelGGL(key_bwd_seg_kernel, list_grid, dim3(THREADS), 0, s, ks, vs, Mk, sentinel, edS,
                      q_row, q_col, dk_row, dk_col, H, d.n_keys, d.dk, r, m, kpart, list, counts, heads);
   hipLaunchKernelGGL(seg_join_kernel, list_grid, dim3(THREADS), 0, s, ks, Mk, d.dk, kpart, dk_row,
-                     heads, counts, H, d.n_keys, dk_col);
+                     heads, counts, H, d.n_keys, dk_col, nullptr);
   if (tucker)   // dC: the per-token partials [T][H dc], summed over tokens into dcore
     hipLaunchKernelGGL(sum_cols_kernel, dim3(H * dc), dim3(THREADS), 0, s, dc_part, dcore, T, H * dc);
   return hipGetLastError();

@@ -395,7 +395,28 @@ UMEM_API umem_status umem_gather_backward(int64_t n_values, int32_t dv, int32_t 
   const size_t need = gather_backward_workspace_bytes(T, bag, dv);
   if (ws == nullptr || !aligned(ws, 16) || ws_bytes < need) return UMEM_ERR_WORKSPACE;
   return hip_status(launch_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm,
-                                           expand, cores, d_pooled, d_values, dw, ws, stream));
+                                           expand, cores, d_pooled, d_values, dw, nullptr, nullptr,
+                                           ws, stream));
+}
+
+UMEM_API umem_status umem_gather_backward_rows(int64_t n_values, int32_t dv, int32_t vdtype,
+                                               const void* values, int32_t T, int32_t bag,
+                                               const int32_t* idx, const float* w,
+                                               const int32_t* perm, int32_t expand, int32_t cores,
+                                               const float* d_pooled, int32_t* rows, float* d_rows,
+                                               int32_t* n_rows, float* dw, void* ws,
+                                               size_t ws_bytes, hipStream_t stream) {
+  umem_status st = check_gather(n_values, dv, vdtype, values, T, bag, idx, w, expand, cores, d_rows);
+  if (st != UMEM_OK || T == 0) return st;
+  if (!rows || !n_rows || !aligned(rows, 4) || !aligned(n_rows, 4)) return UMEM_ERR_INVALID_ARG;
+  if (!d_pooled || !dw || !aligned(d_pooled, 16) || !aligned(dw, 4)) return UMEM_ERR_INVALID_ARG;
+  if ((expand > 1) != (perm != nullptr) || !aligned(perm, 4)) return UMEM_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(T) * bag > kMaxBackwardEntries) return UMEM_ERR_UNSUPPORTED;
+  const size_t need = gather_backward_workspace_bytes(T, bag, dv);
+  if (ws == nullptr || !aligned(ws, 16) || ws_bytes < need) return UMEM_ERR_WORKSPACE;
+  return hip_status(launch_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm,
+                                           expand, cores, d_pooled, d_rows, dw, rows, n_rows, ws,
+                                           stream));
 }
 
 UMEM_API umem_status umem_score_backward_workspace_size(const umem_desc* desc, int32_t T,

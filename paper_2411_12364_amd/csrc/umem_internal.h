@@ -114,7 +114,8 @@ size_t gather_backward_workspace_bytes(int T, int bag, int dv);
 hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const void* values, int T,
                                   int bag, const int32_t* idx, const float* w, const int32_t* perm,
                                   int expand, int cores, const float* d_pooled, float* d_values,
-                                  float* dw, void* ws, hipStream_t s);
+                                  float* dw, int32_t* rows_out, int32_t* n_rows, void* ws,
+                                  hipStream_t s);
 size_t score_backward_workspace_bytes(const umem_desc& d, int T);
 hipError_t launch_score_backward(const umem_desc& d, int T, const float* q_row, const float* q_col,
                                  const float* k_row, const float* k_col, const float* core,

@@ -253,6 +253,19 @@ def test_backward_validation():
     g4 = list(g)
     g4[9] = 4                                                          # expand without perm
     assert U.umem_gather_backward(*g4, fake, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG
+    # the compact form: d_pooled, rows, d_rows, n_rows, dw, ws, ws_bytes, stream
+    R = U.umem_gather_backward_rows
+    assert R(*g, None, fake, fake, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG     # d_pooled
+    assert R(*g, fake, None, fake, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG     # rows
+    assert R(*g, fake, fake, None, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG     # d_rows
+    assert R(*g, fake, fake, fake, None, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG     # n_rows
+    assert R(*g, fake, fake, fake + 4, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG  # d_rows aligned
+    assert R(*g, fake, fake + 2, fake, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG  # rows aligned
+    assert R(*g, fake, fake, fake, fake, fake, fake, 16, 0) == U.UMEM_ERR_WORKSPACE
+    assert R(*g4, fake, fake, fake, fake, fake, fake, n, 0) == U.UMEM_ERR_INVALID_ARG
+    g0 = list(g)
+    g0[4] = 0                                                          # T == 0: nothing to do
+    assert R(*g0, None, None, None, None, None, None, 0, 0) == U.UMEM_OK
     d = desc(grid=1, rank=2)
     st, ns = U.umem_score_backward_workspace_size(d, 32)
     assert st == U.UMEM_OK and ns > 0

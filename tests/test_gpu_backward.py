@@ -46,7 +46,23 @@ def run_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expa
     return dw
 
 
-@pytest.mark.parametrize("dv,vdtype,expand,bag,T,cores,Np", [
+def run_gather_backward_rows(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand, cores, dp):
+    """The compact form; rows past the count keep their sentinels (-1 / NaN)."""
+    st, nws = U.umem_gather_backward_workspace_size(T, bag, dv)
+    U.check(st)
+    ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
+    M = T * bag
+    rows = torch.full((M,), -1, dtype=torch.int32, device="cuda")
+    d_rows = torch.full((M, dv), float("nan"), dtype=torch.float32, device="cuda")
+    n_rows = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    dw = torch.empty(w.shape, dtype=torch.float32, device="cuda")
+    U.check(U.umem_gather_backward_rows(n_values, dv, vdtype, values, T, bag, idx, w, perm, expand,
+                                        cores, dp, rows, d_rows, n_rows, dw, ws, ws.numel()),
+            "umem_gather_backward_rows")
+    return rows, d_rows, n_rows, dw
+
+
+GATHER_BWD_CASES = [
     (512, CF.BF16, 1, 64, 37, 1, 300),        # many repeated rows
     (256, CF.F32, 1, 33, 20, 1, 5000),        # few repeats
     (512, CF.BF16, 4, 96, 25, 2, 200),        # IVE blocks, two cores
@@ -58,10 +74,13 @@ def run_gather_backward(n_values, dv, vdtype, values, T, bag, idx, w, perm, expa
     (512, CF.BF16, 4, 32, 600, 2, 300),       # IVE blocks, two cores
     # the library's limits: a bag of 2048, E = 64, eight cores
     (64, CF.BF16, 64, 2048, 5, 8, 4096),
-])
-def test_gather_backward(dv, vdtype, expand, bag, T, cores, Np):
+]
+
+
+def gather_backward_inputs(dv, vdtype, expand, bag, T, cores, Np):
+    """Seeded bags over min(Np, 4096) rows (forcing repeats), weights, d_pooled; the value
+    table from torch's generator."""
     rng = np.random.default_rng(dv + bag + T + cores)
-    log(f"[case] gather backward dv={dv} E={expand} bag={bag} T={T} cores={cores} Np={Np}")
     torch_dt = torch.float32 if vdtype == CF.F32 else torch.bfloat16
     rows_used = min(Np, 4096)
     V = torch.randn((Np, dv), dtype=torch.float32, device="cuda").to(torch_dt)
@@ -73,12 +92,19 @@ def test_gather_backward(dv, vdtype, expand, bag, T, cores, Np):
         perm = (perm % (rows_used * expand)).astype(np.int32) if Np > rows_used else perm
     w = rng.standard_normal((T, bag) + ((cores,) if cores > 1 else ())).astype(np.float32)
     dp = rng.standard_normal((T, expand, dv)).astype(np.float32)
+    dev = dict(idx=torch.from_numpy(idx).cuda(), w=torch.from_numpy(w).cuda(),
+               perm=None if perm is None else torch.from_numpy(perm).cuda(), dp=torch.from_numpy(dp).cuda())
+    return V, idx, perm, w, dp, dev
+
+
+@pytest.mark.parametrize("dv,vdtype,expand,bag,T,cores,Np", GATHER_BWD_CASES)
+def test_gather_backward(dv, vdtype, expand, bag, T, cores, Np):
+    log(f"[case] gather backward dv={dv} E={expand} bag={bag} T={T} cores={cores} Np={Np}")
+    V, idx, perm, w, dp, dev = gather_backward_inputs(dv, vdtype, expand, bag, T, cores, Np)
     dV0 = torch.randn((Np, dv), dtype=torch.float32, device="cuda")
     dV = dV0.clone()
-    dw = run_gather_backward(Np, dv, vdtype, V, T, bag, torch.from_numpy(idx).cuda(),
-                             torch.from_numpy(w).cuda(),
-                             None if perm is None else torch.from_numpy(perm).cuda(), expand, cores,
-                             torch.from_numpy(dp).cuda(), dV)
+    dw = run_gather_backward(Np, dv, vdtype, V, T, bag, dev["idx"], dev["w"], dev["perm"], expand,
+                             cores, dev["dp"], dV)
     torch.cuda.synchronize()
     Vh = V.float().cpu().numpy()
     rows, dV_ref, dw_ref = B.gather_backward(lambda r: Vh[r], idx, w, dp, perm, Np, expand)
@@ -90,6 +116,62 @@ def test_gather_backward(dv, vdtype, expand, bag, T, cores, Np):
     log(f"[report] gather backward dv={dv} E={expand} cores={cores}: {len(rows)} rows, "
         f"dw err {e_dw:.2e}, dV err {e_dv:.2e}")
     assert e_dw <= RTOL and e_dv <= RTOL
+
+
+@pytest.mark.parametrize("dv,vdtype,expand,bag,T,cores,Np", GATHER_BWD_CASES)
+def test_gather_backward_rows(dv, vdtype, expand, bag, T, cores, Np):
+    """The compact form: the distinct rows ascending and their count, each row's gradient equal
+    bit for bit to what the dense form adds into a zeroed row, the same dw, nothing written past
+    the count; and against the backward oracle."""
+    log(f"[case] gather backward rows dv={dv} E={expand} bag={bag} T={T} cores={cores} Np={Np}")
+    V, idx, perm, w, dp, dev = gather_backward_inputs(dv, vdtype, expand, bag, T, cores, Np)
+    dV = torch.zeros((Np, dv), dtype=torch.float32, device="cuda")
+    dw_dense = run_gather_backward(Np, dv, vdtype, V, T, bag, dev["idx"], dev["w"], dev["perm"],
+                                   expand, cores, dev["dp"], dV)
+    rows, d_rows, n_rows, dw = run_gather_backward_rows(Np, dv, vdtype, V, T, bag, dev["idx"], dev["w"],
+                                                        dev["perm"], expand, cores, dev["dp"])
+    torch.cuda.synchronize()
+    Vh = V.float().cpu().numpy()
+    rows_ref, dV_ref, dw_ref = B.gather_backward(lambda r: Vh[r], idx, w, dp, perm, Np, expand)
+    order = np.argsort(rows_ref)
+    n = int(n_rows.item())
+    assert n == len(rows_ref)
+    got_rows = rows.cpu().numpy()
+    assert np.array_equal(got_rows[:n], np.asarray(rows_ref)[order])
+    assert (got_rows[n:] == -1).all()
+    assert torch.equal(d_rows[:n], dV[rows[:n].long()])
+    assert torch.isnan(d_rows[n:]).all()
+    assert torch.equal(dw, dw_dense)
+    e_dv = rel(d_rows[:n].cpu().numpy(), np.asarray(dV_ref)[order])
+    log(f"[report] gather backward rows dv={dv} E={expand} cores={cores}: {n} rows, dV err {e_dv:.2e}")
+    assert e_dv <= RTOL
+
+
+def test_gather_backward_rows_tucker_ive():
+    """The compact form at the 4M-slot Tucker + IVE layer's 4096-token batch (clustered queries:
+    runs of hundreds of entries spanning many segments), against the dense form bit for bit."""
+    cfg = CF.C5
+    dl = SD.make_layer(cfg)
+    idx, w, _ = G.score_topk(dl, cfg.T, 0)
+    rng = np.random.default_rng(6)
+    dp = torch.from_numpy(rng.standard_normal((cfg.T, cfg.expand, cfg.dv)).astype(np.float32)).cuda()
+    idx2, w2 = idx.reshape(cfg.T, cfg.bag), w.reshape(cfg.T, cfg.bag)
+    dV = torch.zeros((cfg.n_values, cfg.dv), dtype=torch.float32, device="cuda")
+    dw_dense = run_gather_backward(cfg.n_values, cfg.dv, cfg.vdtype, dl.values, cfg.T, cfg.bag, idx2,
+                                   w2, dl.perm, cfg.expand, 1, dp, dV)
+    rows, d_rows, n_rows, dw = run_gather_backward_rows(cfg.n_values, cfg.dv, cfg.vdtype, dl.values,
+                                                        cfg.T, cfg.bag, idx2, w2, dl.perm, cfg.expand,
+                                                        1, dp)
+    torch.cuda.synchronize()
+    n = int(n_rows.item())
+    idx_h = G.host(idx2).astype(np.int64)
+    _, row = O.address_map(idx_h, CF.perm(cfg), cfg.n_values, cfg.expand)
+    uniq = np.unique(row)
+    log(f"[report] gather backward rows tucker-ive-4M: {n} distinct rows of {row.size} entries")
+    assert n == len(uniq)
+    assert np.array_equal(rows[:n].cpu().numpy(), uniq)
+    assert torch.equal(d_rows[:n], dV[rows[:n].long()])
+    assert torch.equal(dw, dw_dense)
 
 
 def test_gather_backward_deterministic():
