@@ -112,7 +112,10 @@ __device__ __forceinline__ bool piece_at(const uint32_t* __restrict__ keys, int 
   return true;
 }
 
-constexpr int kListWaves = 8192;        // waves of the grids that walk the lists
+constexpr int kListWaves = 8192;        // waves of the grids that walk the key lists (b2)
+// ... and the value-row lists (b1): four waves per SIMD, which the piece kernel's registers allow;
+// more value-row loads in flight pay where rows repeat (measured at tucker-ive-4M: 473 -> 453 us)
+constexpr int kValueListWaves = 16384;
 constexpr int kInFlight = 4;            // a piece's entries whose loads are issued together
 
 constexpr int kListPer = 16;                           // positions per thread
@@ -858,7 +861,7 @@ hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const vo
   hipError_t e = sort_pairs(keys, vals, M, bits_for(n_values), sws, s, &rows_sorted, &ents_sorted);
   if (e != hipSuccess) return e;
   const int c = cores > 1 ? cores : 1;
-  const dim3 list_grid(kListWaves / NWAVES);
+  const dim3 list_grid(kValueListWaves / NWAVES);
   // row indices are below 2^31: the sentinel never occurs
   e = list_pieces(rows_sorted, M, 0xFFFFFFFFu, list, counts, lws, s);
   if (e != hipSuccess) return e;
