@@ -750,14 +750,59 @@ __global__ __launch_bounds__(THREADS) void key_bwd_seg_kernel(
   const int width = dk / rank;
   const int n_e = pe - ps;
   const uint32_t my_slot = lane < n_e ? slots[ps + lane] : 0u;   // one entry per lane
+  const bool whole = run_start && run_end;
+  float* const part_row = partial + (static_cast<size_t>(2) * g + (run_start ? 1 : 0)) * dk;
+  if (dk <= 2 * kWave && (dk & (dk - 1)) == 0) {
+    // Rows of at most 128 dims fill a fraction of the wave: G = dk / 4 lanes take one entry, and
+    // the wave's S = 64 / G lane groups take entries s, s + S, s + 2 S, ... of the piece, each
+    // group in order; the groups' sums then meet by a fixed butterfly of shuffles.
+    const int G = dk / 4, S = kWave / G;
+    const int sub = lane / G, d = (lane % G) * 4;
+    const int r = d / width;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const f32x4 old = (whole && sub == 0) ? *reinterpret_cast<const f32x4*>(dK + d) : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j0 = 0; j0 < n_e; j0 += S * kInFlight) {   // wave-uniform
+      f32x4 qv[kInFlight];
+      float ds[kInFlight];
+#pragma unroll
+      for (int u = 0; u < kInFlight; ++u) {              // all loads first
+        const int j = j0 + S * u + sub;
+        const size_t slot = static_cast<uint32_t>(__shfl(static_cast<int>(my_slot), min(j, n_e - 1), kWave));
+        const size_t t = slot / (static_cast<size_t>(2) * H * m);
+        qv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        ds[u] = 0.0f;
+        if (j < n_e) {
+          qv[u] = *reinterpret_cast<const f32x4*>(q + (t * H + h) * dk + d);
+          ds[u] = edS[slot * rank + r];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kInFlight; ++u) {              // then this group's entries in order
+        acc.x = fmaf(ds[u], qv[u].x, acc.x);
+        acc.y = fmaf(ds[u], qv[u].y, acc.y);
+        acc.z = fmaf(ds[u], qv[u].z, acc.z);
+        acc.w = fmaf(ds[u], qv[u].w, acc.w);
+      }
+    }
+    for (int off = G; off < kWave; off <<= 1) {
+      acc.x += __shfl_xor(acc.x, off, kWave);
+      acc.y += __shfl_xor(acc.y, off, kWave);
+      acc.z += __shfl_xor(acc.z, off, kWave);
+      acc.w += __shfl_xor(acc.w, off, kWave);
+    }
+    if (sub == 0) {
+      if (whole) *reinterpret_cast<f32x4*>(dK + d) = old + acc;
+      else *reinterpret_cast<f32x4*>(part_row + d) = acc;
+    }
+    continue;
+  }
   for (int d0 = 0; d0 < dk; d0 += kWave * 4) {
     const int d = d0 + lane * 4;
     const bool active = d < dk;
     const int r = active ? d / width : 0;             // four consecutive dims lie in one slice
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     // a whole run adds into its key's gradient row: read it now, under the entries' loads
-    const f32x4 old = (active && run_start && run_end) ? *reinterpret_cast<const f32x4*>(dK + d)
-                                                       : f32x4{0.f, 0.f, 0.f, 0.f};
+    const f32x4 old = (active && whole) ? *reinterpret_cast<const f32x4*>(dK + d) : f32x4{0.f, 0.f, 0.f, 0.f};
     for (int j0 = 0; j0 < n_e; j0 += 2 * kInFlight) {  // wave-uniform
       f32x4 qv[2 * kInFlight];
       float ds[2 * kInFlight];
@@ -783,11 +828,8 @@ __global__ __launch_bounds__(THREADS) void key_bwd_seg_kernel(
       }
     }
     if (!active) continue;
-    if (run_start && run_end) {
-      *reinterpret_cast<f32x4*>(dK + d) = old + acc;
-    } else {
-      *reinterpret_cast<f32x4*>(partial + (static_cast<size_t>(2) * g + (run_start ? 1 : 0)) * dk + d) = acc;
-    }
+    if (whole) *reinterpret_cast<f32x4*>(dK + d) = old + acc;
+    else *reinterpret_cast<f32x4*>(part_row + d) = acc;
   }
   }
 }
