@@ -676,6 +676,49 @@ __global__ __launch_bounds__(score_bwd_waves<NG>() * kWave) void score_bwd_kerne
     const float* Kh = (a ? k_col : k_row) + static_cast<size_t>(h) * n * dk;
     float* dq = (a ? dq_col : dq_row) + th * dk;
     const int nk = nd[a];
+    if (dk % 4 == 0 && (dk > 2 * kWave || (dk & (dk - 1)) == 0) &&
+        (reinterpret_cast<uintptr_t>(dq) & 15u) == 0) {
+      // four dims per lane (16-byte loads); rows of at most 128 dims take S = 64 / (dk / 4) keys
+      // per load, lane group s summing keys s, s + S, ... in order, the groups then meeting by a
+      // fixed butterfly of shuffles; wider rows go in passes of 256 dims, each lane's sum in key
+      // order
+      const int G = dk <= 2 * kWave ? dk / 4 : kWave, S = kWave / G;
+      const int sub = lane / G;
+      for (int d0 = 0; d0 < dk; d0 += 4 * G) {
+        const int e = d0 + (lane % G) * 4;
+        const bool active = e < dk;
+        const int r = active ? e / width : 0;         // four consecutive dims lie in one slice
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int k0 = 0; k0 < nk; k0 += 4 * S) {      // four 16-byte loads in flight per lane
+          f32x4 kv[4];
+          float sd[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int k = k0 + S * u + sub;
+            const bool ok = active && k < nk;
+            kv[u] = ok ? *reinterpret_cast<const f32x4*>(Kh + static_cast<size_t>(sh.dist[a][k]) * dk + e)
+                       : f32x4{0.f, 0.f, 0.f, 0.f};
+            sd[u] = ok ? sh.sd[a][k][r] : 0.0f;
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (k0 + S * u >= nk) break;              // wave-uniform: no key for any group
+            acc.x = fmaf(sd[u], kv[u].x, acc.x);
+            acc.y = fmaf(sd[u], kv[u].y, acc.y);
+            acc.z = fmaf(sd[u], kv[u].z, acc.z);
+            acc.w = fmaf(sd[u], kv[u].w, acc.w);
+          }
+        }
+        for (int off = G; off < kWave; off <<= 1) {
+          acc.x += __shfl_xor(acc.x, off, kWave);
+          acc.y += __shfl_xor(acc.y, off, kWave);
+          acc.z += __shfl_xor(acc.z, off, kWave);
+          acc.w += __shfl_xor(acc.w, off, kWave);
+        }
+        if (sub == 0 && active) *reinterpret_cast<f32x4*>(dq + e) = acc;
+      }
+      continue;
+    }
     for (int e = lane; e < dk; e += kWave) {
       const int r = e / width;
       float acc = 0.0f;
