@@ -320,7 +320,7 @@ __global__ __launch_bounds__(THREADS) void gather_bwd_seg_kernel(
         wt[u] = 0.0f;
 #pragma unroll
         for (int k = 0; k < EPC / 4; ++k) v[u][k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (active) {
+        if (active && j0 + u < n_e) {                // (past the piece's end: no loads)
           wt[u] = w[static_cast<size_t>(ent[u]) * cores + sl];
           const f32x4* src = reinterpret_cast<const f32x4*>(d_pooled + static_cast<size_t>(prow) * dv + col);
 #pragma unroll
@@ -856,7 +856,7 @@ __global__ __launch_bounds__(THREADS) void key_bwd_seg_kernel(
         const size_t t = slot / (static_cast<size_t>(2) * H * m);
         qv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
         ds[u] = 0.0f;
-        if (active) {
+        if (active && j0 + u < n_e) {                 // (past the piece's end: no loads)
           qv[u] = *reinterpret_cast<const f32x4*>(q + (t * H + h) * dk + d);
           ds[u] = edS[slot * rank + r];
         }
