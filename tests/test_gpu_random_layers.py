@@ -97,13 +97,15 @@ def test_random_layer(i):
 @pytest.mark.parametrize("i", range(0, N_CASES, 2))
 def test_random_layer_backward(i):
     """The backward of every other random layer at the GPU forward's own selection, against the
-    backward oracle: the value-row and weight gradients (eqs. (1), (15), (17) differentiated),
-    then the query, key and core gradients (eqs. (2)-(4), (10), (16) differentiated)."""
+    backward oracle: the value-row and weight gradients (eqs. (1), (15), (17) differentiated, in
+    the dense and the compact form), then the query, key and core gradients (eqs. (2)-(4), (10),
+    (16) differentiated)."""
     import torch
     import oracle.backward_oracle as B
     from synth import device as SD
     from tests import gpu_util as G
-    from tests.test_gpu_backward import RTOL, rel, run_gather_backward, run_score_backward
+    from tests.test_gpu_backward import (RTOL, rel, run_gather_backward, run_gather_backward_rows,
+                                         run_score_backward)
     cfg = random_layer(i)
     print(f"[case] random backward {cfg}", flush=True)
     dl = SD.make_layer(cfg)
@@ -117,6 +119,10 @@ def test_random_layer_backward(i):
     dw_g = run_gather_backward(cfg.n_values, cfg.dv, cfg.vdtype, dl.values, T, cfg.bag,
                                idx.reshape(T, cfg.bag), w.reshape(wshape), dl.perm, cfg.expand,
                                cfg.cores, torch.from_numpy(dp).cuda(), dV)
+    # b1 in compact form: the distinct rows, each equal bit for bit to the dense (zeroed) row
+    rows_c, d_rows, n_rows, dw_c = run_gather_backward_rows(
+        cfg.n_values, cfg.dv, cfg.vdtype, dl.values, T, cfg.bag, idx.reshape(T, cfg.bag),
+        w.reshape(wshape), dl.perm, cfg.expand, cfg.cores, torch.from_numpy(dp).cuda())
     # b2: queries, keys, core
     dw_s = rng.standard_normal(tuple(w.shape)).astype(np.float32)
     dq_row, dq_col, dk_row, dk_col, dcore = run_score_backward(cfg, dl, idx, w, torch.from_numpy(dw_s).cuda())
@@ -126,6 +132,9 @@ def test_random_layer_backward(i):
                                              w_h.reshape(wshape), dp, CF.perm(cfg), cfg.n_values,
                                              cfg.expand)
     errs = dict(dV=rel(G.host(dV)[rows], dV_ref), dw=rel(G.host(dw_g), dw_ref))
+    n = int(n_rows.item())
+    assert n == len(rows) and np.array_equal(rows_c[:n].cpu().numpy(), np.sort(rows))
+    assert torch.equal(d_rows[:n], dV[rows_c[:n].long()]) and torch.equal(dw_c, dw_g)
     qr, qc = CF.queries(cfg)
     kr, kc = CF.keys(cfg)
     core = CF.core(cfg)
