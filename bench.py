@@ -908,8 +908,9 @@ def main():
                    "n_keys": cfg.n_keys, "slots": cfg.n_slots, "dv": cfg.dv, "values": "bf16",
                    "topk": cfg.topk, "topm": cfg.topm, "query_batches": args.batches,
                    "launch": "eager" if args.eager else "hip-graph",
-                   "timed_region": "cold rows: 1 GiB device copy before the timed replay, a "
-                                   "distinct query batch per step",
+                   "timed_region": (f"{WARM_SECONDS:g} s of untimed replays of the same steps, then "
+                                    "cold rows: 1 GiB device copy before the timed replay, a "
+                                    "distinct query batch per step"),
                    "inputs": INPUTS},
         "roofline": roofline_for(cfg, cfg.T, dominant, stage_us[dominant], cfg.name, fused),
         "step_roofline": dict(algorithmic_bytes=step_bytes, GBps=round(step_bytes / (ms * 1e-3) / 1e9, 1),
