@@ -4,11 +4,13 @@
 // w_e d_pooled[t_e, p_e].
 //
 // The T * bag entries are keyed by physical row and stably sorted (sort.hip), so the entries of
-// one row form a run in their original order.  The first wave of each run reads V[row] once,
-// 16 bytes per lane at a time, and for each entry of the run in order computes its weight
-// gradient (a wave reduction per core) and adds w_e d_pooled into an fp32 accumulator; then it
-// adds the accumulator into dV[row].  Every row has one writer and a fixed summation order: the
-// result does not depend on timing, and no atomics are needed.
+// one row form a run in their original order.  Runs are cut into pieces of at most 64 entries;
+// a wave takes a piece, reads V[row] 16 bytes per lane at a time, and for each entry of the
+// piece in order computes its weight gradient (a wave reduction per core) and adds w_e d_pooled
+// into an fp32 accumulator, which it adds into dV[row] (a whole run) or stores as a partial row
+// that a second pass adds in order.  Every row has one writer and a fixed summation order: the
+// result does not depend on timing, and no atomics are needed.  The compact form writes one
+// gradient row per run (distinct row) from zero instead of adding into a dense table.
 //
 // Backward of the scores (eqs. (2)-(4), (10), (16)) with the selection held fixed: one wave
 // per (token, head) turns the weight gradients into grid-score gradients (SoftMax Jacobian where
@@ -17,8 +19,9 @@
 // dS_row / dS_col and to dC, adds the contributions of slots that share a row (or column) in
 // slot order, and writes dq = sum_i dS[i] K[i].  The key
 // gradients dK[i] += dS[i] q are sums over tokens: each (token, head, axis) emits one entry per
-// distinct key, the entries are stably sorted by key, and one wave per key sums them in order.
-// dC sums its per-token partials in a fixed order (per thread, then a tree over the threads).
+// distinct key, the entries are stably sorted by key, and the key's pieces are summed in a fixed
+// order as above.  dC sums its per-token partials in a fixed order (per thread, then a tree over
+// the threads).
 #include <algorithm>
 
 #include "umem_internal.h"
