@@ -85,3 +85,27 @@ def test_decode_select_roofline_bytes():
     assert r["algorithmic_bytes"] == 2_179_072
     assert r["achieved"] == pytest.approx(2_179_072 / 10e-6 / 1e9, rel=1e-3)
     assert r["intermediate_bytes"] == 2_293_760
+
+
+def test_warm_replays_until_the_time_has_passed():
+    # the untimed warm-up before each timed region: at least one replay, and replays (each
+    # followed by a device synchronisation) until the given wall time has passed
+    import time as _time
+
+    class _Cuda:
+        syncs = 0
+
+        @classmethod
+        def synchronize(cls):
+            cls.syncs += 1
+
+    class _Torch:
+        cuda = _Cuda
+
+    calls = []
+    bench.warm(lambda: calls.append(1), _Torch, 0.0)
+    assert len(calls) == 1 and _Cuda.syncs == 1
+    t0 = _time.perf_counter()
+    bench.warm(lambda: (calls.append(1), _time.sleep(0.002)), _Torch, 0.02)
+    assert _time.perf_counter() - t0 >= 0.02
+    assert len(calls) >= 1 + 5 and _Cuda.syncs == len(calls)
