@@ -148,24 +148,44 @@ __device__ __forceinline__ uint32_t block_prefix(uint32_t v, uint32_t* lds, uint
   return incl - v;
 }
 
+// A run of the sorted keys starts here (the compact row output numbers runs, not rows).
+__device__ __forceinline__ bool is_run_start(const uint32_t* __restrict__ keys, int i, int M) {
+  return i < M && (i == 0 || keys[i - 1] != keys[i]);
+}
+
+// Per chunk of kListChunk positions: its piece starts into offs[chunk] and, with runs wanted, its
+// run starts into offs[chunks + chunk]; one exclusive scan over both halves follows.
 __global__ __launch_bounds__(THREADS) void piece_count_kernel(const uint32_t* __restrict__ keys,
                                                               int M, uint32_t sentinel,
-                                                              uint32_t* __restrict__ offs) {
+                                                              uint32_t* __restrict__ offs,
+                                                              int runs) {
   __shared__ uint32_t lds[THREADS];
   const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
-  uint32_t c = 0;
-  for (int k = 0; k < kListPer; ++k) c += is_piece_start(keys, beg + k, M, sentinel);
+  uint32_t c = 0, cr = 0;
+  for (int k = 0; k < kListPer; ++k) {
+    c += is_piece_start(keys, beg + k, M, sentinel);
+    if (runs) cr += is_run_start(keys, beg + k, M);
+  }
   uint32_t total;
   block_prefix(c, lds, &total);
   if (threadIdx.x == 0) offs[blockIdx.x] = total;
+  if (runs) {
+    block_prefix(cr, lds, &total);
+    if (threadIdx.x == 0) offs[gridDim.x + blockIdx.x] = total;
+  }
 }
 
-// offs: the chunks' exclusive offsets; the last chunk also stores the number of pieces.
+// offs: the scanned counts.  Writes the piece starts in order into list, their number into
+// counts[0] (counts[1] cleared); with run_of given also every position's run number, each run's
+// key into rows_out[run] (ascending) and the number of runs into *n_runs.
 __global__ __launch_bounds__(THREADS) void piece_write_kernel(const uint32_t* __restrict__ keys,
                                                               int M, uint32_t sentinel,
                                                               const uint32_t* __restrict__ offs,
                                                               uint32_t* __restrict__ list,
-                                                              uint32_t* __restrict__ counts) {
+                                                              uint32_t* __restrict__ counts,
+                                                              uint32_t* __restrict__ run_of,
+                                                              int32_t* __restrict__ rows_out,
+                                                              int32_t* __restrict__ n_runs) {
   __shared__ uint32_t lds[THREADS];
   const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
   uint32_t c = 0;
@@ -178,76 +198,41 @@ __global__ __launch_bounds__(THREADS) void piece_write_kernel(const uint32_t* __
     counts[0] = offs[blockIdx.x] + total;
     counts[1] = 0u;                                       // the spanning runs, appended later
   }
+  if (run_of == nullptr) return;                          // (uniform over the grid)
+  uint32_t cr = 0;
+  for (int k = 0; k < kListPer; ++k) cr += is_run_start(keys, beg + k, M);
+  const uint32_t pieces = offs[gridDim.x];                // the scan's offset of the run half
+  uint32_t total_r;
+  uint32_t r = offs[gridDim.x + blockIdx.x] - pieces + block_prefix(cr, lds, &total_r);
+  for (int k = 0; k < kListPer && beg + k < M; ++k) {
+    if (is_run_start(keys, beg + k, M)) rows_out[r++] = static_cast<int32_t>(keys[beg + k]);
+    run_of[beg + k] = r - 1;                              // position 0 starts a run: r >= 1 here
+  }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0)
+    *n_runs = static_cast<int32_t>(offs[gridDim.x + blockIdx.x] - pieces + total_r);
 }
 
 size_t list_workspace_bytes(int M) {
   const size_t chunks = (static_cast<size_t>(M) + kListChunk - 1) / kListChunk;
-  return (chunks + 1) * sizeof(uint32_t) + scan_workspace_bytes(static_cast<int>(chunks)) + 64;
+  return (2 * chunks + 1) * sizeof(uint32_t) + scan_workspace_bytes(static_cast<int>(2 * chunks)) + 64;
 }
 
 // The piece starts of the sorted keys into list (in order) and their number into counts[0];
-// counts[1] cleared.  ws: list_workspace_bytes(M).
+// counts[1] cleared.  With run_of given (keys without the sentinel), also the runs as
+// piece_write_kernel states.  ws: list_workspace_bytes(M).
 hipError_t list_pieces(const uint32_t* keys, int M, uint32_t sentinel, uint32_t* list,
-                       uint32_t* counts, void* ws, hipStream_t s) {
+                       uint32_t* counts, void* ws, hipStream_t s, uint32_t* run_of = nullptr,
+                       int32_t* rows_out = nullptr, int32_t* n_runs = nullptr) {
   const int chunks = (M + kListChunk - 1) / kListChunk;
+  const int runs = run_of != nullptr ? 1 : 0;
   uint32_t* offs = static_cast<uint32_t*>(ws);
-  uint32_t* sums = offs + chunks + 1;
-  hipLaunchKernelGGL(piece_count_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, sentinel, offs);
-  hipError_t e = scan_exclusive(offs, chunks, sums, s);
+  uint32_t* sums = offs + 2 * chunks + 1;
+  hipLaunchKernelGGL(piece_count_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, sentinel, offs,
+                     runs);
+  hipError_t e = scan_exclusive(offs, (1 + runs) * chunks, sums, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(piece_write_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, sentinel, offs,
-                     list, counts);
-  return hipGetLastError();
-}
-
-// Compact row output: run r of the sorted keys (the r-th distinct row, ascending) gets slot r.
-// Per chunk of kListChunk positions the run starts are counted, the counts scanned, then every
-// position's run number written (run_of), each run's row into rows_out[r], and the number of
-// runs into *n_runs.
-__device__ __forceinline__ bool is_run_start(const uint32_t* __restrict__ keys, int i, int M) {
-  return i < M && (i == 0 || keys[i - 1] != keys[i]);
-}
-
-__global__ __launch_bounds__(THREADS) void run_count_kernel(const uint32_t* __restrict__ keys, int M,
-                                                            uint32_t* __restrict__ offs) {
-  __shared__ uint32_t lds[THREADS];
-  const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
-  uint32_t c = 0;
-  for (int k = 0; k < kListPer; ++k) c += is_run_start(keys, beg + k, M);
-  uint32_t total;
-  block_prefix(c, lds, &total);
-  if (threadIdx.x == 0) offs[blockIdx.x] = total;
-}
-
-__global__ __launch_bounds__(THREADS) void run_write_kernel(const uint32_t* __restrict__ keys, int M,
-                                                            const uint32_t* __restrict__ offs,
-                                                            uint32_t* __restrict__ run_of,
-                                                            int32_t* __restrict__ rows_out,
-                                                            int32_t* __restrict__ n_runs) {
-  __shared__ uint32_t lds[THREADS];
-  const int beg = blockIdx.x * kListChunk + threadIdx.x * kListPer;
-  uint32_t c = 0;
-  for (int k = 0; k < kListPer; ++k) c += is_run_start(keys, beg + k, M);
-  uint32_t total;
-  uint32_t at = offs[blockIdx.x] + block_prefix(c, lds, &total);   // runs started before beg
-  for (int k = 0; k < kListPer && beg + k < M; ++k) {
-    if (is_run_start(keys, beg + k, M)) rows_out[at++] = static_cast<int32_t>(keys[beg + k]);
-    run_of[beg + k] = at - 1;                         // position 0 starts a run: at >= 1 here
-  }
-  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *n_runs = static_cast<int32_t>(offs[blockIdx.x] + total);
-}
-
-// run_of / rows_out / *n_runs of the sorted keys (no sentinel).  ws: list_workspace_bytes(M).
-hipError_t index_runs(const uint32_t* keys, int M, uint32_t* run_of, int32_t* rows_out,
-                      int32_t* n_runs, void* ws, hipStream_t s) {
-  const int chunks = (M + kListChunk - 1) / kListChunk;
-  uint32_t* offs = static_cast<uint32_t*>(ws);
-  uint32_t* sums = offs + chunks + 1;
-  hipLaunchKernelGGL(run_count_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, offs);
-  hipError_t e = scan_exclusive(offs, chunks, sums, s);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(run_write_kernel, dim3(chunks), dim3(THREADS), 0, s, keys, M, offs, run_of,
-                     rows_out, n_runs);
+                     list, counts, run_of, rows_out, n_runs);
   return hipGetLastError();
 }
 
@@ -951,13 +936,10 @@ hipError_t launch_gather_backward(int64_t n_values, int dv, int vdtype, const vo
   const int c = cores > 1 ? cores : 1;
   const dim3 list_grid(kValueListWaves / NWAVES);
   // row indices are below 2^31: the sentinel never occurs
-  e = list_pieces(rows_sorted, M, 0xFFFFFFFFu, list, counts, lws, s);
-  if (e != hipSuccess) return e;
   const bool compact = rows_out != nullptr;
-  if (compact) {                                      // (reuses the list's scratch, now free)
-    e = index_runs(rows_sorted, M, run_of, rows_out, n_rows, lws, s);
-    if (e != hipSuccess) return e;
-  }
+  e = list_pieces(rows_sorted, M, 0xFFFFFFFFu, list, counts, lws, s, compact ? run_of : nullptr,
+                  rows_out, n_rows);
+  if (e != hipSuccess) return e;
   const uint32_t* ro = compact ? run_of : nullptr;
   if (vdtype == UMEM_F32)
     hipLaunchKernelGGL(gather_bwd_seg_kernel<float>, list_grid, dim3(THREADS), 0, s, rows_sorted,
