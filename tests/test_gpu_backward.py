@@ -251,16 +251,29 @@ SCORE_CASES = [
              vdtype=CF.F32, seed=62),
     CF.Layer("tucker-h64", T=3, heads=64, dk=64, n_keys=128, topk=16, topm=32, dv=8, vdtype=CF.F32,
              seed=63, rank=2, grid=CF.GRID_TUCKER),
+    # key rows of 4 and 8 dims (64 and 32 key entries per wave in the key gradients and dq), and
+    # the paper's Kdim 448 (dq in passes of 256 dims)
+    CF.Layer("add-dk4", T=30, heads=2, dk=4, n_keys=40, topk=6, topm=10, dv=8, vdtype=CF.F32, seed=64),
+    CF.Layer("tucker-dk8", T=25, heads=2, dk=8, n_keys=48, topk=8, topm=16, dv=8, vdtype=CF.F32,
+             seed=65, rank=2, grid=CF.GRID_TUCKER),
+    CF.Layer("tucker-dk448", T=12, heads=2, dk=448, n_keys=96, topk=14, topm=42, dv=8,
+             vdtype=CF.F32, seed=66, rank=2, grid=CF.GRID_TUCKER, cores=2),
 ]
 
 
-def run_score_backward(cfg, dl, idx, w, dw, dk_init=None, dc_init=None):
+SCORE_CASE = {c.name: c for c in SCORE_CASES}
+
+
+def run_score_backward(cfg, dl, idx, w, dw, dk_init=None, dc_init=None, dq_offset=0):
+    """dq_offset: floats by which dq_row and dq_col start past a 256-byte boundary (the API asks
+    4-byte alignment of them only)."""
     d = G.desc_for(cfg)
     st, nws = U.umem_score_backward_workspace_size(d, cfg.T)
     U.check(st)
     ws = torch.empty(max(nws, 256), dtype=torch.uint8, device="cuda")
-    dq_row = torch.empty_like(dl.q_row[0])
-    dq_col = torch.empty_like(dl.q_col[0])
+    nq = dl.q_row[0].numel()
+    dq_row = torch.empty(nq + dq_offset, dtype=torch.float32, device="cuda")[dq_offset:].view_as(dl.q_row[0])
+    dq_col = torch.empty(nq + dq_offset, dtype=torch.float32, device="cuda")[dq_offset:].view_as(dl.q_col[0])
     dk_row = torch.zeros_like(dl.k_row) if dk_init is None else dk_init[0].clone()
     dk_col = torch.zeros_like(dl.k_col) if dk_init is None else dk_init[1].clone()
     dcore = None
@@ -299,8 +312,26 @@ def test_score_backward(cfg):
     assert max(errs.values()) <= RTOL, errs
 
 
+@pytest.mark.parametrize("offset", [1, 2])
+def test_score_backward_dq_unaligned(offset):
+    """dq rows that are 4-byte but not 16-byte aligned take the one-dim-per-lane form of dq: the
+    same result, to the tolerance, as the 16-byte form on aligned rows."""
+    cfg = SCORE_CASE["tucker"]                                     # Tucker, Dk = 64
+    dl = SD.make_layer(cfg)
+    idx, w, _ = G.score_topk(dl, cfg.T, 0)
+    rng = np.random.default_rng(7)
+    dw = torch.from_numpy(rng.standard_normal(tuple(w.shape)).astype(np.float32)).cuda()
+    a = run_score_backward(cfg, dl, idx, w, dw)
+    b = run_score_backward(cfg, dl, idx, w, dw, dq_offset=offset)
+    torch.cuda.synchronize()
+    assert b[0].data_ptr() % 16 != 0
+    for x, y in zip(a[:4], b[:4]):
+        assert rel(G.host(y), G.host(x)) <= RTOL
+    assert torch.equal(a[2], b[2]) and torch.equal(a[3], b[3])      # dK does not involve dq
+
+
 def test_score_backward_deterministic():
-    cfg = SCORE_CASES[-1]
+    cfg = SCORE_CASE["tucker-h64"]
     dl = SD.make_layer(cfg)
     idx, w, _ = G.score_topk(dl, cfg.T, 0)
     dw = torch.randn_like(w)
@@ -315,7 +346,7 @@ def test_backward_graph_replay_matches_eager():
     """Both backward entry points captured in a HIP graph (with the clearing of their accumulated
     outputs by fill kernels), replayed several times with eager work in between, give the eager
     results bit for bit: their piece counters and lists are rebuilt by kernels on every call."""
-    cfg = SCORE_CASES[-1]                  # Tucker r = 4, 64 slots, rows shared by many tokens
+    cfg = SCORE_CASE["tucker-h64"]        # Tucker r = 2, 64 heads, rows shared by many tokens
     dl = SD.make_layer(cfg)
     idx, w, _ = G.score_topk(dl, cfg.T, 0)
     torch.cuda.synchronize()
