@@ -167,12 +167,14 @@ __global__ __launch_bounds__(kThreads) void sort_scatter_kernel(
     }
     __syncthreads();
     // the digit's running offset takes every wave's count (LDS atomics: an integer sum, exact in
-    // any order); each post is cleared by the wave that made it
+    // any order); each post is cleared by the wave that made it.  No barrier is needed before the
+    // next step: every read of this step's offsets and posts came before the barrier above, the
+    // next step's posts go to the posting wave's own row (after its own clears, in program
+    // order), and the next step reads offsets and posts only after its own first barrier.
     if (leader) {
       atomicAdd(&base[digit], here);
       wcnt[wave][digit] = 0;
     }
-    __syncthreads();
   }
 }
 
