@@ -155,10 +155,10 @@ def measured_traffic(name, workload):
 def layer_rules(cfg):
     """(project, fused) as the library decides them: a projection runs when D'v or d_out is set;
     the selection pools the rows itself for layers without expansion or projection, at most two
-    heads, topm <= 64, rows of 1 or 2 KiB and T <= 512."""
+    heads, topm <= 64, rows of 1 or 2 KiB and T <= 128."""
     project = bool(cfg.dv_virt or cfg.d_out)
     fused = (not project and cfg.expand == 1 and cfg.heads <= 2 and cfg.topm <= 64
-             and cfg.dv * cfg.vbytes in (1024, 2048) and cfg.T <= 512)
+             and cfg.dv * cfg.vbytes in (1024, 2048) and cfg.T <= 128)
     return project, fused
 
 

@@ -133,7 +133,7 @@ UMEM_API umem_status umem_axis_scores(const umem_desc* desc, int32_t T, const fl
  *             layers without expansion, with heads <= 2, topm <= 64 and value rows of 1 or
  *             2 KiB (UMEM_ERR_UNSUPPORTED otherwise); with two heads the result does not depend
  *             on their order (two adds onto zero commute exactly).  umem_forward uses this form
- *             where it applies and T <= 512, instead of a separate gather launch. */
+ *             where it applies and T <= 128, instead of a separate gather launch. */
 UMEM_API umem_status umem_select(const umem_desc* desc, int32_t T, const float* sel, const float* q_row,
                         const float* q_col, const float* k_row, const float* k_col,
                         const float* core, int32_t* idx, float* w, int32_t* axis_idx,

@@ -15,7 +15,7 @@ constexpr int kMaxTopKTucker = 64;   // Tucker: the k*k candidate keys in 16 KiB
 constexpr int kMaxTopM = 256;
 constexpr int kMaxCores = 8;          // multi-core scoring: component cores per head
 constexpr int kMaxPoolTopM = 64;      // the selection kernel pools rows itself up to this topm
-constexpr int kMaxPoolTokens = 512;   // ... and umem_forward lets it up to this many tokens
+constexpr int kMaxPoolTokens = 128;   // ... and umem_forward lets it up to this many tokens
 constexpr int kMaxRank = 4;
 constexpr int kMaxBag = 2048;
 constexpr int kMaxTokens = 1 << 20;

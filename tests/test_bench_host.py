@@ -44,10 +44,11 @@ def test_decode_method_bytes_by_hand():
 
 def test_layer_rules():
     # (project, fused): the selection pools only without projection or expansion, at most two
-    # heads, m <= 64, rows of 1 or 2 KiB and T <= 512
+    # heads, m <= 64, rows of 1 or 2 KiB and T <= 128
     assert bench.layer_rules(CF.C3) == (False, True)
     assert bench.layer_rules(CF.C2) == (False, False)          # 2048 tokens
-    assert bench.layer_rules(CF.C2.with_tokens(512)) == (False, True)
+    assert bench.layer_rules(CF.C2.with_tokens(128)) == (False, True)
+    assert bench.layer_rules(CF.C2.with_tokens(129)) == (False, False)
     assert bench.layer_rules(CF.C5) == (True, False)
     assert bench.layer_rules(CF.C6) == (True, False)
 

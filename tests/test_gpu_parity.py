@@ -172,12 +172,12 @@ def test_edge_shapes(kw):
     # 64 heads (one factor pair each), the Tucker grid
     dict(T=3, heads=64, dk=64, n_keys=128, rank=2, grid=CF.GRID_TUCKER, topk=16, topm=32, dv=64,
          vdtype=CF.BF16),
-    # the selection pooling the rows itself at its limits: 512 tokens, m = 64, rows of 2 KiB
-    dict(T=512, heads=2, dk=128, n_keys=256, topk=32, topm=64, dv=1024, vdtype=CF.BF16),
+    # the selection pooling the rows itself at its limits: 128 tokens, m = 64, rows of 2 KiB
+    dict(T=128, heads=2, dk=128, n_keys=256, topk=32, topm=64, dv=1024, vdtype=CF.BF16),
     # n not a multiple of 4 at the largest per-thread share: 32 keys per thread and axis
     dict(T=2, heads=1, dk=64, n_keys=8191, topk=32, topm=32, dv=8, vdtype=CF.BF16),
 ], ids=["n-8192-k-90-m-256", "k-70-m-256", "dk-1024-rank-4", "bag-2048-rows-8KiB",
-        "tucker-k-64-E-64-h-8", "heads-64", "pooled-T-512-m-64-2KiB", "n-8191"])
+        "tucker-k-64-E-64-h-8", "heads-64", "pooled-T-128-m-64-2KiB", "n-8191"])
 def test_library_limits(kw):
     cfg = small("limit", **kw)
     run_and_check(cfg, tokens=None if cfg.T <= 64 else np.arange(0, cfg.T, 7))
@@ -596,10 +596,9 @@ def test_c3_decode_20m_full_size(c3_values):
 
 @pytest.mark.parametrize("T", CF.C4_BATCHES)
 def test_c4_decode_batches(T, c3_values):
-    """The decode batch sweep on the 20.07M-slot layer.  Up to 512 tokens the selection pools the
-    rows itself (scoring clears the output first: the split, 32 x 32 and, above 64 tokens, the
-    fp16-plane kernel); at 1024 the gather kernel pools them.  Every token up to 256, 256 of
-    1024."""
+    """The decode batch sweep on the 20.07M-slot layer.  Up to 128 tokens the selection pools the
+    rows itself (scoring clears the output first: the split and the 32 x 32 kernel); at 256 and
+    1024 the gather kernel pools them.  Every token up to 256, 256 of 1024."""
     rng = np.random.default_rng(T)
     tokens = None if T <= 256 else np.sort(rng.choice(T, 256, replace=False))
     cfg = CF.C3.with_tokens(T)
@@ -608,11 +607,11 @@ def test_c4_decode_batches(T, c3_values):
 
 @pytest.mark.parametrize("n_keys", [300, 301], ids=["planes", "tiled"])
 def test_fused_forward_many_tokens(n_keys):
-    """The forward with the selection pooling the rows for 64 < T <= 512 tokens (two heads, 1 KiB
+    """The forward with the selection pooling the rows for 64 < T <= 128 tokens (two heads, 1 KiB
     bf16 rows, no projection): the scoring kernel, here the fp16-plane one (n % 4 == 0) or the
     tiled fp32 MFMA one (n % 4 != 0), clears the output with its grid before the selection adds
-    both heads' rows into it.  A ragged last token tile (130 = 128 + 2)."""
-    cfg = small("fused-many", T=130, heads=2, dk=128, n_keys=n_keys, topk=16, topm=24, dv=512,
+    both heads' rows into it.  A ragged token tile (100 of 128)."""
+    cfg = small("fused-many", T=100, heads=2, dk=128, n_keys=n_keys, topk=16, topm=24, dv=512,
                 vdtype=CF.BF16, seed=31)
     run_and_check(cfg)
 
